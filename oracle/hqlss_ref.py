@@ -1,0 +1,373 @@
+"""Plain CPU oracle of HQ-MM (forward) and LSS-MM (backward) of one linear layer.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may use this module.  It shares no code with the GPU library
+and imports nothing from it.
+
+Notation follows the paper ("Training Transformers with 4-bit Integers",
+arXiv 2306.11987): Y = X W^T with X: N x D, W: C x D (Sec. 3, Eq. 1); H_k the
+2^k x 2^k Hadamard matrix, H = BlockDiag(H_k, ..., H_k) (Sec. 3.3); INT4 codes
+in [-7, 7] (Sec. 3.1, Eq. 2, Q_N = Q_P = 7).
+
+Readings of the paper taken here (each is listed with its reason in the design
+notes of the repository):
+
+* H_u = 2^{k/2} H_k, the unnormalised +-1 Sylvester matrix, is applied by the
+  radix-2 fast transform, strides ascending, in float32 (the paper computes XH
+  in FP16 on its GPU).  The factor 2^{-k} is folded into the dequantisation
+  scale (H_u H_u^T = 2^k I).
+* Step sizes are dynamic per-tensor absmax scales s = max|v| / 7 (gradients are
+  quantised dynamically in Sec. 4; the learned static step size of Sec. 3.1 is
+  a separate mode).  Codes are round-half-even(v * fl(7/a)), clamped to +-7.
+* Bit splitting (Sec. 4.2, Eq. 4): upper codes round to nearest with
+  s_up = a/7; the residual is scaled by 14 and rounded stochastically, so that
+  s_dn = s_up / 14 and the pair is the integer 14*q_up + q_dn (the paper's
+  "INT8 representation").
+* Leverage scores (Sec. 4.2) are taken on the codes; one shared sample serves
+  both gradients (App. A.6: the activation gradient reuses the weight
+  gradient's quantisation and scores).  Inclusion probabilities follow the
+  clamp-and-rescale loop of App. A.2 in exact integers, then are rounded up to
+  powers of two (p~ = 2^-e >= p*), which keeps the estimator unbiased and lets
+  the weights 2^e enter one exact integer GEMM operand.
+* The gradients carry H^T along D (Sec. 4, the STE gradients): it is applied to
+  the integer GEMM results, before dequantisation.
+
+Everything that decides an integer (codes, stochastic rounding, samples) runs in
+float32 or exact integers exactly as the GPU must; the float outputs are
+formed in float64.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from .philox_ref import uniforms16
+
+QMAX = 7  # Q_N = Q_P = 7 (Sec. 3.1)
+BS_RATIO = 14  # s_up / s_dn (bit-split reading)
+STREAM_SR = 0  # Philox stream of the lower-half stochastic rounding
+STREAM_MASK = 1  # Philox stream of the LSS Bernoulli masks
+
+__all__ = [
+    "QMAX", "BS_RATIO", "fwht_rows", "hadamard_matrix_sylvester", "absmax", "quantize_int4",
+    "pack_int4", "unpack_int4", "HQForward", "hq_forward", "BitSplit", "bit_split",
+    "leverage_scores", "clamp_rescale", "LSSPlan", "lss_plan", "LSSBackward",
+    "lss_backward", "weighted_rows", "stochastic_round",
+]
+
+
+# --------------------------------------------------------------------------
+# Hadamard transform (Sec. 3.3)
+# --------------------------------------------------------------------------
+def fwht_rows(v: np.ndarray, log2_block: int) -> np.ndarray:
+    """Block-diagonal unnormalised Hadamard transform of every row: v @ BlockDiag(H_u).
+
+    H_k is defined by the Sylvester recursion H_k = [[H, H], [H, -H]] (Sec. 3.3,
+    here without the 1/sqrt(2) per level).  Applying the recursion level by
+    level gives the radix-2 butterfly (x[j], x[j+h]) <- (x[j]+x[j+h], x[j]-x[j+h])
+    for h = 1, 2, ..., b/2.  Float inputs are transformed in float32, integer
+    inputs in exact int64.
+    """
+    b = 1 << int(log2_block)
+    v = np.asarray(v)
+    R, D = v.shape
+    assert D % b == 0, "D must be a multiple of the block size (Sec. 3.3)"
+    x = v.astype(np.int64 if np.issubdtype(v.dtype, np.integer) else np.float32, copy=True)
+    h = 1
+    while h < b:
+        y = x.reshape(R, D // (2 * h), 2, h)
+        lo = y[:, :, 0, :].copy()
+        hi = y[:, :, 1, :].copy()
+        y[:, :, 0, :] = lo + hi
+        y[:, :, 1, :] = lo - hi
+        h *= 2
+    return x
+
+
+def hadamard_matrix_sylvester(log2_block: int) -> np.ndarray:
+    """H_u by the Sylvester recursion itself (used to check the fast transform)."""
+    H = np.ones((1, 1), dtype=np.int64)
+    for _ in range(int(log2_block)):
+        H = np.block([[H, H], [H, -H]])
+    return H
+
+
+# --------------------------------------------------------------------------
+# Quantiser (Sec. 3.1, Eq. 2)
+# --------------------------------------------------------------------------
+def absmax(v: np.ndarray) -> np.float32:
+    v = np.asarray(v, dtype=np.float32)
+    return np.float32(np.max(np.abs(v))) if v.size else np.float32(0.0)
+
+
+def quantize_int4(v: np.ndarray, a: np.float32):
+    """int_s(v) = round(clamp(v / s, -7, 7)) with s = a / 7 (Eq. 2).
+
+    The division by s is taken as a multiplication by inv = fl(7 / a), computed
+    once; rounding is half-to-even.  Returns (codes int8, s float32)."""
+    v = np.asarray(v, dtype=np.float32)
+    a = np.float32(a)
+    if a == 0:
+        return np.zeros(v.shape, dtype=np.int8), np.float32(0.0)
+    inv = np.float32(QMAX) / a
+    q = np.clip(np.rint(v * inv), -QMAX, QMAX).astype(np.int8)
+    s = a / np.float32(QMAX)
+    return q, s
+
+
+def pack_int4(q: np.ndarray) -> np.ndarray:
+    """Two codes per byte: (q[2i+1] << 4) | (q[2i] & 15) (App. A.6, data pack)."""
+    q = np.asarray(q).astype(np.int16)
+    assert q.shape[-1] % 2 == 0
+    lo = q[..., 0::2] & 15
+    hi = q[..., 1::2] & 15
+    return (lo | (hi << 4)).astype(np.uint8)
+
+
+def unpack_int4(p: np.ndarray) -> np.ndarray:
+    p = np.asarray(p, dtype=np.uint8).astype(np.int16)
+    lo = p & 15
+    hi = (p >> 4) & 15
+    lo = np.where(lo >= 8, lo - 16, lo)
+    hi = np.where(hi >= 8, hi - 16, hi)
+    out = np.empty(p.shape[:-1] + (p.shape[-1] * 2,), dtype=np.int8)
+    out[..., 0::2] = lo
+    out[..., 1::2] = hi
+    return out
+
+
+def _int_matmul(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Exact integer product a @ b.  float64 BLAS is exact here because every
+    partial sum stays far below 2^53 (|a|,|b| <= 126, K <= 2^20)."""
+    assert a.shape[1] < (1 << 20)
+    r = a.astype(np.float64) @ b.astype(np.float64)
+    return r.astype(np.int64)
+
+
+# --------------------------------------------------------------------------
+# HQ-MM forward (Sec. 3.3, Procedure HQ-MM)
+# --------------------------------------------------------------------------
+@dataclass
+class HQForward:
+    log2_block: int
+    amax_x: np.float32
+    amax_w: np.float32
+    s_x: np.float32
+    s_w: np.float32
+    xq: np.ndarray  # int8 [N][D] codes of X H_u
+    wq: np.ndarray  # int8 [C][D] codes of W H_u
+    x_sumsq: np.ndarray  # int64 [N]  sum_d xq^2
+    acc: np.ndarray = field(default=None)  # int64 [N][C]
+    Y: np.ndarray = field(default=None)  # float64 [N][C]
+
+
+def hq_forward(X: np.ndarray, W: np.ndarray, log2_block: int, compute_output: bool = True) -> HQForward:
+    """Steps of HQ-MM: (1) X H and H^T W^T; (2) quantise both to INT4;
+    (3) integer product; (4) dequantise by s_X s_W (and 2^-k, see module notes)."""
+    vx = fwht_rows(np.asarray(X, dtype=np.float32), log2_block)
+    vw = fwht_rows(np.asarray(W, dtype=np.float32), log2_block)
+    ax, aw = absmax(vx), absmax(vw)
+    xq, sx = quantize_int4(vx, ax)
+    wq, sw = quantize_int4(vw, aw)
+    x_sumsq = np.sum(xq.astype(np.int64) ** 2, axis=1)
+    out = HQForward(int(log2_block), ax, aw, sx, sw, xq, wq, x_sumsq)
+    if compute_output:
+        out.acc = _int_matmul(xq, wq.T)
+        out.Y = float(sx) * float(sw) * 2.0 ** (-int(log2_block)) * out.acc.astype(np.float64)
+    return out
+
+
+# --------------------------------------------------------------------------
+# Bit splitting (Sec. 4.2, Eq. 4)
+# --------------------------------------------------------------------------
+@dataclass
+class BitSplit:
+    amax: np.float32
+    s_up: np.float32
+    q_up: np.ndarray  # int8 [N][C]
+    q_dn: np.ndarray  # int8 [N][C]
+
+    @property
+    def s_dn(self) -> float:
+        return float(self.s_up) / BS_RATIO
+
+    def combined(self) -> np.ndarray:
+        """The integer 14 q_up + q_dn, i.e. dY / s_dn (the INT8 view)."""
+        return BS_RATIO * self.q_up.astype(np.int32) + self.q_dn.astype(np.int32)
+
+
+def stochastic_round(w: np.ndarray, u16: np.ndarray) -> np.ndarray:
+    """floor(w) + [u < frac(w) * 2^16] in float32, u uniform on 0..65535."""
+    w = np.asarray(w, dtype=np.float32)
+    fl = np.floor(w)
+    thr = (w - fl) * np.float32(65536.0)
+    return (fl + (u16.astype(np.float32) < thr)).astype(np.int8)
+
+
+def bit_split(G: np.ndarray, seed: int, offset: int) -> BitSplit:
+    """dY ~ s_up q_up + s_dn q_dn: quantise dY to INT4, then the residual (Sec. 4.2)."""
+    G = np.asarray(G, dtype=np.float32)
+    N, C = G.shape
+    a = absmax(G)
+    if a == 0:
+        z = np.zeros((N, C), dtype=np.int8)
+        return BitSplit(a, np.float32(0.0), z, z.copy())
+    inv = np.float32(QMAX) / a
+    v = G * inv
+    q_up = np.rint(v)  # |v| <= 7(1+2^-23): no clamp needed
+    r = v - q_up  # exact: |r| <= 1/2
+    w = np.float32(BS_RATIO) * r  # |w| <= 7
+    u = uniforms16(seed, offset, STREAM_SR, N * C).reshape(N, C)
+    q_dn = stochastic_round(w, u)
+    return BitSplit(a, a / np.float32(QMAX), q_up.astype(np.int8), q_dn)
+
+
+# --------------------------------------------------------------------------
+# Leverage score sampling (Sec. 4.2, App. A.2)
+# --------------------------------------------------------------------------
+def leverage_scores(sumsq_up: np.ndarray, sumsq_dn: np.ndarray, x_sumsq: np.ndarray) -> np.ndarray:
+    """Integer leverage scores of the 2N stacked rows [up rows; down rows].
+
+    c_i = ||grad_i|| ||X_i|| (Sec. 4.2) with grad rows s_up q_up and s_dn q_dn =
+    s_dn (14 q_up) and s_dn q_dn, and X rows taken as codes.  Dropping the common
+    factor s_dn s_x: c^2 = w^2 * sum q^2 * x_sumsq, w = 14 (up) or 1 (down).
+    Returned as isqrt(c^2 * 2^16), an exact integer (< 2^31 for the shapes here)."""
+    su = [int(v) for v in np.asarray(sumsq_up)]
+    sd = [int(v) for v in np.asarray(sumsq_dn)]
+    sx = [int(v) for v in np.asarray(x_sumsq)]
+    up = [math.isqrt(BS_RATIO * BS_RATIO * a * x << 16) for a, x in zip(su, sx)]
+    dn = [math.isqrt(a * x << 16) for a, x in zip(sd, sx)]
+    return np.array(up + dn, dtype=np.int64)
+
+
+def clamp_rescale(c: np.ndarray, budget: int):
+    """Inclusion probabilities p_i proportional to c_i with sum p_i = budget and
+    p_i <= 1, by the clamp-and-rescale loop of App. A.2, in exact integers.
+
+    Returns (clamped bool[2N], R, S) where rows with clamped=True have p = 1
+    and every other row has p = R * c_i / S (0 if c_i = 0).  When no more rows
+    than the budget have c_i > 0, every such row gets p = 1 (S = 0)."""
+    c = [int(v) for v in c]
+    nz = [v > 0 for v in c]
+    if sum(nz) <= budget:
+        return np.array(nz, dtype=bool), 0, 0
+    clamped = [False] * len(c)
+    k = 0
+    S = sum(c)
+    while True:
+        R = budget - k
+        new = [j for j, v in enumerate(c) if not clamped[j] and v > 0 and R * v >= S]
+        if not new:
+            break
+        for j in new:
+            clamped[j] = True
+        k += len(new)
+        S -= sum(c[j] for j in new)
+    return np.array(clamped, dtype=bool), budget - k, S
+
+
+@dataclass
+class LSSPlan:
+    budget: int
+    c: np.ndarray  # int64 [2N] scores
+    clamped: np.ndarray  # bool [2N]
+    R: int
+    S: int
+    e_dn: np.ndarray  # int [N] exponent of each down row (p~ = 2^-e)
+    w_up: np.ndarray  # int [N] in {0, 1}
+    w_dn: np.ndarray  # int [N] in {0, 1, 2, 4, 8, 16}
+    kept: np.ndarray  # int64 [T] ascending token indices with w_up + w_dn > 0
+
+    def p_dn(self) -> np.ndarray:
+        """Inclusion probability p~ of every down row (0 for rows never kept)."""
+        N = self.w_up.shape[0]
+        p = np.where(self.c[N:] > 0, 2.0 ** (-self.e_dn.astype(np.float64)), 0.0)
+        return p
+
+
+def lss_plan(sumsq_up, sumsq_dn, x_sumsq, budget: int, seed: int, offset: int,
+             u16_masks: np.ndarray = None) -> LSSPlan:
+    """Masks and weights of the shared sample (Sec. 4.2, App. A.2, App. A.6).
+
+    * up rows are always kept when non-zero (weight 1, p~ = 1);
+    * down rows get p~ = 2^-e, the smallest power of two >= p*, with e capped at 4
+      (at 2 when the token's up row is non-zero so |14 q_up + 2^e q_dn| <= 126);
+    * m ~ Bern(p~) from Philox stream 1 as [u16 < 2^(16-e)]; the weight m/p~ = m 2^e."""
+    N = len(sumsq_up)
+    c = leverage_scores(sumsq_up, sumsq_dn, x_sumsq)
+    clamped, R, S = clamp_rescale(c, budget)
+    su = np.asarray(sumsq_up, dtype=np.int64)
+    w_up = (su > 0).astype(np.int64)
+    e_dn = np.zeros(N, dtype=np.int64)
+    for t in range(N):
+        j = N + t
+        cj = int(c[j])
+        if cj == 0 or clamped[j]:
+            continue
+        cap = 2 if su[t] > 0 else 4
+        e = 0
+        while e < cap and (R * cj) << (e + 1) <= S:
+            e += 1
+        e_dn[t] = e
+    if u16_masks is None:
+        u16_masks = uniforms16(seed, offset, STREAM_MASK, N)
+    u = np.asarray(u16_masks).astype(np.int64)
+    m = u < (1 << (16 - e_dn))
+    w_dn = np.where((c[N:] > 0) & m, 1 << e_dn, 0).astype(np.int64)
+    kept = np.nonzero((w_up + w_dn) > 0)[0].astype(np.int64)
+    return LSSPlan(int(budget), c, clamped, int(R), int(S), e_dn, w_up, w_dn, kept)
+
+
+# --------------------------------------------------------------------------
+# LSS-MM backward (Sec. 4.2, App. A.3)
+# --------------------------------------------------------------------------
+@dataclass
+class LSSBackward:
+    bs: BitSplit
+    plan: LSSPlan
+    A: np.ndarray  # int32 [N][C] weighted integer gradient rows (0 for dropped tokens)
+    acc_dx: np.ndarray  # int64 [T][D]  A[kept] @ wq
+    acc_dw: np.ndarray  # int64 [C][D]  A[kept]^T @ xq[kept]
+    dX: np.ndarray  # float64 [N][D]
+    dW: np.ndarray  # float64 [C][D]
+    alpha_dx: float
+    alpha_dw: float
+
+
+def weighted_rows(bs: BitSplit, plan: LSSPlan) -> np.ndarray:
+    """Rows of (I~ M~ grad) in units of s_dn: 14 w_up q_up + w_dn q_dn per token."""
+    return (BS_RATIO * plan.w_up[:, None] * bs.q_up.astype(np.int64)
+            + plan.w_dn[:, None] * bs.q_dn.astype(np.int64))
+
+
+def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: int,
+                 need_dx: bool = True, need_dw: bool = True) -> LSSBackward:
+    """Activation and weight gradients of HQ-MM by LSS-MM.
+
+    grad_X = s_W (grad_Y W^) H^T and grad_W = s_X (grad_Y^T X^) H^T (Sec. 4; the
+    clip masks are identically 1 under absmax scales), with grad_Y replaced by
+    the sampled bit-split estimate s_dn * A (Sec. 4.2, App. A.3)."""
+    k = fwd.log2_block
+    bs = bit_split(G, seed, offset)
+    su = np.sum(bs.q_up.astype(np.int64) ** 2, axis=1)
+    sd = np.sum(bs.q_dn.astype(np.int64) ** 2, axis=1)
+    plan = lss_plan(su, sd, fwd.x_sumsq, budget, seed, offset)
+    A = weighted_rows(bs, plan)
+    assert np.abs(A).max(initial=0) <= 126
+    N, C = A.shape
+    D = fwd.xq.shape[1]
+    s_dn = float(bs.s_up) / BS_RATIO
+    a_dx = s_dn * float(fwd.s_w) * 2.0 ** (-k)
+    a_dw = s_dn * float(fwd.s_x) * 2.0 ** (-k)
+    At = A[plan.kept]
+    acc_dx = acc_dw = dX = dW = None
+    if need_dx:
+        acc_dx = _int_matmul(At, fwd.wq.astype(np.int64))
+        dX = np.zeros((N, D), dtype=np.float64)
+        dX[plan.kept] = a_dx * fwht_rows(acc_dx, k).astype(np.float64)
+    if need_dw:
+        acc_dw = _int_matmul(At.T, fwd.xq[plan.kept].astype(np.int64))
+        dW = a_dw * fwht_rows(acc_dw, k).astype(np.float64)
+    return LSSBackward(bs, plan, A, acc_dx, acc_dw, dX, dW, a_dx, a_dw)
