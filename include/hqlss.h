@@ -1,0 +1,188 @@
+/*
+ * hqlss.h -- C ABI of the INT4 quantised linear operator of
+ * "Training Transformers with 4-bit Integers" (Xi, Li, Chen, Zhu; arXiv 2306.11987),
+ * built for AMD Instinct MI355X (gfx950).
+ *
+ * One linear layer Y = X W^T, X: N x D activations (N tokens), W: C x D weights
+ * (Sec. 3, Eq. 1).
+ *
+ *   forward   HQ-MM  (Sec. 3.3, Procedure HQ-MM): block-diagonal Hadamard transform of
+ *             X and W, per-tensor INT4 quantisation, integer GEMM, dequantisation.
+ *   backward  LSS-MM (Sec. 4.2, Procedure LSS-MM; App. A.3): bit splitting of dY into
+ *             upper/lower INT4 halves, leverage-score sampling of the 2N stacked rows,
+ *             integer GEMMs for dX and dW, dequantisation and the H^T of the STE
+ *             gradients (Sec. 4).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory      All pointers are DEVICE pointers unless stated.  The caller allocates every
+ *             buffer (inputs, outputs, the saved state, the plan, the workspace); the
+ *             library allocates and frees nothing and keeps no pointer after returning.
+ * Layout      Row-major, contiguous.  X [N][D], W [C][D], Y/dY [N][C], dX [N][D], dW [C][D].
+ *             INT4 codes are packed two per byte, even column in the low nibble:
+ *             byte = (q[2i+1] << 4) | (q[2i] & 15)  (App. A.6, data pack).
+ * Dtypes      X, W, Y, dY, dX, dW all use `dt`.  Codes are in [-7, 7] (Q_N = Q_P = 7,
+ *             Sec. 3.1).  Integer GEMMs accumulate exactly in int32; scales and epilogues
+ *             are fp32.
+ * Hadamard    b = 2^log2_block, 0 <= log2_block <= 7.  The unnormalised +-1 Sylvester
+ *             matrix H_u is used (H_u H_u^T = b I, Sec. 3.3); the 2^-k factor is folded
+ *             into the dequantisation scales.
+ * Scales      Dynamic per-tensor absmax: a = max|v|, s = a / 7, codes
+ *             clamp(rint(v * fl(7/a)), -7, 7).  Bit splitting uses s_up = a_g / 7 and
+ *             s_dn = s_up / 14.
+ * Shapes      N >= 1; D and C multiples of 64; D a multiple of b.  N need not be a
+ *             multiple of anything.
+ * Streams     All work is enqueued on `stream` (a hipStream_t; 0 = the null stream) and
+ *             runs asynchronously; no entry point synchronises the host.  Counts that
+ *             the sample produces (the number of kept tokens) stay on the device.
+ * Errors      Arguments are validated on the host before anything is launched; a
+ *             non-zero hqlss_status is returned and nothing is enqueued.  A failed
+ *             launch returns HQLSS_ERR_HIP.  No C++ exception crosses this ABI.
+ * Threads     Calls may be issued from several host threads on different streams, with
+ *             distinct buffers; the kernel-timing facility below is single-threaded.
+ * RNG         Philox4x32-10 (Salmon et al., SC'11) with key = (lo32(seed), hi32(seed)) and
+ *             counter = (lo32(blk), hi32(blk), stream, 0), blk = offset + (i >> 3);
+ *             element i uses 16-bit half (i & 1) of output word ((i >> 1) & 3).
+ *             Stream 0: stochastic rounding of the lower bit-split half, i = n*C + c.
+ *             Stream 1: Bernoulli masks of the lower rows, i = n.
+ *             Equal (seed, offset, budget) give bit-identical codes and samples.
+ */
+#ifndef HQLSS_H
+#define HQLSS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { HQLSS_F32 = 0, HQLSS_F16 = 1, HQLSS_BF16 = 2 } hqlss_dtype;
+
+typedef enum {
+  HQLSS_OK = 0,
+  HQLSS_ERR_NULL = 1,      /* a required pointer is NULL                               */
+  HQLSS_ERR_SHAPE = 2,     /* N < 1, D or C not a positive multiple of 64               */
+  HQLSS_ERR_BLOCK = 3,     /* log2_block outside [0, 7] or D % 2^log2_block != 0         */
+  HQLSS_ERR_ALIGN = 4,     /* a pointer is not 16-byte aligned                          */
+  HQLSS_ERR_DTYPE = 5,     /* unknown dtype                                             */
+  HQLSS_ERR_WORKSPACE = 6, /* ws_bytes smaller than hqlss_workspace_bytes(...)          */
+  HQLSS_ERR_OVERFLOW = 7,  /* an int32 accumulator or an int64 score could overflow    */
+  HQLSS_ERR_HIP = 8,       /* a HIP launch or runtime call failed                       */
+  HQLSS_ERR_ARG = 9        /* any other invalid argument (e.g. budget, which)           */
+} hqlss_status;
+
+/* State written by the forward pass and read by the backward pass: the codes X^ and
+ * W^ "already calculated in forward" (Sec. 4).  Caller-allocated device memory; it must
+ * stay alive and unmodified from hq_linear_fwd until the backward calls have run. */
+typedef struct {
+  uint8_t *xq;      /* [N][D/2]  INT4 codes of X H_u                                  */
+  uint8_t *wq;      /* [C][D/2]  INT4 codes of W H_u                                  */
+  uint8_t *wqT;     /* [D][C/2]  the same codes, transposed (row d holds column d of W^) */
+  int32_t *x_sumsq; /* [N]       sum_d xq[n][d]^2 (feeds the leverage scores)          */
+  float *amax;      /* [2]       a_x = max|X H_u|, a_w = max|W H_u|  (s = a / 7)        */
+} hqlss_saved_t;
+
+/* The quantised gradient and its sample (Sec. 4.2, Procedure LSS-MM steps 1-4).
+ * Caller-allocated device memory, written by lss_grad_plan. */
+typedef struct {
+  uint8_t *qup;      /* [N][C/2]  upper INT4 codes of dY                               */
+  uint8_t *qdn;      /* [N][C/2]  lower INT4 codes of dY (stochastically rounded)      */
+  int32_t *sumsq_up; /* [N]       sum_c qup^2                                          */
+  int32_t *sumsq_dn; /* [N]       sum_c qdn^2                                          */
+  uint8_t *w_up;     /* [N]       weight of the upper row: 1 if kept, else 0            */
+  uint8_t *w_dn;     /* [N]       weight m/p of the lower row: 0, 1, 2, 4, 8 or 16      */
+  int32_t *kept;     /* [N]       ascending tokens with w_up + w_dn > 0 (first n_kept)   */
+  int32_t *n_kept;   /* [1]       |T|, the number of kept tokens                        */
+  float *amax_g;     /* [1]       a_g = max|dY|  (s_up = a_g / 7, s_dn = s_up / 14)      */
+} lss_plan_t;
+
+/* Workspace sizes (bytes) for the entry points below, which = HQLSS_WS_*. */
+enum { HQLSS_WS_FWD = 0, HQLSS_WS_BWD_DX = 1, HQLSS_WS_BWD_DW = 2, HQLSS_WS_BWD = 3,
+       HQLSS_WS_FROM_PLAN = 4 };
+size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C);
+
+/* HQ-MM forward (Sec. 3.3, Eq. 3; Procedure HQ-MM).
+ *   1. v_x = X H_u, v_w = W H_u in fp32 (radix-2 FWHT, strides ascending);
+ *   2. a_x = max|v_x|, a_w = max|v_w|; codes clamp(rint(v * fl(7/a)), -7, 7) -> saved;
+ *   3. acc = X^ W^^T (int32, exact);
+ *   4. Y = fl(alpha * acc), alpha = fl(fl(s_x s_w) / 2^k), cast to dt.
+ * X [N][D], W [C][D] inputs; Y [N][C] output; saved: outputs (all fields required). */
+hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int64_t D,
+                           int64_t C, hqlss_dtype dt, int log2_block,
+                           const hqlss_saved_t *saved, void *ws, size_t ws_bytes,
+                           void *stream);
+
+/* Bit splitting and leverage-score sampling of dY (Sec. 4.2, App. A.2; Procedure LSS-MM
+ * steps 1-3, shared by both gradients as in App. A.6).
+ *   q_up = rint(dY * fl(7/a_g)); r = that product - q_up; q_dn = SR(fl(14 r)) (stream 0);
+ *   scores c_j^2 = w^2 sum q^2 x_sumsq (w = 14 upper, 1 lower), c_j = isqrt(c_j^2 2^16);
+ *   p* by the clamp-and-rescale loop of App. A.2 with sum p* = budget (exact integers);
+ *   upper rows: kept iff non-zero; lower rows: p~ = 2^-e >= p* (e <= 4, <= 2 if the upper
+ *   row is non-zero), m = [u16 < 2^(16-e)] (stream 1), weight m 2^e.
+ * budget_rows <= 0 selects budget = N (Sec. 4.2: sum p_i = N).  dY [N][C] input; saved is
+ * read (x_sumsq); plan: outputs (all fields required). */
+hqlss_status lss_grad_plan(const void *dY, const hqlss_saved_t *saved, const lss_plan_t *plan,
+                           int64_t N, int64_t D, int64_t C, hqlss_dtype dt,
+                           int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
+                           size_t ws_bytes, void *stream);
+
+/* LSS-MM gradients from a plan (Sec. 4, Sec. 4.2, App. A.3; Procedure LSS-MM steps 4-6).
+ *   A_t = 14 w_up q_up[t] + w_dn q_dn[t] for kept tokens t (|A| <= 126, int8);
+ *   dX[t] = fl(alpha_dx * FWHT_b(A_t W^)),           alpha_dx = fl(fl(s_up s_w) / (14 b));
+ *   dW    = fl(alpha_dw * FWHT_b(A_T^T X^_T)) rows,  alpha_dw = fl(fl(s_up s_x) / (14 b));
+ *   rows of dX of dropped tokens are 0.  FWHT_b is along D, in exact int32.
+ * dX [N][D] or NULL, dW [C][D] or NULL (at least one).  saved and plan are inputs. */
+hqlss_status lss_linear_bwd_from_plan(const lss_plan_t *plan, const hqlss_saved_t *saved,
+                                      void *dX, void *dW, int64_t N, int64_t D, int64_t C,
+                                      hqlss_dtype dt, int log2_block, void *ws,
+                                      size_t ws_bytes, void *stream);
+
+/* Both gradients from one shared sample: lss_grad_plan into the workspace, then
+ * lss_linear_bwd_from_plan.  dX, dW outputs (either may be NULL, not both). */
+hqlss_status lss_linear_bwd(const void *dY, const hqlss_saved_t *saved, void *dX, void *dW,
+                            int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                            int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
+                            size_t ws_bytes, void *stream);
+
+/* Activation gradient alone (Sec. 4.2 "Activation Gradient"; App. A.3).  Same sample as
+ * lss_linear_bwd_dw for equal (seed, offset, budget_rows). */
+hqlss_status lss_linear_bwd_dx(const void *dY, const hqlss_saved_t *saved, void *dX,
+                               int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                               int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
+                               size_t ws_bytes, void *stream);
+
+/* Weight gradient alone (Sec. 4.2 "Weight Gradient", Eq. 5). */
+hqlss_status lss_linear_bwd_dw(const void *dY, const hqlss_saved_t *saved, void *dW,
+                               int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                               int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
+                               size_t ws_bytes, void *stream);
+
+/* Philox blocks one stream consumes per backward call: advance `offset` by at least this
+ * much between calls that must draw independent randomness. */
+uint64_t lss_philox_offset_advance(int64_t N, int64_t C);
+
+const char *hqlss_status_string(hqlss_status s);
+
+/* ---- inspection (tests) ------------------------------------------------------------
+ * Raw int32 accumulators of the three integer GEMMs, before any scaling or transform:
+ *   which 0: acc[N][C]   = X^ W^^T                     (inputs: saved)
+ *   which 1: acc[T][D]   = A_T W^  (rows in kept order, T = n_kept rows written)
+ *   which 2: acc[C][D]   = A_T^T X^_T
+ * acc is an int32 device buffer of N*C (0), N*D (1) or C*D (2) elements. */
+hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t *plan, const hqlss_saved_t *saved,
+                                  int32_t *acc, int64_t N, int64_t D, int64_t C, void *ws,
+                                  size_t ws_bytes, void *stream);
+
+/* ---- kernel timing (benchmarks) ------------------------------------------------------
+ * When enabled, every kernel the library launches is bracketed by two HIP events
+ * recorded on the launch stream.  hqlss_timing_read waits for them, writes up to `cap`
+ * (kernel id, milliseconds) pairs and clears the log; hqlss_kernel_name maps ids. */
+hqlss_status hqlss_timing_enable(int on);
+int hqlss_timing_read(int *ids, float *ms, int cap);
+const char *hqlss_kernel_name(int id);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HQLSS_H */

@@ -1,0 +1,248 @@
+"""ctypes binding of libhqlss.so: argument marshalling only (see include/hqlss.h)."""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhqlss.so")
+
+WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN = 0, 1, 2, 3, 4
+DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+_vp, _i64, _u64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int, ctypes.c_size_t
+
+
+class _SavedC(ctypes.Structure):
+    _fields_ = [("xq", _vp), ("wq", _vp), ("wqT", _vp), ("x_sumsq", _vp), ("amax", _vp)]
+
+
+class _PlanC(ctypes.Structure):
+    _fields_ = [("qup", _vp), ("qdn", _vp), ("sumsq_up", _vp), ("sumsq_dn", _vp), ("w_up", _vp),
+                ("w_dn", _vp), ("kept", _vp), ("n_kept", _vp), ("amax_g", _vp)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(LIB_PATH)
+    st = ctypes.c_int
+    sig = {
+        "hqlss_workspace_bytes": (_sz, [_int, _i64, _i64, _i64]),
+        "hq_linear_fwd": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
+                               _vp, _sz, _vp]),
+        "lss_grad_plan": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_PlanC), _i64, _i64, _i64,
+                               _int, _i64, _u64, _u64, _vp, _sz, _vp]),
+        "lss_linear_bwd_from_plan": (st, [ctypes.POINTER(_PlanC), ctypes.POINTER(_SavedC), _vp, _vp,
+                                          _i64, _i64, _i64, _int, _int, _vp, _sz, _vp]),
+        "lss_linear_bwd": (st, [_vp, ctypes.POINTER(_SavedC), _vp, _vp, _i64, _i64, _i64, _int, _int,
+                                _i64, _u64, _u64, _vp, _sz, _vp]),
+        "lss_linear_bwd_dx": (st, [_vp, ctypes.POINTER(_SavedC), _vp, _i64, _i64, _i64, _int, _int,
+                                   _i64, _u64, _u64, _vp, _sz, _vp]),
+        "lss_linear_bwd_dw": (st, [_vp, ctypes.POINTER(_SavedC), _vp, _i64, _i64, _i64, _int, _int,
+                                   _i64, _u64, _u64, _vp, _sz, _vp]),
+        "lss_philox_offset_advance": (_u64, [_i64, _i64]),
+        "hqlss_status_string": (ctypes.c_char_p, [_int]),
+        "hqlss_debug_gemm_acc": (st, [_int, ctypes.POINTER(_PlanC), ctypes.POINTER(_SavedC), _vp, _i64,
+                                      _i64, _i64, _vp, _sz, _vp]),
+        "hqlss_timing_enable": (st, [_int]),
+        "hqlss_timing_read": (_int, [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _int]),
+        "hqlss_kernel_name": (ctypes.c_char_p, [_int]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype, f.argtypes = res, args
+    return L
+
+
+lib = _load()
+
+
+class HQLSSError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+def status_string(status: int) -> str:
+    return lib.hqlss_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise HQLSSError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors handed to libhqlss must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors handed to libhqlss must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype not in DTYPE_CODES:
+        raise ValueError(f"unsupported dtype {t.dtype}")
+    return DTYPE_CODES[t.dtype]
+
+
+@dataclass
+class Saved:
+    """Forward-to-backward state (hqlss_saved_t): codes of X H_u and W H_u and friends."""
+
+    xq: torch.Tensor  # uint8 [N, D/2]
+    wq: torch.Tensor  # uint8 [C, D/2]
+    wqT: torch.Tensor  # uint8 [D, C/2]
+    x_sumsq: torch.Tensor  # int32 [N]
+    amax: torch.Tensor  # float32 [2]
+
+    @staticmethod
+    def empty(N: int, D: int, C: int, device="cuda") -> "Saved":
+        u8 = dict(dtype=torch.uint8, device=device)
+        return Saved(torch.empty(N, D // 2, **u8), torch.empty(C, D // 2, **u8),
+                     torch.empty(D, C // 2, **u8), torch.empty(N, dtype=torch.int32, device=device),
+                     torch.empty(2, dtype=torch.float32, device=device))
+
+    def c(self) -> _SavedC:
+        return _SavedC(_ptr(self.xq), _ptr(self.wq), _ptr(self.wqT), _ptr(self.x_sumsq), _ptr(self.amax))
+
+
+@dataclass
+class Plan:
+    """Quantised gradient and its sample (lss_plan_t)."""
+
+    qup: torch.Tensor  # uint8 [N, C/2]
+    qdn: torch.Tensor  # uint8 [N, C/2]
+    sumsq_up: torch.Tensor  # int32 [N]
+    sumsq_dn: torch.Tensor  # int32 [N]
+    w_up: torch.Tensor  # uint8 [N]
+    w_dn: torch.Tensor  # uint8 [N]
+    kept: torch.Tensor  # int32 [N]
+    n_kept: torch.Tensor  # int32 [1]
+    amax_g: torch.Tensor  # float32 [1]
+
+    @staticmethod
+    def empty(N: int, C: int, device="cuda") -> "Plan":
+        u8 = dict(dtype=torch.uint8, device=device)
+        i32 = dict(dtype=torch.int32, device=device)
+        return Plan(torch.empty(N, C // 2, **u8), torch.empty(N, C // 2, **u8), torch.empty(N, **i32),
+                    torch.empty(N, **i32), torch.empty(N, **u8), torch.empty(N, **u8),
+                    torch.empty(N, **i32), torch.empty(1, **i32),
+                    torch.empty(1, dtype=torch.float32, device=device))
+
+    def c(self) -> _PlanC:
+        return _PlanC(*[_ptr(getattr(self, f)) for f, _ in _PlanC._fields_])
+
+
+def workspace_bytes(which: int, N: int, D: int, C: int) -> int:
+    return int(lib.hqlss_workspace_bytes(int(which), int(N), int(D), int(C)))
+
+
+def workspace(which: int, N: int, D: int, C: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(workspace_bytes(which, N, D, C), 256), dtype=torch.uint8, device=device)
+
+
+def lss_philox_offset_advance(N: int, C: int) -> int:
+    return int(lib.lss_philox_offset_advance(int(N), int(C)))
+
+
+def _ws(ws: Optional[torch.Tensor]):
+    return (None, 0) if ws is None else (_ptr(ws), ws.numel())
+
+
+def hq_linear_fwd(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Saved, log2_block: int,
+                  ws: Optional[torch.Tensor] = None) -> None:
+    N, D = X.shape
+    C = W.shape[0]
+    p, n = _ws(ws)
+    sv = saved.c()
+    _check(lib.hq_linear_fwd(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
+                             ctypes.byref(sv), p, n, _stream(X)), "hq_linear_fwd")
+
+
+def lss_grad_plan(dY: torch.Tensor, saved: Saved, plan: Plan, D: int, budget: int = 0, seed: int = 0,
+                  offset: int = 0) -> None:
+    N, C = dY.shape
+    sv, pl = saved.c(), plan.c()
+    _check(lib.lss_grad_plan(_ptr(dY), ctypes.byref(sv), ctypes.byref(pl), N, int(D), C, _dt(dY),
+                             int(budget), int(seed), int(offset), None, 0, _stream(dY)), "lss_grad_plan")
+
+
+def lss_linear_bwd_from_plan(plan: Plan, saved: Saved, dX: Optional[torch.Tensor],
+                             dW: Optional[torch.Tensor], N: int, D: int, C: int, log2_block: int,
+                             ws: torch.Tensor) -> None:
+    ref = dX if dX is not None else dW
+    p, n = _ws(ws)
+    sv, pl = saved.c(), plan.c()
+    _check(lib.lss_linear_bwd_from_plan(ctypes.byref(pl), ctypes.byref(sv), _ptr(dX), _ptr(dW), N, D, C,
+                                        _dt(ref), int(log2_block), p, n, _stream(ref)),
+           "lss_linear_bwd_from_plan")
+
+
+def lss_linear_bwd(dY: torch.Tensor, saved: Saved, dX: Optional[torch.Tensor], dW: Optional[torch.Tensor],
+                   D: int, log2_block: int, budget: int = 0, seed: int = 0, offset: int = 0,
+                   ws: Optional[torch.Tensor] = None) -> None:
+    N, C = dY.shape
+    p, n = _ws(ws)
+    sv = saved.c()
+    _check(lib.lss_linear_bwd(_ptr(dY), ctypes.byref(sv), _ptr(dX), _ptr(dW), N, int(D), C, _dt(dY),
+                              int(log2_block), int(budget), int(seed), int(offset), p, n, _stream(dY)),
+           "lss_linear_bwd")
+
+
+def lss_linear_bwd_dx(dY: torch.Tensor, saved: Saved, dX: torch.Tensor, log2_block: int, budget: int = 0,
+                      seed: int = 0, offset: int = 0, ws: Optional[torch.Tensor] = None) -> None:
+    N, C = dY.shape
+    D = dX.shape[1]
+    p, n = _ws(ws)
+    sv = saved.c()
+    _check(lib.lss_linear_bwd_dx(_ptr(dY), ctypes.byref(sv), _ptr(dX), N, D, C, _dt(dY), int(log2_block),
+                                 int(budget), int(seed), int(offset), p, n, _stream(dY)), "lss_linear_bwd_dx")
+
+
+def lss_linear_bwd_dw(dY: torch.Tensor, saved: Saved, dW: torch.Tensor, log2_block: int, budget: int = 0,
+                      seed: int = 0, offset: int = 0, ws: Optional[torch.Tensor] = None) -> None:
+    N, C = dY.shape
+    D = dW.shape[1]
+    p, n = _ws(ws)
+    sv = saved.c()
+    _check(lib.lss_linear_bwd_dw(_ptr(dY), ctypes.byref(sv), _ptr(dW), N, D, C, _dt(dY), int(log2_block),
+                                 int(budget), int(seed), int(offset), p, n, _stream(dY)), "lss_linear_bwd_dw")
+
+
+def debug_gemm_acc(which: int, plan: Optional[Plan], saved: Saved, acc: torch.Tensor, N: int, D: int, C: int,
+                   ws: Optional[torch.Tensor] = None) -> None:
+    p, n = _ws(ws)
+    sv = saved.c()
+    pl = plan.c() if plan is not None else None
+    _check(lib.hqlss_debug_gemm_acc(int(which), ctypes.byref(pl) if pl is not None else None,
+                                    ctypes.byref(sv), _ptr(acc), N, D, C, p, n, _stream(acc)),
+           "hqlss_debug_gemm_acc")
+
+
+def timing_enable(on: bool) -> None:
+    _check(lib.hqlss_timing_enable(1 if on else 0), "hqlss_timing_enable")
+
+
+def timing_read(cap: int = 4096):
+    ids = (ctypes.c_int * cap)()
+    ms = (ctypes.c_float * cap)()
+    n = lib.hqlss_timing_read(ids, ms, cap)
+    if n < 0:
+        raise HQLSSError(8, "hqlss_timing_read")
+    return [(int(ids[i]), float(ms[i])) for i in range(n)]
+
+
+def kernel_name(i: int) -> str:
+    return lib.hqlss_kernel_name(int(i)).decode()

@@ -1,0 +1,440 @@
+// C ABI of libhqlss: argument validation, workspace carving and the launch sequence of
+// HQ-MM (forward) and LSS-MM (backward) on the caller's stream.  See include/hqlss.h.
+#include <hip/hip_runtime.h>
+
+#include <vector>
+
+#include "../../include/hqlss.h"
+#include "common.h"
+#include "launch.h"
+
+using namespace hqlss;
+
+namespace {
+
+constexpr int64_t kPad = 128;  // row padding of gathered operands (GEMM tile / K step)
+
+int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+size_t al(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool a16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+bool a4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
+
+hqlss_status hip_status(hipError_t e) { return e == hipSuccess ? HQLSS_OK : HQLSS_ERR_HIP; }
+#define HQ_TRY(expr)                              \
+  do {                                            \
+    hipError_t e_ = (expr);                       \
+    if (e_ != hipSuccess) return HQLSS_ERR_HIP;   \
+  } while (0)
+
+// ---------------------------------------------------------------- shape checks
+hqlss_status check_shape(int64_t N, int64_t D, int64_t C) {
+  if (N < 1 || D < 64 || C < 64 || D % 64 || C % 64) return HQLSS_ERR_SHAPE;
+  if (N > (int64_t(1) << 30) || D > (int64_t(1) << 24) || C > (int64_t(1) << 24)) return HQLSS_ERR_SHAPE;
+  return HQLSS_OK;
+}
+hqlss_status check_block(int log2_block, int64_t D) {
+  if (log2_block < 0 || log2_block > 7) return HQLSS_ERR_BLOCK;
+  if (D % (int64_t(1) << log2_block)) return HQLSS_ERR_BLOCK;
+  return HQLSS_OK;
+}
+hqlss_status check_dtype(int dt) {
+  return (dt == HQLSS_F32 || dt == HQLSS_F16 || dt == HQLSS_BF16) ? HQLSS_OK : HQLSS_ERR_DTYPE;
+}
+const int64_t kI32 = int64_t(1) << 31;
+// forward accumulators: 16 x 16 x 49 x D (both operands widened by 16)
+hqlss_status check_fwd_overflow(int64_t D) {
+  return 256 * 49 * D < kI32 ? HQLSS_OK : HQLSS_ERR_OVERFLOW;
+}
+// gradient accumulators: 16 x 126 x 7 x K raw, and b x 126 x 7 x K after the transform;
+// K = C for dX, K = kept tokens <= N for dW.  Scores: 196 (49 C)(49 D) 2^16 < 2^64.
+hqlss_status check_bwd_overflow(int64_t N, int64_t D, int64_t C, int log2_block) {
+  const int64_t b = int64_t(1) << log2_block;
+  const int64_t kmax = N > C ? N : C;
+  const int64_t f = (b > 16 ? b : 16) * 126 * 7;
+  if (f * kmax >= kI32) return HQLSS_ERR_OVERFLOW;
+  const long double sc = 196.0L * 49.0L * (long double)C * 49.0L * (long double)D * 65536.0L;
+  if (sc >= 18446744073709551615.0L) return HQLSS_ERR_OVERFLOW;
+  if (N > 65536) return HQLSS_ERR_SHAPE;  // one-workgroup sampler keeps <= 64 tokens per thread
+  return HQLSS_OK;
+}
+
+hqlss_status check_saved(const hqlss_saved_t* s) {
+  if (!s || !s->xq || !s->wq || !s->wqT || !s->x_sumsq || !s->amax) return HQLSS_ERR_NULL;
+  if (!a16(s->xq) || !a16(s->wq) || !a16(s->wqT) || !a16(s->x_sumsq) || !a4(s->amax))
+    return HQLSS_ERR_ALIGN;
+  return HQLSS_OK;
+}
+hqlss_status check_plan(const lss_plan_t* p) {
+  if (!p || !p->qup || !p->qdn || !p->sumsq_up || !p->sumsq_dn || !p->w_up || !p->w_dn ||
+      !p->kept || !p->n_kept || !p->amax_g)
+    return HQLSS_ERR_NULL;
+  if (!a16(p->qup) || !a16(p->qdn) || !a16(p->sumsq_up) || !a16(p->sumsq_dn) || !a16(p->w_up) ||
+      !a16(p->w_dn) || !a16(p->kept) || !a4(p->n_kept) || !a4(p->amax_g))
+    return HQLSS_ERR_ALIGN;
+  return HQLSS_OK;
+}
+
+// ---------------------------------------------------------------- workspace layout
+size_t plan_bytes(int64_t N, int64_t C) {
+  return al(N * C / 2) * 2 + al(4 * N) * 2 + al(N) * 2 + al(4 * N) + al(4) * 2;
+}
+size_t dx_bytes(int64_t N, int64_t C) { return al(rup(N, kPad) * C); }
+size_t dw_bytes(int64_t N, int64_t D, int64_t C) {
+  return al(C * rup(N, kPad)) + al(D * rup(N, kPad) / 2);
+}
+
+struct Carve {
+  char* base;
+  size_t off, cap;
+  template <class T>
+  T* take(size_t bytes) {
+    off = al(off);
+    T* p = reinterpret_cast<T*>(base + off);
+    off += bytes;
+    return p;
+  }
+  bool ok() const { return off <= cap; }
+};
+
+void plan_from_ws(Carve& w, int64_t N, int64_t C, lss_plan_t* p) {
+  p->qup = w.take<uint8_t>(N * C / 2);
+  p->qdn = w.take<uint8_t>(N * C / 2);
+  p->sumsq_up = w.take<int32_t>(4 * N);
+  p->sumsq_dn = w.take<int32_t>(4 * N);
+  p->w_up = w.take<uint8_t>(N);
+  p->w_dn = w.take<uint8_t>(N);
+  p->kept = w.take<int32_t>(4 * N);
+  p->n_kept = w.take<int32_t>(4);
+  p->amax_g = w.take<float>(4);
+}
+
+// ---------------------------------------------------------------- timing log
+struct TimingLog {
+  bool on = false;
+  std::vector<hipEvent_t> ev;  // pairs
+  std::vector<int> ids;
+  size_t used = 0;
+  bool overflow = false;
+};
+TimingLog g_log;
+constexpr size_t kLogPairs = 4096;
+
+// ---------------------------------------------------------------- the two passes
+hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
+                    int dt, int k, const hqlss_saved_t* sv, hipStream_t s) {
+  uint32_t* amax = reinterpret_cast<uint32_t*>(sv->amax);
+  HQ_TRY(launch_zero(s, amax, 2, reinterpret_cast<uint32_t*>(sv->x_sumsq), N));
+  HQ_TRY(launch_fwht_absmax(s, dt, k, X, N, D, amax));
+  HQ_TRY(launch_fwht_absmax(s, dt, k, W, C, D, amax + 1));
+  HQ_TRY(launch_fwht_quant(s, dt, k, X, N, D, amax, sv->xq, sv->x_sumsq));
+  HQ_TRY(launch_fwht_quant(s, dt, k, W, C, D, amax + 1, sv->wq, nullptr));
+  HQ_TRY(launch_transpose_packed(s, sv->wq, C, D, sv->wqT));
+  if (Y) {
+    GemmArgs g{};
+    g.A = sv->xq; g.lda = D / 2;
+    g.B = sv->wq; g.ldb = D / 2;
+    g.M = N; g.N = C; g.K = D;
+    g.out = Y; g.ldo = C;
+    g.amax1 = amax; g.amax2 = amax + 1;
+    g.denom = (float)(int64_t(1) << k);
+    g.log2b = k;
+    HQ_TRY(launch_gemm(s, kEpiFwd, dt, true, true, g));
+  }
+  return HQLSS_OK;
+}
+
+hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* p, int64_t N,
+                     int64_t C, int dt, int64_t budget, uint64_t seed, uint64_t offset,
+                     hipStream_t s) {
+  uint32_t* ag = reinterpret_cast<uint32_t*>(p->amax_g);
+  HQ_TRY(launch_zero(s, ag, 1, reinterpret_cast<uint32_t*>(p->sumsq_up), N,
+                     reinterpret_cast<uint32_t*>(p->sumsq_dn), N));
+  HQ_TRY(launch_fwht_absmax(s, dt, 0, dY, N, C, ag));
+  HQ_TRY(launch_bit_split(s, dt, dY, N, C, ag, p->qup, p->qdn, p->sumsq_up, p->sumsq_dn, seed,
+                          offset));
+  HQ_TRY(launch_lss_plan(s, p->sumsq_up, p->sumsq_dn, sv->x_sumsq, N, budget, seed, offset,
+                         p->w_up, p->w_dn, p->kept, p->n_kept));
+  return HQLSS_OK;
+}
+
+hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, void* dW,
+                      int32_t* acc, int which_acc, int64_t N, int64_t D, int64_t C, int dt,
+                      int k, Carve& w, hipStream_t s) {
+  const uint32_t* amax = reinterpret_cast<const uint32_t*>(sv->amax);
+  const uint32_t* ag = reinterpret_cast<const uint32_t*>(p->amax_g);
+  const float denom = (float)(kBsRatio * (int64_t(1) << k));
+  const bool want_dx = dX || (acc && which_acc == 1);
+  const bool want_dw = dW || (acc && which_acc == 2);
+  if (want_dx) {
+    int8_t* Ag = w.take<int8_t>(rup(N, kPad) * C);
+    HQ_TRY(launch_build_ag(s, dt, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept, N, C, D,
+                           Ag, dX));
+    GemmArgs g{};
+    g.A = Ag; g.lda = C;
+    g.B = sv->wqT; g.ldb = C / 2;
+    g.M = N; g.m_dev = p->n_kept; g.N = D; g.K = C;
+    g.out_rows = p->kept;
+    g.amax1 = ag; g.amax2 = amax + 1; g.denom = denom; g.log2b = k;
+    if (dX) {
+      g.out = dX; g.ldo = D;
+      HQ_TRY(launch_gemm(s, kEpiDx, dt, false, true, g));
+    }
+    if (acc && which_acc == 1) {
+      g.out = acc; g.ldo = D;
+      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g));
+    }
+  }
+  if (want_dw) {
+    const int64_t Kp = rup(N, kPad);
+    int8_t* At = w.take<int8_t>(C * Kp);
+    uint8_t* XtT = w.take<uint8_t>(D * Kp / 2);
+    HQ_TRY(launch_build_dw_operands(s, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept,
+                                    sv->xq, N, C, D, At, XtT));
+    GemmArgs g{};
+    g.A = At; g.lda = Kp;
+    g.B = XtT; g.ldb = Kp / 2;
+    g.M = C; g.N = D; g.K = Kp; g.k_dev = p->n_kept;
+    g.amax1 = ag; g.amax2 = amax; g.denom = denom; g.log2b = k;
+    if (dW) {
+      g.out = dW; g.ldo = D;
+      HQ_TRY(launch_gemm(s, kEpiDw, dt, false, true, g));
+    }
+    if (acc && which_acc == 2) {
+      g.out = acc; g.ldo = D;
+      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g));
+    }
+  }
+  return HQLSS_OK;
+}
+
+hqlss_status check_bwd_common(const void* dY, const hqlss_saved_t* saved, int64_t N, int64_t D,
+                              int64_t C, int dt, int log2_block, int64_t budget) {
+  if (!dY) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if ((st = check_block(log2_block, D))) return st;
+  if ((st = check_dtype(dt))) return st;
+  if ((st = check_saved(saved))) return st;
+  if (!a16(dY)) return HQLSS_ERR_ALIGN;
+  if ((st = check_bwd_overflow(N, D, C, log2_block))) return st;
+  if (budget > 2 * N) return HQLSS_ERR_ARG;
+  return HQLSS_OK;
+}
+
+}  // namespace
+
+namespace hqlss {
+
+const char* kernel_name(int id) {
+  static const char* names[kKCount] = {"zero", "fwht_absmax", "fwht_quant", "transpose_packed",
+                                       "bit_split", "lss_plan", "build_ag", "build_dw_operands",
+                                       "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc"};
+  return (id >= 0 && id < kKCount) ? names[id] : "?";
+}
+
+void timing_begin(hipStream_t s) {
+  if (!g_log.on) return;
+  if (g_log.used >= kLogPairs) { g_log.overflow = true; return; }
+  (void)hipEventRecord(g_log.ev[2 * g_log.used], s);
+}
+void timing_end(hipStream_t s, int id) {
+  if (!g_log.on || g_log.used >= kLogPairs) return;
+  (void)hipEventRecord(g_log.ev[2 * g_log.used + 1], s);
+  g_log.ids[g_log.used] = id;
+  ++g_log.used;
+}
+
+}  // namespace hqlss
+
+extern "C" {
+
+size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
+  if (N < 1 || D < 1 || C < 1) return 0;
+  switch (which) {
+    case HQLSS_WS_FWD: return 0;
+    case HQLSS_WS_BWD_DX: return plan_bytes(N, C) + dx_bytes(N, C);
+    case HQLSS_WS_BWD_DW: return plan_bytes(N, C) + dw_bytes(N, D, C);
+    case HQLSS_WS_BWD: return plan_bytes(N, C) + dx_bytes(N, C) + dw_bytes(N, D, C);
+    case HQLSS_WS_FROM_PLAN: return dx_bytes(N, C) + dw_bytes(N, D, C);
+  }
+  return 0;
+}
+
+uint64_t lss_philox_offset_advance(int64_t N, int64_t C) {
+  if (N < 1 || C < 1) return 0;
+  return (uint64_t)((N * C + 7) / 8);
+}
+
+const char* hqlss_status_string(hqlss_status s) {
+  switch (s) {
+    case HQLSS_OK: return "ok";
+    case HQLSS_ERR_NULL: return "a required pointer is NULL";
+    case HQLSS_ERR_SHAPE: return "invalid shape (N >= 1; D, C positive multiples of 64)";
+    case HQLSS_ERR_BLOCK: return "invalid Hadamard block (0 <= log2_block <= 7, D % 2^k == 0)";
+    case HQLSS_ERR_ALIGN: return "pointer not aligned (16 bytes for arrays, 4 for scalars)";
+    case HQLSS_ERR_DTYPE: return "unknown dtype";
+    case HQLSS_ERR_WORKSPACE: return "workspace too small";
+    case HQLSS_ERR_OVERFLOW: return "shape would overflow an int32 accumulator or int64 score";
+    case HQLSS_ERR_HIP: return "HIP launch or runtime error";
+    case HQLSS_ERR_ARG: return "invalid argument";
+  }
+  return "unknown status";
+}
+
+hqlss_status hq_linear_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
+                           hqlss_dtype dt, int log2_block, const hqlss_saved_t* saved, void* ws,
+                           size_t ws_bytes, void* stream) {
+  (void)ws; (void)ws_bytes;
+  if (!X || !W || !Y) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if ((st = check_block(log2_block, D))) return st;
+  if ((st = check_dtype(dt))) return st;
+  if ((st = check_saved(saved))) return st;
+  if (!a16(X) || !a16(W) || !a16(Y)) return HQLSS_ERR_ALIGN;
+  if ((st = check_fwd_overflow(D))) return st;
+  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, static_cast<hipStream_t>(stream));
+}
+
+hqlss_status lss_grad_plan(const void* dY, const hqlss_saved_t* saved, const lss_plan_t* plan,
+                           int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int64_t budget_rows,
+                           uint64_t seed, uint64_t offset, void* ws, size_t ws_bytes,
+                           void* stream) {
+  (void)ws; (void)ws_bytes;
+  hqlss_status st;
+  if ((st = check_bwd_common(dY, saved, N, D, C, dt, 0, budget_rows))) return st;
+  if ((st = check_plan(plan))) return st;
+  const int64_t B = budget_rows <= 0 ? N : budget_rows;
+  return do_plan(dY, saved, plan, N, C, dt, B, seed, offset, static_cast<hipStream_t>(stream));
+}
+
+hqlss_status lss_linear_bwd_from_plan(const lss_plan_t* plan, const hqlss_saved_t* saved,
+                                      void* dX, void* dW, int64_t N, int64_t D, int64_t C,
+                                      hqlss_dtype dt, int log2_block, void* ws, size_t ws_bytes,
+                                      void* stream) {
+  if (!dX && !dW) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if ((st = check_block(log2_block, D))) return st;
+  if ((st = check_dtype(dt))) return st;
+  if ((st = check_saved(saved))) return st;
+  if ((st = check_plan(plan))) return st;
+  if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
+  if ((st = check_bwd_overflow(N, D, C, log2_block))) return st;
+  const size_t need = (dX ? dx_bytes(N, C) : 0) + (dW ? dw_bytes(N, D, C) : 0);
+  if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  return do_grads(plan, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w,
+                  static_cast<hipStream_t>(stream));
+}
+
+static hqlss_status bwd_impl(const void* dY, const hqlss_saved_t* saved, void* dX, void* dW,
+                             int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                             int64_t budget_rows, uint64_t seed, uint64_t offset, void* ws,
+                             size_t ws_bytes, void* stream) {
+  if (!dX && !dW) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_bwd_common(dY, saved, N, D, C, dt, log2_block, budget_rows))) return st;
+  if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
+  const size_t need = plan_bytes(N, C) + (dX ? dx_bytes(N, C) : 0) + (dW ? dw_bytes(N, D, C) : 0);
+  if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  lss_plan_t p;
+  plan_from_ws(w, N, C, &p);
+  const int64_t B = budget_rows <= 0 ? N : budget_rows;
+  if ((st = do_plan(dY, saved, &p, N, C, dt, B, seed, offset, s))) return st;
+  return do_grads(&p, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w, s);
+}
+
+hqlss_status lss_linear_bwd(const void* dY, const hqlss_saved_t* saved, void* dX, void* dW,
+                            int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                            int64_t budget_rows, uint64_t seed, uint64_t offset, void* ws,
+                            size_t ws_bytes, void* stream) {
+  return bwd_impl(dY, saved, dX, dW, N, D, C, dt, log2_block, budget_rows, seed, offset, ws,
+                  ws_bytes, stream);
+}
+
+hqlss_status lss_linear_bwd_dx(const void* dY, const hqlss_saved_t* saved, void* dX, int64_t N,
+                               int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                               int64_t budget_rows, uint64_t seed, uint64_t offset, void* ws,
+                               size_t ws_bytes, void* stream) {
+  if (!dX) return HQLSS_ERR_NULL;
+  return bwd_impl(dY, saved, dX, nullptr, N, D, C, dt, log2_block, budget_rows, seed, offset, ws,
+                  ws_bytes, stream);
+}
+
+hqlss_status lss_linear_bwd_dw(const void* dY, const hqlss_saved_t* saved, void* dW, int64_t N,
+                               int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                               int64_t budget_rows, uint64_t seed, uint64_t offset, void* ws,
+                               size_t ws_bytes, void* stream) {
+  if (!dW) return HQLSS_ERR_NULL;
+  return bwd_impl(dY, saved, nullptr, dW, N, D, C, dt, log2_block, budget_rows, seed, offset, ws,
+                  ws_bytes, stream);
+}
+
+hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t* plan, const hqlss_saved_t* saved,
+                                  int32_t* acc, int64_t N, int64_t D, int64_t C, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  if (!acc) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if ((st = check_saved(saved))) return st;
+  if (!a16(acc)) return HQLSS_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (which == 0) {
+    if ((st = check_fwd_overflow(D))) return st;
+    GemmArgs g{};
+    g.A = saved->xq; g.lda = D / 2;
+    g.B = saved->wq; g.ldb = D / 2;
+    g.M = N; g.N = C; g.K = D;
+    g.out = acc; g.ldo = C;
+    return hip_status(launch_gemm(s, kEpiAcc, HQLSS_F32, true, true, g));
+  }
+  if (which != 1 && which != 2) return HQLSS_ERR_ARG;
+  if ((st = check_plan(plan))) return st;
+  if ((st = check_bwd_overflow(N, D, C, 0))) return st;
+  const size_t need = which == 1 ? dx_bytes(N, C) : dw_bytes(N, D, C);
+  if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
+  if (!a16(ws)) return HQLSS_ERR_ALIGN;
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  return do_grads(plan, saved, nullptr, nullptr, acc, which, N, D, C, HQLSS_F32, 0, w, s);
+}
+
+hqlss_status hqlss_timing_enable(int on) {
+  if (on && !g_log.on) {
+    if (g_log.ev.empty()) {
+      g_log.ev.resize(2 * kLogPairs);
+      g_log.ids.resize(kLogPairs);
+      for (auto& e : g_log.ev)
+        if (hipEventCreate(&e) != hipSuccess) return HQLSS_ERR_HIP;
+    }
+    g_log.used = 0;
+    g_log.overflow = false;
+    g_log.on = true;
+  } else if (!on) {
+    g_log.on = false;
+  }
+  return HQLSS_OK;
+}
+
+int hqlss_timing_read(int* ids, float* ms, int cap) {
+  int n = 0;
+  for (size_t i = 0; i < g_log.used; ++i) {
+    if (hipEventSynchronize(g_log.ev[2 * i + 1]) != hipSuccess) return -1;
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, g_log.ev[2 * i], g_log.ev[2 * i + 1]) != hipSuccess) return -1;
+    if (n < cap) {
+      ids[n] = g_log.ids[i];
+      ms[n] = t;
+      ++n;
+    }
+  }
+  g_log.used = 0;
+  return n;
+}
+
+const char* hqlss_kernel_name(int id) { return hqlss::kernel_name(id); }
+
+}  // extern "C"

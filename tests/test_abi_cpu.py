@@ -1,0 +1,136 @@
+"""Host-side checks of the C ABI (no GPU needed, nothing is launched).
+
+The library loads, exports every symbol the public header declares, and rejects
+invalid arguments with the documented status before touching the device.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hqlss.h")
+
+import torch  # noqa: E402
+
+# Host-only: these calls pass fake device pointers that must be rejected by validation.
+# Never run them where a GPU is visible, so that a validation slip cannot launch.
+pytestmark = pytest.mark.skipif(torch.cuda.device_count() > 0,
+                                reason="host-only ABI validation checks (fake pointers)")
+
+H = pytest.importorskip("paper_2306_11987_amd", reason="libhqlss.so not built")
+lib = H.lib
+
+OK, NULL, SHAPE, BLOCK, ALIGN, DTYPE, WS, OVF, HIP, ARG = range(10)
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    names = re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", txt)
+    skip = {"if", "sizeof", "defined"}
+    return sorted({n for n in names if n not in skip and (n.startswith("hq") or n.startswith("lss"))})
+
+
+def test_exports_every_declared_symbol():
+    fns = declared_functions()
+    assert len(fns) >= 13
+    raw = ctypes.CDLL(H._binding.LIB_PATH)
+    for name in fns:
+        assert hasattr(raw, name), f"missing export {name}"
+
+
+def test_status_strings():
+    for s in range(10):
+        assert H.status_string(s) and H.status_string(s) != "unknown status"
+    assert H.status_string(99) == "unknown status"
+
+
+def test_workspace_sizes_monotone():
+    for which in range(5):
+        a = H.workspace_bytes(which, 128, 256, 256)
+        b = H.workspace_bytes(which, 16384, 768, 3072)
+        assert b >= a >= 0
+    assert H.workspace_bytes(H.WS_FWD, 128, 256, 256) == 0
+    assert H.workspace_bytes(H.WS_BWD, 128, 256, 256) >= H.workspace_bytes(H.WS_BWD_DX, 128, 256, 256)
+    assert H.workspace_bytes(H.WS_BWD, 0, 256, 256) == 0
+
+
+def test_philox_offset_advance():
+    assert H.lss_philox_offset_advance(128, 256) == 128 * 256 // 8
+    assert H.lss_philox_offset_advance(3, 64) == 24
+    assert H.lss_philox_offset_advance(1, 72) == 9
+
+
+_Saved = H._binding._SavedC  # the hqlss_saved_t mirror of the binding
+
+
+FAKE = 0x10000  # never dereferenced: every call below must fail validation first
+
+
+def _saved(**over):
+    s = _Saved(FAKE, FAKE, FAKE, FAKE, FAKE)
+    for k, v in over.items():
+        setattr(s, k, v)
+    return s
+
+
+def fwd(X=FAKE, W=FAKE, Y=FAKE, N=128, D=256, C=256, dt=0, k=5, saved=None):
+    s = saved if saved is not None else _saved()
+    return lib.hq_linear_fwd(X, W, Y, N, D, C, dt, k, ctypes.byref(s), None, 0, None)
+
+
+def test_fwd_argument_errors():
+    assert fwd(X=None) == NULL
+    assert fwd(saved=_saved(wqT=None)) == NULL
+    assert fwd(N=0) == SHAPE
+    assert fwd(D=100) == SHAPE
+    assert fwd(C=32) == SHAPE
+    assert fwd(k=8) == BLOCK
+    assert fwd(k=-1) == BLOCK
+    assert fwd(D=192, k=7) == BLOCK  # 192 % 128 != 0
+    assert fwd(dt=3) == DTYPE
+    assert fwd(X=FAKE + 4) == ALIGN
+    assert fwd(saved=_saved(xq=FAKE + 8)) == ALIGN
+    assert fwd(D=1 << 20, C=64, N=1) == OVF  # 256 * 49 * D >= 2^31
+
+
+def bwd(dY=FAKE, dX=FAKE, dW=FAKE, N=128, D=256, C=256, dt=0, k=5, budget=0, ws=FAKE, nbytes=1 << 40):
+    s = _saved()
+    return lib.lss_linear_bwd(dY, ctypes.byref(s), dX, dW, N, D, C, dt, k, budget, 0, 0, ws, nbytes, None)
+
+
+def test_bwd_argument_errors():
+    assert bwd(dX=None, dW=None) == NULL
+    assert bwd(dY=None) == NULL
+    assert bwd(N=-1) == SHAPE
+    assert bwd(C=100) == SHAPE
+    assert bwd(k=9) == BLOCK
+    assert bwd(dt=7) == DTYPE
+    assert bwd(dX=FAKE + 2) == ALIGN
+    assert bwd(budget=1000) == ARG  # budget > 2N
+    assert bwd(ws=None) == WS
+    assert bwd(nbytes=100) == WS
+    assert bwd(N=70000) == SHAPE  # sampler limit
+    assert bwd(N=1, C=1 << 20, D=64, k=0) == OVF  # 16 * 882 * C >= 2^31
+    assert bwd(N=16384 + 8192, C=256, D=256, k=7) == OVF  # 128 * 882 * N >= 2^31
+    assert lib.lss_linear_bwd_dx(FAKE, ctypes.byref(_saved()), None, 128, 256, 256, 0, 5, 0, 0, 0,
+                                 FAKE, 1 << 40, None) == NULL
+    assert lib.lss_linear_bwd_dw(FAKE, ctypes.byref(_saved()), None, 128, 256, 256, 0, 5, 0, 0, 0,
+                                 FAKE, 1 << 40, None) == NULL
+
+
+def test_debug_acc_errors():
+    s = _saved()
+    assert lib.hqlss_debug_gemm_acc(0, None, ctypes.byref(s), None, 128, 256, 256, None, 0, None) == NULL
+    assert lib.hqlss_debug_gemm_acc(5, None, ctypes.byref(s), FAKE, 128, 256, 256, None, 0, None) == ARG
+    assert lib.hqlss_debug_gemm_acc(1, None, ctypes.byref(s), FAKE, 128, 256, 256, None, 0, None) == NULL
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    X = torch.zeros(128, 256)
+    sv = H.Saved(*(torch.zeros(2) for _ in range(5)))
+    with pytest.raises(ValueError):
+        H.hq_linear_fwd(X, X, X, sv, 5)

@@ -1,0 +1,177 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Bit-exact: codes, scales, row sums, sample weights, kept lists and every int32 GEMM
+accumulator.  Float outputs: within 1e-5 relative (fp32) or one unit in the last place of
+the output dtype around the fp64 oracle value (fp16, bf16).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from gpu_util import (check_backward_acc, check_float_output, check_forward, check_plan,
+                      dev_tensor, need_gpu, run_backward, run_forward, say, to_np, TORCH_DT)
+
+pytestmark = pytest.mark.gpu
+
+# (N, D, C, log2_block, dtype, grad_kind): several tiles, ragged N, every dtype and block size
+SHAPES = [
+    (128, 256, 256, 5, "f32", "sparse_rows"),
+    (1, 64, 64, 0, "f32", "lognormal"),
+    (200, 192, 320, 6, "f16", "lognormal"),
+    (333, 256, 128, 7, "bf16", "pareto"),
+    (77, 512, 576, 3, "f16", "pareto"),
+    (300, 1024, 384, 5, "bf16", "lognormal"),
+    (517, 128, 704, 1, "f32", "pareto"),
+]
+
+
+def _case(shape, seed=0):
+    N, D, C, k, dt, kind = shape
+    lin = synth.Linear(f"t{N}x{D}x{C}", N, D, C, k, dt, max(1, D // 100), 20.0, kind, N)
+    X, W, G = synth.linear_inputs(lin, seed)
+    return lin, X, W, G
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"N{s[0]}_D{s[1]}_C{s[2]}_k{s[3]}_{s[4]}")
+def test_forward_parity(shape):
+    H = need_gpu()
+    lin, X, W, _ = _case(shape)
+    say(f"forward parity {shape}")
+    saved, Y = run_forward(H, X, W, lin.log2_block, lin.dtype)
+    rel = check_forward(H, X, W, lin.log2_block, lin.dtype, saved, Y)
+    assert rel <= (1e-5 if lin.dtype == "f32" else 2e-3)
+
+
+@pytest.mark.parametrize("budget_div", [1, 4])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"N{s[0]}_D{s[1]}_C{s[2]}_k{s[3]}_{s[4]}")
+def test_backward_parity(shape, budget_div):
+    H = need_gpu()
+    lin, X, W, G = _case(shape, seed=1)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    budget = max(1, N // budget_div)
+    seed, offset = 1234, 77
+    say(f"backward parity {shape} budget={budget}")
+    saved, _ = run_forward(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)
+    b = O.lss_backward(G, f, budget, seed, offset)
+    tG, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, budget, seed, offset)
+    check_plan(plan, b)
+    check_backward_acc(H, plan, saved, b, N, D, C)
+    check_float_output("dX", dX, b.dX, dt)
+    check_float_output("dW", dW, b.dW, dt)
+
+    # the one-call entry points reproduce the same sample and outputs bit for bit
+    ws = H.workspace(H.WS_BWD, N, D, C)
+    dX2 = torch.empty_like(dX)
+    dW2 = torch.empty_like(dW)
+    H.lss_linear_bwd(tG, saved, dX2, dW2, D, k, budget, seed, offset, ws)
+    dX3 = torch.empty_like(dX)
+    dW3 = torch.empty_like(dW)
+    H.lss_linear_bwd_dx(tG, saved, dX3, k, budget, seed, offset, ws)
+    H.lss_linear_bwd_dw(tG, saved, dW3, k, budget, seed, offset, ws)
+    torch.cuda.synchronize()
+    for t in (dX2, dX3):
+        assert torch.equal(t, dX)
+    for t in (dW2, dW3):
+        assert torch.equal(t, dW)
+
+
+def test_sampling_exercised_and_deterministic():
+    """A small budget makes the Bernoulli path live; equal (seed, offset) give identical
+    samples, a different offset a different one."""
+    H = need_gpu()
+    lin, X, W, G = _case((512, 256, 256, 5, "f16", "pareto"), seed=3)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    saved, _ = run_forward(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)
+    outs = []
+    for off in (5, 5, 6):
+        say(f"determinism offset={off}")
+        b = O.lss_backward(G, f, N // 8, 9, off)
+        assert (b.plan.e_dn > 0).any() and len(b.plan.kept) < N
+        _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N // 8, 9, off)
+        check_plan(plan, b)
+        outs.append((to_np(plan.w_dn).copy(), to_np(dW).copy()))
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+    assert not np.array_equal(outs[0][0], outs[2][0])
+
+
+def test_zero_gradient_and_zero_input():
+    """dY = 0: nothing is kept, both gradients are exactly zero.  X = 0: Y = 0."""
+    H = need_gpu()
+    lin, X, W, G = _case((130, 128, 192, 4, "bf16", "lognormal"))
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    saved, Y = run_forward(H, np.zeros_like(X), W, k, dt)
+    torch.cuda.synchronize()
+    assert not Y.float().abs().sum().item()
+    saved, _ = run_forward(H, X, W, k, dt)
+    _, plan, dX, dW = run_backward(H, np.zeros_like(G), saved, N, D, C, k, dt, N, 0, 0)
+    torch.cuda.synchronize()
+    assert int(to_np(plan.n_kept)[0]) == 0
+    assert not dX.float().abs().sum().item() and not dW.float().abs().sum().item()
+
+
+def test_exact_reconstruction_on_gpu():
+    """X = 2^m Q H_u / b: the GPU codes equal Q and Y equals X W^T exactly (Sec. 3.3)."""
+    import scipy.linalg
+    H = need_gpu()
+    k, b = 4, 16
+    rng = np.random.default_rng(11)
+    N, D, C = 70, 128, 64
+    Qx = rng.integers(-7, 8, size=(N, D)); Qx[0, 0] = 7
+    Qw = rng.integers(-7, 8, size=(C, D)); Qw[0, 1] = -7
+    Hb = np.kron(np.eye(D // b), scipy.linalg.hadamard(b))
+    X = (2.0 ** 2 * Qx @ Hb / b).astype(np.float32)
+    W = (2.0 ** -3 * Qw @ Hb / b).astype(np.float32)
+    saved, Y = run_forward(H, X, W, k, "f32")
+    torch.cuda.synchronize()
+    assert np.array_equal(O.unpack_int4(to_np(saved.xq)), Qx)
+    exact = X.astype(np.float64) @ W.astype(np.float64).T
+    assert np.array_equal(to_np(Y).astype(np.float64), exact)
+
+
+@pytest.mark.parametrize("li", [0, 1])
+def test_bench_workload_full_size_sampled(li):
+    """BERT-base FFN pair at full size (N = 16384, fp16, b = 32), in the configuration the
+    benchmark times: codes of sampled rows, the whole sample, and sampled output blocks are
+    checked against the oracle computing them one by one."""
+    H = need_gpu()
+    lin = synth.workload(1).linears[li]
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    say(f"full-size sampled parity {lin.name} N={N} D={D} C={C}")
+    X, W, G = synth.linear_inputs(lin, 1, li)
+    saved, Y = run_forward(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)  # codes of every row (cheap)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(saved.xq), O.pack_int4(f.xq))
+    assert np.array_equal(to_np(saved.wq), O.pack_int4(f.wq))
+    rng = np.random.default_rng(0)
+    rows = rng.choice(N, 64, replace=False)
+    ref = float(f.s_x) * float(f.s_w) * 2.0 ** -k * (f.xq[rows].astype(np.float64) @ f.wq.T.astype(np.float64))
+    check_float_output("Y rows", Y[torch.from_numpy(rows).cuda()], ref, dt)
+
+    seed, offset = 42, 1000
+    b = O.lss_backward(G, f, N, seed, offset, need_dx=False, need_dw=False)
+    _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N, seed, offset)
+    nk = check_plan(plan, b)
+    say(f"  kept {nk}/{N}")
+    A = b.A.astype(np.float64)
+    kept = b.plan.kept
+    bsz = 1 << k
+    a_dx, a_dw = b.alpha_dx, b.alpha_dw
+    # dX on sampled kept tokens and dropped tokens
+    toks = rng.choice(kept, 32, replace=False)
+    accx = A[toks] @ f.wq.astype(np.float64)
+    refx = a_dx * O.fwht_rows(accx.astype(np.int64), k).astype(np.float64)
+    check_float_output("dX rows", dX[torch.from_numpy(toks).cuda()], refx, dt)
+    dropped = np.setdiff1d(np.arange(N), kept)
+    if len(dropped):
+        assert not dX[torch.from_numpy(dropped[:64]).cuda()].float().abs().sum().item()
+    # dW on sampled rows c (all D columns, so whole Hadamard blocks)
+    cs = rng.choice(C, 16, replace=False)
+    accw = A[kept][:, cs].T @ f.xq[kept].astype(np.float64)
+    refw = a_dw * O.fwht_rows(accw.astype(np.int64), k).astype(np.float64)
+    check_float_output("dW rows", dW[torch.from_numpy(cs).cuda()], refw, dt)
+    assert bsz == 32
