@@ -1,0 +1,279 @@
+"""Benchmark: INT4 HQ-MM / LSS-MM linear fwd+bwd on one MI355X.
+
+One step = forward (HQ-MM) and backward (LSS-MM: dX and dW from one shared sample) of
+both linears of the BERT-base FFN pair: N = 16384 tokens (batch 32 x seq 512),
+768 -> 3072 and 3072 -> 768, fp16 inputs, Hadamard block 32, LSS budget N.
+Inputs are seeded synthetic tensors with the paper's structure (outlier channels in X,
+heavy-tailed row norms in dY), resident in HBM before timing starts.
+
+Metric: effective TOPS = sum over linears of 6 N C D / step time (the dense-equivalent
+work of fwd + dX + dW), also as a fraction of the int8 MFMA peak, beside the same three
+GEMMs per linear in bf16 through torch (hipBLASLt) and the CPU oracle on a token slice.
+
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+INT8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
+HBM_PEAK_GBS = 8000.0
+METRIC = "INT4 linear fwd+bwd effective TOPS (fraction of int8-MFMA peak) vs bf16"
+CFG_ID = 1  # BERT-base FFN pair
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-bf16", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time")
+    return p.parse_args()
+
+
+def gemm_source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2306_11987_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` measured by rocprofv3 counters, if the committed
+    summary was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m_src = re.search(r"kernel_source_digest:\s*([0-9a-f]+)", txt)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not (m_src and m_b) or m_src.group(1) != gemm_source_digest():
+        return None
+    return float(m_b.group(1))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); "
+              "multi-GPU runs are not part of it", file=sys.stderr)
+        sys.exit(3)
+
+    import numpy as np
+    import torch
+
+    import paper_2306_11987_amd as H
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    wl = synth.workload(CFG_ID)
+    lins = wl.linears
+    N = lins[0].N
+    tdt = {"f16": torch.float16, "bf16": torch.bfloat16, "f32": torch.float32}[lins[0].dtype]
+
+    # ---- inputs resident in HBM, state and workspaces preallocated
+    L = []
+    for li, lin in enumerate(lins):
+        X, W, G = synth.linear_inputs(lin, CFG_ID, li)
+        e = dict(lin=lin,
+                 X=torch.from_numpy(X).to(dev, tdt), W=torch.from_numpy(W).to(dev, tdt),
+                 G=torch.from_numpy(G).to(dev, tdt),
+                 Y=torch.empty(lin.N, lin.C, device=dev, dtype=tdt),
+                 dX=torch.empty(lin.N, lin.D, device=dev, dtype=tdt),
+                 dW=torch.empty(lin.C, lin.D, device=dev, dtype=tdt),
+                 saved=H.Saved.empty(lin.N, lin.D, lin.C, dev),
+                 ws=H.workspace(H.WS_BWD, lin.N, lin.D, lin.C, dev),
+                 adv=H.lss_philox_offset_advance(lin.N, lin.C))
+        L.append(e)
+    del X, W, G
+    seed = 0
+    offsets = [0] * len(L)
+
+    def step():
+        for e in L:
+            H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block)
+        for i in reversed(range(len(L))):
+            e = L[i]
+            lin = e["lin"]
+            H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block, lin.budget,
+                             seed, offsets[i], e["ws"])
+            offsets[i] += e["adv"]
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    step_offsets = list(offsets)
+    H.timing_enable(True)
+    H.timing_read()  # clear
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log = H.timing_read(1 << 16)
+    H.timing_enable(False)
+    ms_step_events = (t1 - t0) * 1e3 / args.steps
+
+    # untimed rerun of the same steps without event bracketing, for the headline time
+    offsets[:] = step_offsets
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    ops_step = sum(6.0 * e["lin"].N * e["lin"].C * e["lin"].D for e in L)
+    tops = ops_step / (ms_step * 1e-3) / 1e12
+
+    # ---- per-kernel times (HIP events on the launch stream, over the timed region)
+    per = {}
+    for kid, ms in log:
+        nm = H.kernel_name(kid)
+        c = per.setdefault(nm, [0, 0.0])
+        c[0] += 1
+        c[1] += ms
+    kernels = {nm: {"launches_per_step": c[0] / args.steps, "avg_us": 1e3 * c[1] / c[0],
+                    "us_per_step": 1e3 * c[1] / args.steps} for nm, c in per.items()}
+
+    # kept tokens of the timed steps (replayed plans; needed for algorithmic GEMM ops)
+    kept = []
+    for i, e in enumerate(L):
+        lin = e["lin"]
+        plan = H.Plan.empty(lin.N, lin.C, dev)
+        off = step_offsets[i]
+        ks = []
+        for _ in range(args.steps):
+            H.lss_grad_plan(e["G"], e["saved"], plan, lin.D, lin.budget, seed, off)
+            ks.append(int(plan.n_kept.item()))
+            off += e["adv"]
+        kept.append(float(np.mean(ks)))
+
+    # dominant kernel and its roofline
+    dom = max(kernels, key=lambda k: kernels[k]["us_per_step"])
+    algo = None
+    if dom == "gemm_fwd":
+        algo = float(np.mean([2.0 * e["lin"].N * e["lin"].C * e["lin"].D for e in L]))
+    elif dom in ("gemm_dx", "gemm_dw"):
+        algo = float(np.mean([2.0 * k * e["lin"].C * e["lin"].D for k, e in zip(kept, L)]))
+    roof = None
+    if algo is not None:
+        ach = algo / (kernels[dom]["avg_us"] * 1e-6) / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS,
+                "unit": "TFLOP/s", "frac": round(ach / INT8_PEAK_TOPS, 4),
+                "traffic": committed_traffic(dom, "bert_base_ffn"),
+                "algorithmic_ops_per_launch": algo,
+                "note": "int8 MFMA ops (multiply-adds x 2) of the kept-token GEMM"}
+
+    # ---- bf16 reference: the same three GEMMs per linear through torch (hipBLASLt)
+    bf16 = None
+    if not args.no_bf16:
+        B = []
+        for e in L:
+            lin = e["lin"]
+            B.append((e["X"].to(torch.bfloat16), e["W"].to(torch.bfloat16), e["G"].to(torch.bfloat16)))
+
+        def bstep():
+            for X, W, G in B:
+                torch.matmul(X, W.t())
+                torch.matmul(G, W)
+                torch.matmul(G.t(), X)
+
+        for _ in range(args.warmup):
+            bstep()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            bstep()
+        torch.cuda.synchronize()
+        bms = (time.perf_counter() - t0) * 1e3 / args.steps
+        bf16 = {"ms_per_step": round(bms, 4), "tops": round(ops_step / (bms * 1e-3) / 1e12, 2),
+                "speedup_int4_over_bf16": round(bms / ms_step, 3)}
+
+    # ---- CPU oracle on a bounded token slice of the same workload
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(lins, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(tops, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "N": N, "linears": [[e["lin"].D, e["lin"].C] for e in L],
+                   "log2_block": lins[0].log2_block, "io_dtype": lins[0].dtype, "budget": lins[0].budget,
+                   "kept_tokens": [round(k, 1) for k in kept]},
+        "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
+        "ms_per_step_with_kernel_events": round(ms_step_events, 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "bf16": bf16,
+        "kernels": {k: {kk: round(vv, 3) for kk, vv in v.items()} for k, v in sorted(kernels.items())},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(lins, target_s: float):
+    """The oracle, as it stands, on the first n tokens of each linear (fwd + bwd)."""
+    import numpy as np
+
+    import oracle as O
+    import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+
+    def run(n):
+        ops = 0.0
+        t = 0.0
+        for li, lin in enumerate(lins):
+            sub = synth.Linear(lin.name, n, lin.D, lin.C, lin.log2_block, lin.dtype,
+                               lin.x_outlier_channels, lin.x_outlier_scale, lin.grad_kind, n)
+            X, W, G = synth.linear_inputs(sub, CFG_ID, li)
+            t0 = time.perf_counter()
+            f = O.hq_forward(X, W, lin.log2_block)
+            O.lss_backward(G, f, n, 0, 0)
+            t += time.perf_counter() - t0
+            ops += 6.0 * n * lin.C * lin.D
+        return t, ops
+
+    n = 256
+    t, ops = run(n)
+    for _ in range(3):  # grow the slice until it is about target_s of CPU work
+        if t >= 0.7 * target_s or n >= lins[0].N:
+            break
+        n = int(min(lins[0].N, max(n + 64, n * target_s / max(t, 1e-3))) // 64 * 64)
+        t, ops = run(n)
+    return {"value": round(ops / t / 1e12, 6), "unit": "TOPS", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} of {lins[0].N} tokens of each linear, fwd + bwd (budget = {n}); "
+                      f"{t:.1f} s", "seconds": round(t, 2)}
+
+
+if __name__ == "__main__":
+    main()
