@@ -96,6 +96,7 @@ def main():
                  dW=torch.empty(lin.C, lin.D, device=dev, dtype=tdt),
                  saved=H.Saved.empty(lin.N, lin.D, lin.C, dev),
                  ws=H.workspace(H.WS_BWD, lin.N, lin.D, lin.C, dev),
+                 wsf=H.workspace(H.WS_FWD, lin.N, lin.D, lin.C, dev),
                  adv=H.lss_philox_offset_advance(lin.N, lin.C))
         L.append(e)
     del X, W, G
@@ -104,7 +105,7 @@ def main():
 
     def step():
         for e in L:
-            H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block)
+            H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
         for i in reversed(range(len(L))):
             e = L[i]
             lin = e["lin"]
@@ -156,10 +157,11 @@ def main():
     for i, e in enumerate(L):
         lin = e["lin"]
         plan = H.Plan.empty(lin.N, lin.C, dev)
+        wsp = H.workspace(H.WS_PLAN, lin.N, lin.D, lin.C, dev)
         off = step_offsets[i]
         ks = []
         for _ in range(args.steps):
-            H.lss_grad_plan(e["G"], e["saved"], plan, lin.D, lin.budget, seed, off)
+            H.lss_grad_plan(e["G"], e["saved"], plan, lin.D, lin.budget, seed, off, wsp)
             ks.append(int(plan.n_kept.item()))
             off += e["adv"]
         kept.append(float(np.mean(ks)))

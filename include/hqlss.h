@@ -99,7 +99,7 @@ typedef struct {
 
 /* Workspace sizes (bytes) for the entry points below, which = HQLSS_WS_*. */
 enum { HQLSS_WS_FWD = 0, HQLSS_WS_BWD_DX = 1, HQLSS_WS_BWD_DW = 2, HQLSS_WS_BWD = 3,
-       HQLSS_WS_FROM_PLAN = 4 };
+       HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5 };
 size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C);
 
 /* HQ-MM forward (Sec. 3.3, Eq. 3; Procedure HQ-MM).
@@ -107,7 +107,8 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C);
  *   2. a_x = max|v_x|, a_w = max|v_w|; codes clamp(rint(v * fl(7/a)), -7, 7) -> saved;
  *   3. acc = X^ W^^T (int32, exact);
  *   4. Y = fl(alpha * acc), alpha = fl(fl(s_x s_w) / 2^k), cast to dt.
- * X [N][D], W [C][D] inputs; Y [N][C] output; saved: outputs (all fields required). */
+ * X [N][D], W [C][D] inputs; Y [N][C] output; saved: outputs (all fields required);
+ * ws: scratch of at least hqlss_workspace_bytes(HQLSS_WS_FWD, ...) bytes. */
 hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int64_t D,
                            int64_t C, hqlss_dtype dt, int log2_block,
                            const hqlss_saved_t *saved, void *ws, size_t ws_bytes,
@@ -121,7 +122,8 @@ hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int
  *   upper rows: kept iff non-zero; lower rows: p~ = 2^-e >= p* (e <= 4, <= 2 if the upper
  *   row is non-zero), m = [u16 < 2^(16-e)] (stream 1), weight m 2^e.
  * budget_rows <= 0 selects budget = N (Sec. 4.2: sum p_i = N).  dY [N][C] input; saved is
- * read (x_sumsq); plan: outputs (all fields required). */
+ * read (x_sumsq); plan: outputs (all fields required); ws: scratch of at least
+ * hqlss_workspace_bytes(HQLSS_WS_PLAN, ...) bytes. */
 hqlss_status lss_grad_plan(const void *dY, const hqlss_saved_t *saved, const lss_plan_t *plan,
                            int64_t N, int64_t D, int64_t C, hqlss_dtype dt,
                            int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
@@ -173,6 +175,10 @@ const char *hqlss_status_string(hqlss_status s);
 hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t *plan, const hqlss_saved_t *saved,
                                   int32_t *acc, int64_t N, int64_t D, int64_t C, void *ws,
                                   size_t ws_bytes, void *stream);
+
+/* Test hook: force the split-K factor of every integer GEMM (0 restores the built-in
+ * choice).  Workspace sizes follow the factor in force when they are queried. */
+void hqlss_debug_set_gemm_splits(int splits);
 
 /* ---- kernel timing (benchmarks) ------------------------------------------------------
  * When enabled, every kernel the library launches is bracketed by two HIP events

@@ -11,6 +11,7 @@ from ._binding import (  # noqa: F401
     Plan,
     Saved,
     debug_gemm_acc,
+    debug_set_gemm_splits,
     hq_linear_fwd,
     kernel_name,
     lib,
@@ -30,4 +31,5 @@ from ._binding import (  # noqa: F401
     WS_BWD_DW,
     WS_BWD,
     WS_FROM_PLAN,
+    WS_PLAN,
 )

@@ -11,7 +11,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhqlss.so")
 
-WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN = 0, 1, 2, 3, 4
+WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN = 0, 1, 2, 3, 4, 5
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
 _vp, _i64, _u64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int, ctypes.c_size_t
@@ -52,6 +52,7 @@ def _load() -> ctypes.CDLL:
         "hqlss_timing_enable": (st, [_int]),
         "hqlss_timing_read": (_int, [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _int]),
         "hqlss_kernel_name": (ctypes.c_char_p, [_int]),
+        "hqlss_debug_set_gemm_splits": (None, [_int]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -165,6 +166,8 @@ def hq_linear_fwd(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Save
                   ws: Optional[torch.Tensor] = None) -> None:
     N, D = X.shape
     C = W.shape[0]
+    if ws is None:
+        ws = workspace(WS_FWD, N, D, C, X.device)
     p, n = _ws(ws)
     sv = saved.c()
     _check(lib.hq_linear_fwd(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
@@ -172,11 +175,14 @@ def hq_linear_fwd(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Save
 
 
 def lss_grad_plan(dY: torch.Tensor, saved: Saved, plan: Plan, D: int, budget: int = 0, seed: int = 0,
-                  offset: int = 0) -> None:
+                  offset: int = 0, ws: Optional[torch.Tensor] = None) -> None:
     N, C = dY.shape
+    if ws is None:
+        ws = workspace(WS_PLAN, N, D, C, dY.device)
+    p, n = _ws(ws)
     sv, pl = saved.c(), plan.c()
     _check(lib.lss_grad_plan(_ptr(dY), ctypes.byref(sv), ctypes.byref(pl), N, int(D), C, _dt(dY),
-                             int(budget), int(seed), int(offset), None, 0, _stream(dY)), "lss_grad_plan")
+                             int(budget), int(seed), int(offset), p, n, _stream(dY)), "lss_grad_plan")
 
 
 def lss_linear_bwd_from_plan(plan: Plan, saved: Saved, dX: Optional[torch.Tensor],
@@ -242,6 +248,10 @@ def timing_read(cap: int = 4096):
     if n < 0:
         raise HQLSSError(8, "hqlss_timing_read")
     return [(int(ids[i]), float(ms[i])) for i in range(n)]
+
+
+def debug_set_gemm_splits(splits: int) -> None:
+    lib.hqlss_debug_set_gemm_splits(int(splits))
 
 
 def kernel_name(i: int) -> str:

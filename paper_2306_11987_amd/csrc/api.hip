@@ -76,12 +76,26 @@ hqlss_status check_plan(const lss_plan_t* p) {
 }
 
 // ---------------------------------------------------------------- workspace layout
+constexpr size_t kSlotBytes = size_t(kSlotWords) * 4;  // absmax partial slots of one tensor
+size_t fwd_gemm_partial(int64_t N, int64_t D, int64_t C) {
+  return al(gemm_partial_bytes(N, C, gemm_splits(N, C, D, true, true)));
+}
+size_t dx_gemm_partial(int64_t N, int64_t D, int64_t C) {
+  return al(gemm_partial_bytes(N, D, gemm_splits(N, D, C, false, true)));
+}
+size_t dw_gemm_partial(int64_t N, int64_t D, int64_t C) {
+  return al(gemm_partial_bytes(C, D, gemm_splits(C, D, (N + 127) / 128 * 128, false, true)));
+}
+size_t fwd_bytes(int64_t N, int64_t D, int64_t C) { return 2 * kSlotBytes + fwd_gemm_partial(N, D, C); }
+size_t plan_scratch_bytes() { return kSlotBytes; }
 size_t plan_bytes(int64_t N, int64_t C) {
   return al(N * C / 2) * 2 + al(4 * N) * 2 + al(N) * 2 + al(4 * N) + al(4) * 2;
 }
-size_t dx_bytes(int64_t N, int64_t C) { return al(rup(N, kPad) * C); }
+size_t dx_bytes(int64_t N, int64_t D, int64_t C) {
+  return al(rup(N, kPad) * C) + dx_gemm_partial(N, D, C);
+}
 size_t dw_bytes(int64_t N, int64_t D, int64_t C) {
-  return al(C * rup(N, kPad)) + al(D * rup(N, kPad) / 2);
+  return al(C * rup(N, kPad)) + al(D * rup(N, kPad) / 2) + dw_gemm_partial(N, D, C);
 }
 
 struct Carve {
@@ -122,13 +136,14 @@ constexpr size_t kLogPairs = 4096;
 
 // ---------------------------------------------------------------- the two passes
 hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
-                    int dt, int k, const hqlss_saved_t* sv, hipStream_t s) {
+                    int dt, int k, const hqlss_saved_t* sv, void* ws, hipStream_t s) {
   uint32_t* amax = reinterpret_cast<uint32_t*>(sv->amax);
-  HQ_TRY(launch_zero(s, amax, 2, reinterpret_cast<uint32_t*>(sv->x_sumsq), N));
-  HQ_TRY(launch_fwht_absmax(s, dt, k, X, N, D, amax));
-  HQ_TRY(launch_fwht_absmax(s, dt, k, W, C, D, amax + 1));
-  HQ_TRY(launch_fwht_quant(s, dt, k, X, N, D, amax, sv->xq, sv->x_sumsq));
-  HQ_TRY(launch_fwht_quant(s, dt, k, W, C, D, amax + 1, sv->wq, nullptr));
+  uint32_t* slots = static_cast<uint32_t*>(ws);  // [2][kSlotWords]
+  HQ_TRY(launch_zero(s, slots, 2 * kSlotWords, reinterpret_cast<uint32_t*>(sv->x_sumsq), N));
+  HQ_TRY(launch_fwht_absmax(s, dt, k, X, N, D, slots));
+  HQ_TRY(launch_fwht_absmax(s, dt, k, W, C, D, slots + kSlotWords));
+  HQ_TRY(launch_fwht_quant(s, dt, k, X, N, D, slots, sv->amax, sv->xq, sv->x_sumsq));
+  HQ_TRY(launch_fwht_quant(s, dt, k, W, C, D, slots + kSlotWords, sv->amax + 1, sv->wq, nullptr));
   HQ_TRY(launch_transpose_packed(s, sv->wq, C, D, sv->wqT));
   if (Y) {
     GemmArgs g{};
@@ -139,20 +154,22 @@ hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D,
     g.amax1 = amax; g.amax2 = amax + 1;
     g.denom = (float)(int64_t(1) << k);
     g.log2b = k;
-    HQ_TRY(launch_gemm(s, kEpiFwd, dt, true, true, g));
+    const int sp = gemm_splits(N, C, D, true, true);
+    int32_t* part = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * kSlotBytes);
+    HQ_TRY(launch_gemm(s, kEpiFwd, dt, true, true, g, sp, part));
   }
   return HQLSS_OK;
 }
 
 hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* p, int64_t N,
                      int64_t C, int dt, int64_t budget, uint64_t seed, uint64_t offset,
-                     hipStream_t s) {
-  uint32_t* ag = reinterpret_cast<uint32_t*>(p->amax_g);
-  HQ_TRY(launch_zero(s, ag, 1, reinterpret_cast<uint32_t*>(p->sumsq_up), N,
+                     Carve& w, hipStream_t s) {
+  uint32_t* slots = w.take<uint32_t>(kSlotBytes);
+  HQ_TRY(launch_zero(s, slots, kSlotWords, reinterpret_cast<uint32_t*>(p->sumsq_up), N,
                      reinterpret_cast<uint32_t*>(p->sumsq_dn), N));
-  HQ_TRY(launch_fwht_absmax(s, dt, 0, dY, N, C, ag));
-  HQ_TRY(launch_bit_split(s, dt, dY, N, C, ag, p->qup, p->qdn, p->sumsq_up, p->sumsq_dn, seed,
-                          offset));
+  HQ_TRY(launch_fwht_absmax(s, dt, 0, dY, N, C, slots));
+  HQ_TRY(launch_bit_split(s, dt, dY, N, C, slots, p->amax_g, p->qup, p->qdn, p->sumsq_up,
+                          p->sumsq_dn, seed, offset));
   HQ_TRY(launch_lss_plan(s, p->sumsq_up, p->sumsq_dn, sv->x_sumsq, N, budget, seed, offset,
                          p->w_up, p->w_dn, p->kept, p->n_kept));
   return HQLSS_OK;
@@ -168,6 +185,8 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   const bool want_dw = dW || (acc && which_acc == 2);
   if (want_dx) {
     int8_t* Ag = w.take<int8_t>(rup(N, kPad) * C);
+    const int sp = gemm_splits(N, D, C, false, true);
+    int32_t* part = w.take<int32_t>(gemm_partial_bytes(N, D, sp));
     HQ_TRY(launch_build_ag(s, dt, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept, N, C, D,
                            Ag, dX));
     GemmArgs g{};
@@ -178,17 +197,19 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     g.amax1 = ag; g.amax2 = amax + 1; g.denom = denom; g.log2b = k;
     if (dX) {
       g.out = dX; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiDx, dt, false, true, g));
+      HQ_TRY(launch_gemm(s, kEpiDx, dt, false, true, g, sp, part));
     }
     if (acc && which_acc == 1) {
       g.out = acc; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g));
+      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g, sp, part));
     }
   }
   if (want_dw) {
     const int64_t Kp = rup(N, kPad);
     int8_t* At = w.take<int8_t>(C * Kp);
     uint8_t* XtT = w.take<uint8_t>(D * Kp / 2);
+    const int sp = gemm_splits(C, D, Kp, false, true);
+    int32_t* part = w.take<int32_t>(gemm_partial_bytes(C, D, sp));
     HQ_TRY(launch_build_dw_operands(s, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept,
                                     sv->xq, N, C, D, At, XtT));
     GemmArgs g{};
@@ -198,11 +219,11 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     g.amax1 = ag; g.amax2 = amax; g.denom = denom; g.log2b = k;
     if (dW) {
       g.out = dW; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiDw, dt, false, true, g));
+      HQ_TRY(launch_gemm(s, kEpiDw, dt, false, true, g, sp, part));
     }
     if (acc && which_acc == 2) {
       g.out = acc; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g));
+      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g, sp, part));
     }
   }
   return HQLSS_OK;
@@ -229,7 +250,8 @@ namespace hqlss {
 const char* kernel_name(int id) {
   static const char* names[kKCount] = {"zero", "fwht_absmax", "fwht_quant", "transpose_packed",
                                        "bit_split", "lss_plan", "build_ag", "build_dw_operands",
-                                       "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc"};
+                                       "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
+                                       "gemm_reduce"};
   return (id >= 0 && id < kKCount) ? names[id] : "?";
 }
 
@@ -252,11 +274,13 @@ extern "C" {
 size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
   if (N < 1 || D < 1 || C < 1) return 0;
   switch (which) {
-    case HQLSS_WS_FWD: return 0;
-    case HQLSS_WS_BWD_DX: return plan_bytes(N, C) + dx_bytes(N, C);
-    case HQLSS_WS_BWD_DW: return plan_bytes(N, C) + dw_bytes(N, D, C);
-    case HQLSS_WS_BWD: return plan_bytes(N, C) + dx_bytes(N, C) + dw_bytes(N, D, C);
-    case HQLSS_WS_FROM_PLAN: return dx_bytes(N, C) + dw_bytes(N, D, C);
+    case HQLSS_WS_FWD: return fwd_bytes(N, D, C);
+    case HQLSS_WS_BWD_DX: return plan_bytes(N, C) + plan_scratch_bytes() + dx_bytes(N, D, C);
+    case HQLSS_WS_BWD_DW: return plan_bytes(N, C) + plan_scratch_bytes() + dw_bytes(N, D, C);
+    case HQLSS_WS_BWD:
+      return plan_bytes(N, C) + plan_scratch_bytes() + dx_bytes(N, D, C) + dw_bytes(N, D, C);
+    case HQLSS_WS_FROM_PLAN: return dx_bytes(N, D, C) + dw_bytes(N, D, C);
+    case HQLSS_WS_PLAN: return plan_scratch_bytes();
   }
   return 0;
 }
@@ -285,7 +309,6 @@ const char* hqlss_status_string(hqlss_status s) {
 hqlss_status hq_linear_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
                            hqlss_dtype dt, int log2_block, const hqlss_saved_t* saved, void* ws,
                            size_t ws_bytes, void* stream) {
-  (void)ws; (void)ws_bytes;
   if (!X || !W || !Y) return HQLSS_ERR_NULL;
   hqlss_status st;
   if ((st = check_shape(N, D, C))) return st;
@@ -294,19 +317,23 @@ hqlss_status hq_linear_fwd(const void* X, const void* W, void* Y, int64_t N, int
   if ((st = check_saved(saved))) return st;
   if (!a16(X) || !a16(W) || !a16(Y)) return HQLSS_ERR_ALIGN;
   if ((st = check_fwd_overflow(D))) return st;
-  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, static_cast<hipStream_t>(stream));
+  if (!ws || ws_bytes < fwd_bytes(N, D, C)) return HQLSS_ERR_WORKSPACE;
+  if (!a16(ws)) return HQLSS_ERR_ALIGN;
+  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
 }
 
 hqlss_status lss_grad_plan(const void* dY, const hqlss_saved_t* saved, const lss_plan_t* plan,
                            int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int64_t budget_rows,
                            uint64_t seed, uint64_t offset, void* ws, size_t ws_bytes,
                            void* stream) {
-  (void)ws; (void)ws_bytes;
   hqlss_status st;
   if ((st = check_bwd_common(dY, saved, N, D, C, dt, 0, budget_rows))) return st;
   if ((st = check_plan(plan))) return st;
+  if (!ws || ws_bytes < plan_scratch_bytes()) return HQLSS_ERR_WORKSPACE;
+  if (!a16(ws)) return HQLSS_ERR_ALIGN;
   const int64_t B = budget_rows <= 0 ? N : budget_rows;
-  return do_plan(dY, saved, plan, N, C, dt, B, seed, offset, static_cast<hipStream_t>(stream));
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  return do_plan(dY, saved, plan, N, C, dt, B, seed, offset, w, static_cast<hipStream_t>(stream));
 }
 
 hqlss_status lss_linear_bwd_from_plan(const lss_plan_t* plan, const hqlss_saved_t* saved,
@@ -322,7 +349,7 @@ hqlss_status lss_linear_bwd_from_plan(const lss_plan_t* plan, const hqlss_saved_
   if ((st = check_plan(plan))) return st;
   if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
   if ((st = check_bwd_overflow(N, D, C, log2_block))) return st;
-  const size_t need = (dX ? dx_bytes(N, C) : 0) + (dW ? dw_bytes(N, D, C) : 0);
+  const size_t need = (dX ? dx_bytes(N, D, C) : 0) + (dW ? dw_bytes(N, D, C) : 0);
   if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
   Carve w{static_cast<char*>(ws), 0, ws_bytes};
   return do_grads(plan, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w,
@@ -337,14 +364,15 @@ static hqlss_status bwd_impl(const void* dY, const hqlss_saved_t* saved, void* d
   hqlss_status st;
   if ((st = check_bwd_common(dY, saved, N, D, C, dt, log2_block, budget_rows))) return st;
   if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
-  const size_t need = plan_bytes(N, C) + (dX ? dx_bytes(N, C) : 0) + (dW ? dw_bytes(N, D, C) : 0);
+  const size_t need = plan_bytes(N, C) + plan_scratch_bytes() + (dX ? dx_bytes(N, D, C) : 0) +
+                      (dW ? dw_bytes(N, D, C) : 0);
   if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Carve w{static_cast<char*>(ws), 0, ws_bytes};
   lss_plan_t p;
   plan_from_ws(w, N, C, &p);
   const int64_t B = budget_rows <= 0 ? N : budget_rows;
-  if ((st = do_plan(dY, saved, &p, N, C, dt, B, seed, offset, s))) return st;
+  if ((st = do_plan(dY, saved, &p, N, C, dt, B, seed, offset, w, s))) return st;
   return do_grads(&p, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w, s);
 }
 
@@ -390,12 +418,16 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t* plan, const hqlss
     g.B = saved->wq; g.ldb = D / 2;
     g.M = N; g.N = C; g.K = D;
     g.out = acc; g.ldo = C;
-    return hip_status(launch_gemm(s, kEpiAcc, HQLSS_F32, true, true, g));
+    const int sp = gemm_splits(N, C, D, true, true);
+    if (sp > 1 && (!ws || ws_bytes < fwd_bytes(N, D, C))) return HQLSS_ERR_WORKSPACE;
+    int32_t* part = sp > 1 ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * kSlotBytes)
+                           : nullptr;
+    return hip_status(launch_gemm(s, kEpiAcc, HQLSS_F32, true, true, g, sp, part));
   }
   if (which != 1 && which != 2) return HQLSS_ERR_ARG;
   if ((st = check_plan(plan))) return st;
   if ((st = check_bwd_overflow(N, D, C, 0))) return st;
-  const size_t need = which == 1 ? dx_bytes(N, C) : dw_bytes(N, D, C);
+  const size_t need = which == 1 ? dx_bytes(N, D, C) : dw_bytes(N, D, C);
   if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
   if (!a16(ws)) return HQLSS_ERR_ALIGN;
   Carve w{static_cast<char*>(ws), 0, ws_bytes};
@@ -436,5 +468,7 @@ int hqlss_timing_read(int* ids, float* ms, int cap) {
 }
 
 const char* hqlss_kernel_name(int id) { return hqlss::kernel_name(id); }
+
+void hqlss_debug_set_gemm_splits(int splits) { hqlss::gemm_set_split_override(splits); }
 
 }  // extern "C"

@@ -8,6 +8,9 @@ namespace hqlss {
 constexpr int kWave = 64;
 constexpr int kQmax = 7;      // Q_N = Q_P = 7 (Sec. 3.1)
 constexpr int kBsRatio = 14;  // s_up / s_dn of the bit split
+constexpr int kSlots = 64;      // per-tensor absmax partial slots
+constexpr int kSlotStride = 32; // 32 words = one 128-byte line per slot
+constexpr int kSlotWords = kSlots * kSlotStride;
 
 enum Dt : int { kF32 = 0, kF16 = 1, kBF16 = 2 };
 

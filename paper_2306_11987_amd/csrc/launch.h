@@ -8,7 +8,7 @@ namespace hqlss {
 // Kernel ids for the timing log (kept in sync with kernel_name()).
 enum KernelId : int {
   kKZero = 0, kKAbsmax, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuildAg, kKBuildDw,
-  kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKCount
+  kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCount
 };
 const char* kernel_name(int id);
 
@@ -21,19 +21,21 @@ hipError_t launch_zero(hipStream_t s, uint32_t* p0, int64_t n0, uint32_t* p1 = n
                        int64_t n1 = 0, uint32_t* p2 = nullptr, int64_t n2 = 0,
                        uint32_t* p3 = nullptr, int64_t n3 = 0);
 
-// max |rows x cols block-FWHT(src)| -> atomicMax into *amax_bits (fp32 bit pattern).
+// max |rows x cols block-FWHT(src)| -> atomicMax into kSlots zeroed slots (kSlotWords
+// words, fp32 bit patterns); consumers reduce the slots.
 hipError_t launch_fwht_absmax(hipStream_t s, int dt, int log2b, const void* src, int64_t rows,
-                              int64_t cols, uint32_t* amax_bits);
-// codes of block-FWHT(src) -> packed [rows][cols/2]; optional per-row sum of squares.
+                              int64_t cols, uint32_t* slots);
+// codes of block-FWHT(src) -> packed [rows][cols/2]; optional per-row sum of squares;
+// the reduced maximum is also stored to *amax_out.
 hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const void* src, int64_t rows,
-                             int64_t cols, const uint32_t* amax_bits, uint8_t* packed,
-                             int32_t* row_sumsq);
+                             int64_t cols, const uint32_t* slots, float* amax_out,
+                             uint8_t* packed, int32_t* row_sumsq);
 // packed [rows][cols/2] -> packed [cols][rows/2] (rows, cols multiples of 64).
 hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t rows, int64_t cols,
                                    uint8_t* dst);
 // bit split of dY [N][C] into two packed code planes and their row sums of squares.
 hipError_t launch_bit_split(hipStream_t s, int dt, const void* g, int64_t N, int64_t C,
-                            const uint32_t* amax_bits, uint8_t* qup, uint8_t* qdn,
+                            const uint32_t* slots, float* amax_out, uint8_t* qup, uint8_t* qdn,
                             int32_t* sumsq_up, int32_t* sumsq_dn, uint64_t seed,
                             uint64_t offset);
 // leverage scores, clamp-rescale, masks, compaction (one workgroup).
@@ -55,7 +57,7 @@ hipError_t launch_build_dw_operands(hipStream_t s, const uint8_t* qup, const uin
                                     int8_t* At, uint8_t* XtT);
 
 // Integer GEMM  acc[m][n] = sum_k A[m][k] B[n][k]  (both operands K-contiguous rows).
-enum Epi : int { kEpiFwd = 0, kEpiDx = 1, kEpiDw = 2, kEpiAcc = 3 };
+enum Epi : int { kEpiFwd = 0, kEpiDx = 1, kEpiDw = 2, kEpiAcc = 3, kEpiPartial = 4 };
 struct GemmArgs {
   const void* A;        // [M][lda] bytes: packed int4 (a_int4) or K-interleaved int8
   const void* B;        // [N][ldb] bytes
@@ -71,7 +73,12 @@ struct GemmArgs {
   float denom;                 // alpha = fl(fl(s1 s2) / denom)
   int log2b;                   // FWHT block of the gradient epilogues
 };
-hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4,
-                       const GemmArgs& g);
+// Split-K factor the launcher uses for this shape (1 = no split), and the int32 partial
+// buffer it then needs (splits x M x N words).  A non-zero override forces the factor.
+int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4);
+size_t gemm_partial_bytes(int64_t M, int64_t N, int splits);
+void gemm_set_split_override(int splits);
+hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4, const GemmArgs& g,
+                       int splits, int32_t* partial);
 
 }  // namespace hqlss

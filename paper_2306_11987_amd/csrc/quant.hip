@@ -14,7 +14,7 @@
 // b = 2^k <= 128 columns then lives in b/8 consecutive lanes, so strides 1..4 run in
 // registers and strides 8..64 across lanes.  Per-row results reduce inside the wave and
 // land with one integer atomic per (row, chunk); per-tensor maxima with one atomic per
-// wave.  All loads are 16-byte vectors, fully coalesced along the row.
+// workgroup into one of 64 slots.  All loads are 16-byte vectors, coalesced along the row.
 #include "common.h"
 #include "launch.h"
 
@@ -24,6 +24,13 @@ namespace {
 
 constexpr int kChunk = 512;  // columns per wave item (64 lanes x 8)
 constexpr int kThreads = 256;
+
+// Per-tensor maxima land in kSlots words, one 128-byte line apart, so that the
+// workgroups' atomics spread over many L2 channels; a consumer wave reduces them
+// (one slot per lane).
+__device__ __forceinline__ float read_slots(const uint32_t* __restrict__ slots) {
+  return wave_max(__uint_as_float(slots[(threadIdx.x & 63) * kSlotStride]));
+}
 
 template <int LOG2B>
 __device__ __forceinline__ void fwht8(float v[8], int lane) {
@@ -78,19 +85,19 @@ __global__ __launch_bounds__(kThreads) void zero_kernel(uint32_t* p0, int64_t n0
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kThreads) void fwht_absmax_kernel(const void* __restrict__ src,
                                                                int64_t rows, int64_t cols,
-                                                               uint32_t* __restrict__ amax) {
+                                                               uint32_t* __restrict__ slots) {
+  __shared__ float wmax[kThreads / kWave];
   const int lane = threadIdx.x & 63;
-  const int64_t chunks = (cols + kChunk - 1) / kChunk;
-  const int64_t items = rows * chunks;
-  const int64_t nwaves = (int64_t)gridDim.x * (kThreads / kWave);
+  const uint32_t chunks = (uint32_t)((cols + kChunk - 1) / kChunk);
+  const uint32_t items = (uint32_t)rows * chunks;
+  const uint32_t nwaves = gridDim.x * (kThreads / kWave);
   float m = 0.f;
-  for (int64_t it = (int64_t)blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items;
-       it += nwaves) {
-    const int64_t row = it / chunks;
-    const int64_t col = (it - row * chunks) * kChunk + lane * 8;
+  for (uint32_t it = blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items; it += nwaves) {
+    const uint32_t row = it / chunks;
+    const int64_t col = (int64_t)(it - row * chunks) * kChunk + lane * 8;
     float v[8];
     if (col < cols) {
-      load8<DT>(static_cast<const char*>(src) + (row * cols + col) * Elem<DT>::bytes, v);
+      load8<DT>(static_cast<const char*>(src) + ((int64_t)row * cols + col) * Elem<DT>::bytes, v);
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = 0.f;
@@ -100,27 +107,33 @@ __global__ __launch_bounds__(kThreads) void fwht_absmax_kernel(const void* __res
     for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(v[j]));
   }
   m = wave_max(m);
-  if (lane == 0 && m > 0.f) atomicMax(amax, __float_as_uint(m));  // |v| >= 0: uint order
+  if (lane == 0) wmax[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+    // one atomic per workgroup, spread over kSlots cache lines; |v| >= 0: uint order
+    if (m > 0.f) atomicMax(slots + (blockIdx.x % kSlots) * kSlotStride, __float_as_uint(m));
+  }
 }
 
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kThreads) void fwht_quant_kernel(
-    const void* __restrict__ src, int64_t rows, int64_t cols, const uint32_t* __restrict__ amax,
-    uint8_t* __restrict__ packed, int32_t* __restrict__ row_sumsq) {
+    const void* __restrict__ src, int64_t rows, int64_t cols, const uint32_t* __restrict__ slots,
+    float* __restrict__ amax_out, uint8_t* __restrict__ packed, int32_t* __restrict__ row_sumsq) {
   const int lane = threadIdx.x & 63;
-  const int64_t chunks = (cols + kChunk - 1) / kChunk;
-  const int64_t items = rows * chunks;
-  const int64_t nwaves = (int64_t)gridDim.x * (kThreads / kWave);
-  const float a = __uint_as_float(*amax);
+  const uint32_t chunks = (uint32_t)((cols + kChunk - 1) / kChunk);
+  const uint32_t items = (uint32_t)rows * chunks;
+  const uint32_t nwaves = gridDim.x * (kThreads / kWave);
+  const float a = read_slots(slots);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *amax_out = a;
   const float inv = a > 0.f ? 7.0f / a : 0.f;
-  for (int64_t it = (int64_t)blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items;
-       it += nwaves) {
-    const int64_t row = it / chunks;
-    const int64_t col = (it - row * chunks) * kChunk + lane * 8;
+  for (uint32_t it = blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items; it += nwaves) {
+    const uint32_t row = it / chunks;
+    const int64_t col = (int64_t)(it - row * chunks) * kChunk + lane * 8;
     const bool live = col < cols;
     float v[8];
     if (live) {
-      load8<DT>(static_cast<const char*>(src) + (row * cols + col) * Elem<DT>::bytes, v);
+      load8<DT>(static_cast<const char*>(src) + ((int64_t)row * cols + col) * Elem<DT>::bytes, v);
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = 0.f;
@@ -133,7 +146,7 @@ __global__ __launch_bounds__(kThreads) void fwht_quant_kernel(
       q[j] = code_of(v[j], inv);
       ss += q[j] * q[j];
     }
-    if (live) *reinterpret_cast<uint32_t*>(packed + row * (cols / 2) + col / 2) = pack8(q);
+    if (live) *reinterpret_cast<uint32_t*>(packed + (int64_t)row * (cols / 2) + col / 2) = pack8(q);
     if (row_sumsq) {
       ss = wave_sum(ss);
       if (lane == 0 && ss) atomicAdd(row_sumsq + row, ss);
@@ -175,19 +188,20 @@ __global__ __launch_bounds__(kThreads) void transpose_packed_kernel(const uint8_
 
 template <int DT>
 __global__ __launch_bounds__(kThreads) void bit_split_kernel(
-    const void* __restrict__ g, int64_t N, int64_t C, const uint32_t* __restrict__ amax,
-    uint8_t* __restrict__ qup, uint8_t* __restrict__ qdn, int32_t* __restrict__ sumsq_up,
-    int32_t* __restrict__ sumsq_dn, uint64_t seed, uint64_t offset) {
+    const void* __restrict__ g, int64_t N, int64_t C, const uint32_t* __restrict__ slots,
+    float* __restrict__ amax_out, uint8_t* __restrict__ qup, uint8_t* __restrict__ qdn,
+    int32_t* __restrict__ sumsq_up, int32_t* __restrict__ sumsq_dn, uint64_t seed,
+    uint64_t offset) {
   const int lane = threadIdx.x & 63;
-  const int64_t chunks = (C + kChunk - 1) / kChunk;
-  const int64_t items = N * chunks;
-  const int64_t nwaves = (int64_t)gridDim.x * (kThreads / kWave);
-  const float a = __uint_as_float(*amax);
+  const uint32_t chunks = (uint32_t)((C + kChunk - 1) / kChunk);
+  const uint32_t items = (uint32_t)N * chunks;
+  const uint32_t nwaves = gridDim.x * (kThreads / kWave);
+  const float a = read_slots(slots);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *amax_out = a;
   const float inv = a > 0.f ? 7.0f / a : 0.f;
-  for (int64_t it = (int64_t)blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items;
-       it += nwaves) {
+  for (uint32_t it = blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items; it += nwaves) {
     const int64_t row = it / chunks;
-    const int64_t col = (it - row * chunks) * kChunk + lane * 8;
+    const int64_t col = (int64_t)(it - (uint32_t)row * chunks) * kChunk + lane * 8;
     const bool live = col < C;
     float v[8];
     if (live) {
@@ -229,27 +243,27 @@ __global__ __launch_bounds__(kThreads) void bit_split_kernel(
 // Enough waves to fill the chip several times over; every wave loops over items.
 int grid_for(int64_t items) {
   int64_t wg = (items + (kThreads / kWave) - 1) / (kThreads / kWave);
-  if (wg > 256 * 16) wg = 256 * 16;
+  if (wg > 2048) wg = 2048;
   if (wg < 1) wg = 1;
   return (int)wg;
 }
 
 template <int DT, int LOG2B>
-hipError_t absmax_t(hipStream_t s, const void* src, int64_t rows, int64_t cols, uint32_t* amax) {
+hipError_t absmax_t(hipStream_t s, const void* src, int64_t rows, int64_t cols, uint32_t* slots) {
   const int64_t items = rows * ((cols + kChunk - 1) / kChunk);
   timing_begin(s);
-  fwht_absmax_kernel<DT, LOG2B><<<grid_for(items), kThreads, 0, s>>>(src, rows, cols, amax);
+  fwht_absmax_kernel<DT, LOG2B><<<grid_for(items), kThreads, 0, s>>>(src, rows, cols, slots);
   timing_end(s, kKAbsmax);
   return hipGetLastError();
 }
 
 template <int DT, int LOG2B>
 hipError_t quant_t(hipStream_t s, const void* src, int64_t rows, int64_t cols,
-                   const uint32_t* amax, uint8_t* packed, int32_t* row_sumsq) {
+                   const uint32_t* slots, float* amax_out, uint8_t* packed, int32_t* row_sumsq) {
   const int64_t items = rows * ((cols + kChunk - 1) / kChunk);
   timing_begin(s);
   fwht_quant_kernel<DT, LOG2B>
-      <<<grid_for(items), kThreads, 0, s>>>(src, rows, cols, amax, packed, row_sumsq);
+      <<<grid_for(items), kThreads, 0, s>>>(src, rows, cols, slots, amax_out, packed, row_sumsq);
   timing_end(s, kKQuant);
   return hipGetLastError();
 }
@@ -276,8 +290,8 @@ template <int DT, int LOG2B> struct AbsmaxF {
 };
 template <int DT, int LOG2B> struct QuantF {
   static hipError_t run(hipStream_t s, const void* src, int64_t r, int64_t c, const uint32_t* a,
-                        uint8_t* p, int32_t* ss) {
-    return quant_t<DT, LOG2B>(s, src, r, c, a, p, ss);
+                        float* ao, uint8_t* p, int32_t* ss) {
+    return quant_t<DT, LOG2B>(s, src, r, c, a, ao, p, ss);
   }
 };
 
@@ -308,15 +322,15 @@ hipError_t launch_fwht_absmax(hipStream_t s, int dt, int log2b, const void* src,
 }
 
 hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const void* src, int64_t rows,
-                             int64_t cols, const uint32_t* amax_bits, uint8_t* packed,
+                             int64_t cols, const uint32_t* slots, float* amax_out, uint8_t* packed,
                              int32_t* row_sumsq) {
   switch (dt) {
     case kF32:
-      return dispatch_block<QuantF, kF32>(log2b, s, src, rows, cols, amax_bits, packed, row_sumsq);
+      return dispatch_block<QuantF, kF32>(log2b, s, src, rows, cols, slots, amax_out, packed, row_sumsq);
     case kF16:
-      return dispatch_block<QuantF, kF16>(log2b, s, src, rows, cols, amax_bits, packed, row_sumsq);
+      return dispatch_block<QuantF, kF16>(log2b, s, src, rows, cols, slots, amax_out, packed, row_sumsq);
     case kBF16:
-      return dispatch_block<QuantF, kBF16>(log2b, s, src, rows, cols, amax_bits, packed, row_sumsq);
+      return dispatch_block<QuantF, kBF16>(log2b, s, src, rows, cols, slots, amax_out, packed, row_sumsq);
   }
   return hipErrorInvalidValue;
 }
@@ -331,7 +345,7 @@ hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t ro
 }
 
 hipError_t launch_bit_split(hipStream_t s, int dt, const void* g, int64_t N, int64_t C,
-                            const uint32_t* amax_bits, uint8_t* qup, uint8_t* qdn,
+                            const uint32_t* slots, float* amax_out, uint8_t* qup, uint8_t* qdn,
                             int32_t* sumsq_up, int32_t* sumsq_dn, uint64_t seed,
                             uint64_t offset) {
   const int64_t items = N * ((C + kChunk - 1) / kChunk);
@@ -339,15 +353,15 @@ hipError_t launch_bit_split(hipStream_t s, int dt, const void* g, int64_t N, int
   timing_begin(s);
   switch (dt) {
     case kF32:
-      bit_split_kernel<kF32><<<grid, kThreads, 0, s>>>(g, N, C, amax_bits, qup, qdn, sumsq_up,
+      bit_split_kernel<kF32><<<grid, kThreads, 0, s>>>(g, N, C, slots, amax_out, qup, qdn, sumsq_up,
                                                       sumsq_dn, seed, offset);
       break;
     case kF16:
-      bit_split_kernel<kF16><<<grid, kThreads, 0, s>>>(g, N, C, amax_bits, qup, qdn, sumsq_up,
+      bit_split_kernel<kF16><<<grid, kThreads, 0, s>>>(g, N, C, slots, amax_out, qup, qdn, sumsq_up,
                                                       sumsq_dn, seed, offset);
       break;
     case kBF16:
-      bit_split_kernel<kBF16><<<grid, kThreads, 0, s>>>(g, N, C, amax_bits, qup, qdn, sumsq_up,
+      bit_split_kernel<kBF16><<<grid, kThreads, 0, s>>>(g, N, C, slots, amax_out, qup, qdn, sumsq_up,
                                                        sumsq_dn, seed, offset);
       break;
     default:

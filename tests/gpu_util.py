@@ -82,7 +82,7 @@ def check_forward(H, X, W, k, dt, saved, Y, f=None):
     assert np.array_equal(to_np(saved.wqT), O.pack_int4(f.wq.T.copy())), "W^T codes"
     assert np.array_equal(to_np(saved.x_sumsq), f.x_sumsq.astype(np.int32)), "x_sumsq"
     acc = torch.empty(N, C, dtype=torch.int32, device="cuda")
-    H.debug_gemm_acc(0, None, saved, acc, N, D, C)
+    H.debug_gemm_acc(0, None, saved, acc, N, D, C, H.workspace(H.WS_FWD, N, D, C))
     torch.cuda.synchronize()
     assert np.array_equal(to_np(acc), f.acc.astype(np.int32)), "forward int32 accumulators"
     return check_float_output("Y", Y, f.Y, dt)

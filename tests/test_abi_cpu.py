@@ -52,7 +52,8 @@ def test_workspace_sizes_monotone():
         a = H.workspace_bytes(which, 128, 256, 256)
         b = H.workspace_bytes(which, 16384, 768, 3072)
         assert b >= a >= 0
-    assert H.workspace_bytes(H.WS_FWD, 128, 256, 256) == 0
+    assert H.workspace_bytes(H.WS_FWD, 128, 256, 256) == H.workspace_bytes(H.WS_FWD, 16384, 768, 3072) > 0
+    assert H.workspace_bytes(H.WS_PLAN, 128, 256, 256) > 0
     assert H.workspace_bytes(H.WS_BWD, 128, 256, 256) >= H.workspace_bytes(H.WS_BWD_DX, 128, 256, 256)
     assert H.workspace_bytes(H.WS_BWD, 0, 256, 256) == 0
 
@@ -78,7 +79,7 @@ def _saved(**over):
 
 def fwd(X=FAKE, W=FAKE, Y=FAKE, N=128, D=256, C=256, dt=0, k=5, saved=None):
     s = saved if saved is not None else _saved()
-    return lib.hq_linear_fwd(X, W, Y, N, D, C, dt, k, ctypes.byref(s), None, 0, None)
+    return lib.hq_linear_fwd(X, W, Y, N, D, C, dt, k, ctypes.byref(s), FAKE, 1 << 40, None)
 
 
 def test_fwd_argument_errors():
@@ -94,6 +95,9 @@ def test_fwd_argument_errors():
     assert fwd(X=FAKE + 4) == ALIGN
     assert fwd(saved=_saved(xq=FAKE + 8)) == ALIGN
     assert fwd(D=1 << 20, C=64, N=1) == OVF  # 256 * 49 * D >= 2^31
+    s = _saved()
+    assert lib.hq_linear_fwd(FAKE, FAKE, FAKE, 128, 256, 256, 0, 5, ctypes.byref(s), None, 0, None) == WS
+    assert lib.hq_linear_fwd(FAKE, FAKE, FAKE, 128, 256, 256, 0, 5, ctypes.byref(s), FAKE, 16, None) == WS
 
 
 def bwd(dY=FAKE, dX=FAKE, dW=FAKE, N=128, D=256, C=256, dt=0, k=5, budget=0, ws=FAKE, nbytes=1 << 40):

@@ -24,6 +24,7 @@ SHAPES = [
     (77, 512, 576, 3, "f16", "pareto"),
     (300, 1024, 384, 5, "bf16", "lognormal"),
     (517, 128, 704, 1, "f32", "pareto"),
+    (2048, 256, 256, 5, "f16", "lognormal"),  # dW over 2048 tokens: split-K by default
 ]
 
 
@@ -175,3 +176,25 @@ def test_bench_workload_full_size_sampled(li):
     refw = a_dw * O.fwht_rows(accw.astype(np.int64), k).astype(np.float64)
     check_float_output("dW rows", dW[torch.from_numpy(cs).cuda()], refw, dt)
     assert bsz == 32
+
+
+@pytest.mark.parametrize("splits", [2, 3])
+def test_forced_split_k_parity(splits):
+    """Every GEMM split along K into int32 partials and re-summed: still bit-exact."""
+    H = need_gpu()
+    lin, X, W, G = _case((600, 1024, 512, 7, "bf16", "pareto"), seed=4)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    say(f"forced split-K {splits}")
+    H.debug_set_gemm_splits(splits)
+    try:
+        saved, Y = run_forward(H, X, W, k, dt)
+        check_forward(H, X, W, k, dt, saved, Y)
+        f = O.hq_forward(X, W, k, compute_output=False)
+        b = O.lss_backward(G, f, N // 2, 5, 0)
+        _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N // 2, 5, 0)
+        check_plan(plan, b)
+        check_backward_acc(H, plan, saved, b, N, D, C)
+        check_float_output("dX", dX, b.dX, dt)
+        check_float_output("dW", dW, b.dW, dt)
+    finally:
+        H.debug_set_gemm_splits(0)
