@@ -17,9 +17,11 @@
 // and as the reduction over k is order-free the product is exact.  The factor 16 per INT4
 // operand is a power of two, removed by an arithmetic shift.
 //
-// Tiling: a 256 x 256 tile per 256-thread workgroup (one per CU), 2 x 2 waves of 128 x 128,
-// each wave a grid of 4 x 4 MFMA 32 x 32 tiles with its accumulators in AGPRs.  Large wave
-// tiles keep the fragment reads (and the INT4 widening after them) at 0.5 per MFMA.  The MFMA "A" operand carries the n rows and the "B"
+// Tiling: a BM x 256 tile per 256-thread workgroup, 2 x 2 waves.  INT4 x INT4 (forward) uses
+// BM = 256, one workgroup per CU, wave tiles of 128 x 128 (4 x 4 MFMA 32 x 32 tiles,
+// accumulators in AGPRs), keeping fragment reads and INT4 widening at 0.5 per MFMA.  The
+// int8 x INT4 gradient GEMMs use BM = 128 with two workgroups per CU, so that one
+// workgroup's stage boundaries and epilogue overlap the other's MFMAs.  The MFMA "A" operand carries the n rows and the "B"
 // operand the m rows, so that a lane's accumulators run along n: lane l, MFMA tile (i, j),
 // register r holds m = 32 i + (l % 32) and n = 16 j + r + (BN/4) (l / 32) of the wave tile.
 // This is arranged by storing the B rows in LDS in that permuted slot order.  Each lane then
@@ -46,7 +48,9 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
-constexpr int kBM = 256, kBN = 256;  // workgroup tile (m x n); one workgroup per CU
+constexpr int kBN = 256;  // workgroup tile width (n)
+// tile height: 256 (one workgroup per CU) for INT4 x INT4, 128 (two per CU) for int8 x INT4
+template <bool A4> constexpr int tile_m() { return A4 ? 256 : 128; }
 
 template <int BM, int BN, bool A4, bool B4>
 struct Cfg {
@@ -55,8 +59,11 @@ struct Cfg {
   static constexpr int B_ROW = B4 ? KS / 2 : KS;
   // 144-byte row pitch: the fragment reads (rows lane % 32, 16-byte column lane / 32) are
   // free of LDS bank conflicts at this pitch (measured); 64-byte rows use it too.
-  static constexpr int A_PITCH = 144;
-  static constexpr int B_PITCH = 144;
+  // 128-row tiles run two workgroups per CU: their 64-byte INT4 rows take an 80-byte pitch
+  // (a few bank conflicts) so that two double-buffered stages fit in 80 KB.
+  static constexpr int A_PITCH = (BM == 128 && A_ROW == 64) ? 80 : 144;
+  static constexpr int B_PITCH = (BM == 128 && B_ROW == 64) ? 80 : 144;
+  static constexpr int OCC = BM == 128 ? 2 : 1;  // workgroups per CU
   static constexpr int A_BUF = BM * A_PITCH, B_BUF = BN * B_PITCH;
   static constexpr int STAGE = A_BUF + B_BUF;
   static constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
@@ -167,7 +174,7 @@ __device__ __forceinline__ void tile_of(int& tm, int& tn) {
 }
 
 template <int BM, int BN, bool A4, bool B4, int EPI, int DT>
-__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs g) {
+__global__ __launch_bounds__(kThreads, (BM == 128 ? 2 : 1)) void gemm_kernel(GemmArgs g) {
   using C_ = Cfg<BM, BN, A4, B4>;
   constexpr int TI = C_::TI, TJ = C_::TJ;
   // epilogue staging: rows of BN output elements of ES bytes, written back row-contiguous
@@ -487,11 +494,11 @@ hipError_t reduce_dt(hipStream_t s, const int32_t* P, int S, const GemmArgs& g) 
 
 template <bool A4, bool B4, int EPI, int DT>
 hipError_t run(hipStream_t s, const GemmArgs& g, int splits, int32_t* partial, int id) {
-  if (splits <= 1) return gemm_t<kBM, kBN, A4, B4, EPI, DT>(s, g, 1, id);
+  if (splits <= 1) return gemm_t<tile_m<A4>(), kBN, A4, B4, EPI, DT>(s, g, 1, id);
   GemmArgs p = g;
   p.out = partial;
   p.ldo = g.N;
-  hipError_t e = gemm_t<kBM, kBN, A4, B4, kEpiPartial, DT>(s, p, splits, id);
+  hipError_t e = gemm_t<tile_m<A4>(), kBN, A4, B4, kEpiPartial, DT>(s, p, splits, id);
   if (e != hipSuccess) return e;
   GemmArgs r = g;
   return reduce_dt<EPI, DT>(s, partial, splits, r);
@@ -513,13 +520,14 @@ static int g_split_override = 0;
 void gemm_set_split_override(int splits) { g_split_override = splits < 0 ? 0 : splits; }
 
 int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4) {
-  (void)a_int4; (void)b_int4;
+  (void)b_int4;
   if (g_split_override) return g_split_override;
-  const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  const int64_t bm = a_int4 ? 256 : 128, slots = a_int4 ? 256 : 512;  // workgroups in flight
+  const int64_t tiles = ((M + bm - 1) / bm) * ((N + kBN - 1) / kBN);
   const int64_t stages = (K + 127) / 128;  // in units of 128 k
-  if (tiles >= 128 || stages < 16) return 1;
-  int64_t s = (256 + tiles - 1) / tiles;  // about one workgroup per CU
-  const int64_t smax = stages / 8;        // keep >= 8 stages per split
+  if (2 * tiles >= slots || stages < 16) return 1;
+  int64_t s = (slots + tiles - 1) / tiles;  // about one workgroup per slot
+  const int64_t smax = stages / 8;          // keep >= 8 stages per split
   if (s > smax) s = smax;
   return (int)(s < 1 ? 1 : s);
 }
