@@ -39,6 +39,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="before the steps, run the library's plain copy kernel once over MIB MiB "
+                        "(reference for hardware traffic counters)")
     return p.parse_args()
 
 
@@ -112,6 +115,15 @@ def main():
             H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block, lin.budget,
                              seed, offsets[i], e["ws"])
             offsets[i] += e["adv"]
+
+    if args.copy_calibration > 0:
+        nb = args.copy_calibration << 20
+        src = torch.ones(nb // 4, device=dev, dtype=torch.int32)
+        dst = torch.empty_like(src)
+        H.debug_copy(src, dst)
+        torch.cuda.synchronize()
+        assert torch.equal(src, dst)
+        del src, dst
 
     for _ in range(args.warmup):
         step()

@@ -180,6 +180,12 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t *plan, const hqlss
  * choice).  Workspace sizes follow the factor in force when they are queried. */
 void hqlss_debug_set_gemm_splits(int splits);
 
+/* Benchmark hook: a plain device-to-device copy kernel ("copy") of `bytes` bytes (a
+ * multiple of 16, both pointers 16-byte aligned, non-overlapping), asynchronous on
+ * `stream`.  Its bytes read and written are known exactly, which calibrates hardware
+ * traffic counters.  Errors: HQLSS_ERR_NULL, HQLSS_ERR_ALIGN, HQLSS_ERR_ARG (size). */
+hqlss_status hqlss_debug_copy(const void *src, void *dst, size_t bytes, void *stream);
+
 /* ---- kernel timing (benchmarks) ------------------------------------------------------
  * When enabled, every kernel the library launches is bracketed by two HIP events
  * recorded on the launch stream.  hqlss_timing_read waits for them, writes up to `cap`

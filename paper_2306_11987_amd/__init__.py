@@ -10,6 +10,7 @@ from ._binding import (  # noqa: F401
     HQLSSError,
     Plan,
     Saved,
+    debug_copy,
     debug_gemm_acc,
     debug_set_gemm_splits,
     hq_linear_fwd,

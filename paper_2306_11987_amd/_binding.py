@@ -53,6 +53,7 @@ def _load() -> ctypes.CDLL:
         "hqlss_timing_read": (_int, [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _int]),
         "hqlss_kernel_name": (ctypes.c_char_p, [_int]),
         "hqlss_debug_set_gemm_splits": (None, [_int]),
+        "hqlss_debug_copy": (st, [_vp, _vp, _sz, _vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -252,6 +253,14 @@ def timing_read(cap: int = 4096):
 
 def debug_set_gemm_splits(splits: int) -> None:
     lib.hqlss_debug_set_gemm_splits(int(splits))
+
+
+def debug_copy(src: torch.Tensor, dst: torch.Tensor) -> None:
+    """Plain device copy kernel of src's bytes into dst (traffic-counter calibration)."""
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < n:
+        raise ValueError("debug_copy: destination smaller than source")
+    _check(lib.hqlss_debug_copy(_ptr(src), _ptr(dst), n, _stream(src)), "hqlss_debug_copy")
 
 
 def kernel_name(i: int) -> str:

@@ -251,7 +251,7 @@ const char* kernel_name(int id) {
   static const char* names[kKCount] = {"zero", "fwht_absmax", "fwht_quant", "transpose_packed",
                                        "bit_split", "lss_plan", "build_ag", "build_dw_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
-                                       "gemm_reduce"};
+                                       "gemm_reduce", "copy"};
   return (id >= 0 && id < kKCount) ? names[id] : "?";
 }
 
@@ -470,5 +470,13 @@ int hqlss_timing_read(int* ids, float* ms, int cap) {
 const char* hqlss_kernel_name(int id) { return hqlss::kernel_name(id); }
 
 void hqlss_debug_set_gemm_splits(int splits) { hqlss::gemm_set_split_override(splits); }
+
+hqlss_status hqlss_debug_copy(const void* src, void* dst, size_t bytes, void* stream) {
+  if (!src || !dst) return HQLSS_ERR_NULL;
+  if (!a16(src) || !a16(dst)) return HQLSS_ERR_ALIGN;
+  if (bytes % 16) return HQLSS_ERR_ARG;
+  if (!bytes) return HQLSS_OK;
+  return hip_status(launch_copy(static_cast<hipStream_t>(stream), src, dst, (int64_t)bytes));
+}
 
 }  // extern "C"

@@ -8,13 +8,16 @@ namespace hqlss {
 // Kernel ids for the timing log (kept in sync with kernel_name()).
 enum KernelId : int {
   kKZero = 0, kKAbsmax, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuildAg, kKBuildDw,
-  kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCount
+  kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKCount
 };
 const char* kernel_name(int id);
 
 // Every launch goes through this hook so that the timing log can bracket it.
 void timing_begin(hipStream_t s);
 void timing_end(hipStream_t s, int id);
+
+// Plain device copy of `bytes` (a multiple of 16; both pointers 16-byte aligned).
+hipError_t launch_copy(hipStream_t s, const void* src, void* dst, int64_t bytes);
 
 // Zero up to four u32 buffers (counts in 32-bit words).
 hipError_t launch_zero(hipStream_t s, uint32_t* p0, int64_t n0, uint32_t* p1 = nullptr,

@@ -71,6 +71,15 @@ __device__ __forceinline__ uint32_t pack8(const int q[8]) {
   return w;
 }
 
+// Plain 16-byte copy: the reference kernel against which hardware traffic counters are
+// calibrated (its bytes read and written are known exactly).
+__global__ __launch_bounds__(kThreads) void copy_kernel(const uint4* __restrict__ src,
+                                                        uint4* __restrict__ dst, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = src[i];
+}
+
 __global__ __launch_bounds__(kThreads) void zero_kernel(uint32_t* p0, int64_t n0, uint32_t* p1,
                                                         int64_t n1, uint32_t* p2, int64_t n2,
                                                         uint32_t* p3, int64_t n3) {
@@ -308,6 +317,17 @@ hipError_t launch_zero(hipStream_t s, uint32_t* p0, int64_t n0, uint32_t* p1, in
   timing_begin(s);
   zero_kernel<<<(int)wg, kThreads, 0, s>>>(p0, n0, p1, n1, p2, n2, p3, n3);
   timing_end(s, kKZero);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy(hipStream_t s, const void* src, void* dst, int64_t bytes) {
+  const int64_t n = bytes / 16;
+  int64_t wg = (n + kThreads - 1) / kThreads;
+  if (wg > 4096) wg = 4096;
+  if (wg < 1) wg = 1;
+  timing_begin(s);
+  copy_kernel<<<(int)wg, kThreads, 0, s>>>(static_cast<const uint4*>(src), static_cast<uint4*>(dst), n);
+  timing_end(s, kKCopy);
   return hipGetLastError();
 }
 
