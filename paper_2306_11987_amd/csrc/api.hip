@@ -76,7 +76,8 @@ hqlss_status check_plan(const lss_plan_t* p) {
 }
 
 // ---------------------------------------------------------------- workspace layout
-constexpr size_t kSlotBytes = size_t(kSlotWords) * 4;  // absmax partial slots of one tensor
+// forward head of the workspace: per-workgroup absmax partials of X and W
+constexpr size_t kFwdHead = size_t(2) * kQMaxWg * sizeof(float);
 size_t fwd_gemm_partial(int64_t N, int64_t D, int64_t C) {
   return al(gemm_partial_bytes(N, C, gemm_splits(N, C, D, true, true)));
 }
@@ -86,8 +87,12 @@ size_t dx_gemm_partial(int64_t N, int64_t D, int64_t C) {
 size_t dw_gemm_partial(int64_t N, int64_t D, int64_t C) {
   return al(gemm_partial_bytes(C, D, gemm_splits(C, D, (N + 127) / 128 * 128, false, true)));
 }
-size_t fwd_bytes(int64_t N, int64_t D, int64_t C) { return 2 * kSlotBytes + fwd_gemm_partial(N, D, C); }
-size_t plan_scratch_bytes() { return kSlotBytes; }
+size_t fwd_bytes(int64_t N, int64_t D, int64_t C) { return kFwdHead + fwd_gemm_partial(N, D, C); }
+// absmax partials of dY, leverage scores [2][round_up(N, 8)], bit-split partials
+int64_t score_pitch(int64_t N) { return rup(N, 8); }
+size_t plan_scratch_bytes(int64_t N) {
+  return al(sizeof(float) * kQMaxWg) + al(8 * score_pitch(N)) + al(sizeof(uint4) * kQMaxWg);
+}
 size_t plan_bytes(int64_t N, int64_t C) {
   return al(N * C / 2) * 2 + al(4 * N) * 2 + al(N) * 2 + al(4 * N) + al(4) * 2;
 }
@@ -138,12 +143,13 @@ constexpr size_t kLogPairs = 4096;
 hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
                     int dt, int k, const hqlss_saved_t* sv, void* ws, hipStream_t s) {
   uint32_t* amax = reinterpret_cast<uint32_t*>(sv->amax);
-  uint32_t* slots = static_cast<uint32_t*>(ws);  // [2][kSlotWords]
-  HQ_TRY(launch_zero(s, slots, 2 * kSlotWords, reinterpret_cast<uint32_t*>(sv->x_sumsq), N));
-  HQ_TRY(launch_fwht_absmax(s, dt, k, X, N, D, slots));
-  HQ_TRY(launch_fwht_absmax(s, dt, k, W, C, D, slots + kSlotWords));
-  HQ_TRY(launch_fwht_quant(s, dt, k, X, N, D, slots, sv->amax, sv->xq, sv->x_sumsq));
-  HQ_TRY(launch_fwht_quant(s, dt, k, W, C, D, slots + kSlotWords, sv->amax + 1, sv->wq, nullptr));
+  float* px = static_cast<float*>(ws);  // [2][kQMaxWg] absmax partials
+  float* pw = px + kQMaxWg;
+  QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
+  HQ_TRY(launch_fwht_absmax(s, dt, k, jx, px, jw, pw));
+  const QOut ox{px, jx.wg, sv->amax, sv->xq, sv->x_sumsq};
+  const QOut ow{pw, jw.wg, sv->amax + 1, sv->wq, nullptr};
+  HQ_TRY(launch_fwht_quant(s, dt, k, jx, ox, jw, ow));
   HQ_TRY(launch_transpose_packed(s, sv->wq, C, D, sv->wqT));
   if (Y) {
     GemmArgs g{};
@@ -155,7 +161,7 @@ hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D,
     g.denom = (float)(int64_t(1) << k);
     g.log2b = k;
     const int sp = gemm_splits(N, C, D, true, true);
-    int32_t* part = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * kSlotBytes);
+    int32_t* part = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kFwdHead);
     HQ_TRY(launch_gemm(s, kEpiFwd, dt, true, true, g, sp, part));
   }
   return HQLSS_OK;
@@ -164,13 +170,17 @@ hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D,
 hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* p, int64_t N,
                      int64_t C, int dt, int64_t budget, uint64_t seed, uint64_t offset,
                      Carve& w, hipStream_t s) {
-  uint32_t* slots = w.take<uint32_t>(kSlotBytes);
-  HQ_TRY(launch_zero(s, slots, kSlotWords, reinterpret_cast<uint32_t*>(p->sumsq_up), N,
-                     reinterpret_cast<uint32_t*>(p->sumsq_dn), N));
-  HQ_TRY(launch_fwht_absmax(s, dt, 0, dY, N, C, slots));
-  HQ_TRY(launch_bit_split(s, dt, dY, N, C, slots, p->amax_g, p->qup, p->qdn, p->sumsq_up,
-                          p->sumsq_dn, seed, offset));
-  HQ_TRY(launch_lss_plan(s, p->sumsq_up, p->sumsq_dn, sv->x_sumsq, N, budget, seed, offset,
+  float* pg = w.take<float>(sizeof(float) * kQMaxWg);
+  const int64_t pitch = score_pitch(N);
+  uint32_t* scores = w.take<uint32_t>(8 * pitch);
+  uint4* bparts = w.take<uint4>(sizeof(uint4) * kQMaxWg);
+  QJob jg = make_job(dY, N, C), none = make_job(nullptr, 0, C);
+  HQ_TRY(launch_fwht_absmax(s, dt, 0, jg, pg, none, nullptr));
+  const int nparts = jg.wg;  // absmax partials of dY
+  const BsOut o{p->amax_g, p->qup, p->qdn, p->sumsq_up, p->sumsq_dn, sv->x_sumsq, scores, pitch,
+                bparts};
+  HQ_TRY(launch_bit_split(s, dt, jg, pg, nparts, o, seed, offset));
+  HQ_TRY(launch_lss_plan(s, p->sumsq_up, scores, pitch, bparts, jg.wg, N, budget, seed, offset,
                          p->w_up, p->w_dn, p->kept, p->n_kept));
   return HQLSS_OK;
 }
@@ -248,7 +258,7 @@ hqlss_status check_bwd_common(const void* dY, const hqlss_saved_t* saved, int64_
 namespace hqlss {
 
 const char* kernel_name(int id) {
-  static const char* names[kKCount] = {"zero", "fwht_absmax", "fwht_quant", "transpose_packed",
+  static const char* names[kKCount] = {"fwht_absmax", "fwht_quant", "transpose_packed",
                                        "bit_split", "lss_plan", "build_ag", "build_dw_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
                                        "gemm_reduce", "copy"};
@@ -275,12 +285,12 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
   if (N < 1 || D < 1 || C < 1) return 0;
   switch (which) {
     case HQLSS_WS_FWD: return fwd_bytes(N, D, C);
-    case HQLSS_WS_BWD_DX: return plan_bytes(N, C) + plan_scratch_bytes() + dx_bytes(N, D, C);
-    case HQLSS_WS_BWD_DW: return plan_bytes(N, C) + plan_scratch_bytes() + dw_bytes(N, D, C);
+    case HQLSS_WS_BWD_DX: return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C);
+    case HQLSS_WS_BWD_DW: return plan_bytes(N, C) + plan_scratch_bytes(N) + dw_bytes(N, D, C);
     case HQLSS_WS_BWD:
-      return plan_bytes(N, C) + plan_scratch_bytes() + dx_bytes(N, D, C) + dw_bytes(N, D, C);
+      return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C) + dw_bytes(N, D, C);
     case HQLSS_WS_FROM_PLAN: return dx_bytes(N, D, C) + dw_bytes(N, D, C);
-    case HQLSS_WS_PLAN: return plan_scratch_bytes();
+    case HQLSS_WS_PLAN: return plan_scratch_bytes(N);
   }
   return 0;
 }
@@ -329,7 +339,7 @@ hqlss_status lss_grad_plan(const void* dY, const hqlss_saved_t* saved, const lss
   hqlss_status st;
   if ((st = check_bwd_common(dY, saved, N, D, C, dt, 0, budget_rows))) return st;
   if ((st = check_plan(plan))) return st;
-  if (!ws || ws_bytes < plan_scratch_bytes()) return HQLSS_ERR_WORKSPACE;
+  if (!ws || ws_bytes < plan_scratch_bytes(N)) return HQLSS_ERR_WORKSPACE;
   if (!a16(ws)) return HQLSS_ERR_ALIGN;
   const int64_t B = budget_rows <= 0 ? N : budget_rows;
   Carve w{static_cast<char*>(ws), 0, ws_bytes};
@@ -364,7 +374,7 @@ static hqlss_status bwd_impl(const void* dY, const hqlss_saved_t* saved, void* d
   hqlss_status st;
   if ((st = check_bwd_common(dY, saved, N, D, C, dt, log2_block, budget_rows))) return st;
   if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
-  const size_t need = plan_bytes(N, C) + plan_scratch_bytes() + (dX ? dx_bytes(N, D, C) : 0) +
+  const size_t need = plan_bytes(N, C) + plan_scratch_bytes(N) + (dX ? dx_bytes(N, D, C) : 0) +
                       (dW ? dw_bytes(N, D, C) : 0);
   if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -420,7 +430,7 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t* plan, const hqlss
     g.out = acc; g.ldo = C;
     const int sp = gemm_splits(N, C, D, true, true);
     if (sp > 1 && (!ws || ws_bytes < fwd_bytes(N, D, C))) return HQLSS_ERR_WORKSPACE;
-    int32_t* part = sp > 1 ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * kSlotBytes)
+    int32_t* part = sp > 1 ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kFwdHead)
                            : nullptr;
     return hip_status(launch_gemm(s, kEpiAcc, HQLSS_F32, true, true, g, sp, part));
   }

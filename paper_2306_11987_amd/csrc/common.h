@@ -8,9 +8,6 @@ namespace hqlss {
 constexpr int kWave = 64;
 constexpr int kQmax = 7;      // Q_N = Q_P = 7 (Sec. 3.1)
 constexpr int kBsRatio = 14;  // s_up / s_dn of the bit split
-constexpr int kSlots = 64;      // per-tensor absmax partial slots
-constexpr int kSlotStride = 32; // 32 words = one 128-byte line per slot
-constexpr int kSlotWords = kSlots * kSlotStride;
 
 enum Dt : int { kF32 = 0, kF16 = 1, kBF16 = 2 };
 
@@ -103,10 +100,10 @@ __device__ __forceinline__ U4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
-    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
-    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
-    const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
-    c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;  // one 32 x 32 -> 64 multiply each
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0, n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c0 = n0; c1 = (uint32_t)p1; c2 = n2; c3 = (uint32_t)p0;
   }
   return U4{c0, c1, c2, c3};
 }
@@ -141,6 +138,14 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
     v += ((uint64_t)hi << 32) | lo;
   }
   return v;
+}
+
+// floor(sqrt(x)) for x < 2^64: a double estimate corrected by at most a few steps.
+__device__ __forceinline__ uint32_t isqrt64(uint64_t x) {
+  uint64_t r = (uint64_t)sqrt((double)x);
+  while (r * r > x) --r;
+  while ((r + 1) * (r + 1) <= x) ++r;
+  return (uint32_t)r;
 }
 
 // ---------------------------------------------------------------- scales

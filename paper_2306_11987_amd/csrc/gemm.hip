@@ -10,30 +10,30 @@
 // All three are "NT" products acc[m][n] = sum_k A[m][k] B[n][k] with K-contiguous rows.
 // CDNA4 has no INT4 matrix instruction, so INT4 codes run on the int8 MFMA
 // (v_mfma_i32_32x32x32_i8, int32 accumulation).  INT4 operands stay packed in HBM and in
-// LDS and are widened after the LDS read with two masks per 32-bit word:
+// LDS and are widened right after the LDS read with two masks per 32-bit word:
 // (w << 4) & 0xF0F0F0F0 places the even nibbles, w & 0xF0F0F0F0 the odd ones, in the high
 // half of each byte, i.e. 16 x the signed code.  Inside every group of 8 k the register
 // order becomes 0,2,4,6,1,3,5,7; int8 operands are stored in that order by their producer,
 // and as the reduction over k is order-free the product is exact.  The factor 16 per INT4
-// operand is a power of two, removed by an arithmetic shift.
+// operand is a power of two, removed by an arithmetic shift (or folded into the scale).
 //
-// Tiling: a BM x 256 tile per 256-thread workgroup, 2 x 2 waves.  INT4 x INT4 (forward) uses
-// BM = 256, one workgroup per CU, wave tiles of 128 x 128 (4 x 4 MFMA 32 x 32 tiles,
-// accumulators in AGPRs), keeping fragment reads and INT4 widening at 0.5 per MFMA.  The
-// int8 x INT4 gradient GEMMs use BM = 128 with two workgroups per CU, so that one
-// workgroup's stage boundaries and epilogue overlap the other's MFMAs.  The MFMA "A" operand carries the n rows and the "B"
-// operand the m rows, so that a lane's accumulators run along n: lane l, MFMA tile (i, j),
-// register r holds m = 32 i + (l % 32) and n = 16 j + r + (BN/4) (l / 32) of the wave tile.
-// This is arranged by storing the B rows in LDS in that permuted slot order.  Each lane then
-// owns 16 consecutive n per (i, j) (32-byte stores), and the gradient epilogue's Hadamard
-// transform along n runs in registers except for the single stride n = BN/4, which pairs
-// lanes l and l ^ 32.
+// Tiling.  Workgroup tile BM x 256 with waves of 64 x 128 (2 x 4 MFMA tiles of 32 x 32,
+// 128 accumulators in AGPRs): BM = 256 runs 8 waves and one workgroup per CU, BM = 128
+// runs 4 waves and two workgroups per CU.  Either way every SIMD holds two waves, so one
+// wave's LDS reads, INT4 widening and epilogue overlap the other's MFMAs.  The MFMA "A"
+// operand carries the n rows and the "B" operand the m rows, so that a lane's accumulators
+// run along n: lane l, MFMA tile (i, j), register r holds m = 32 i + (l % 32) and
+// n = 16 j + r + 64 (l / 32) of the wave tile.  This is arranged by the order in which the
+// B rows are placed in LDS.  Each lane then owns 16 consecutive n per (i, j), and the
+// gradient epilogue's Hadamard transform along n runs in registers for blocks up to 64
+// and pairs lanes l and l ^ 32 for the stride 64.
 //
-// Main loop: K in stages of 256 (both operands INT4) or 128, register prefetch of stage s+1
-// while stage s computes from LDS, two LDS buffers, one barrier per stage.  All fragments of
-// a stage are read from LDS right after the barrier (one latency exposure per stage) and
-// widened just before their MFMAs; every operand row sits at a 144-byte pitch, at which the
-// fragment reads are free of bank conflicts.
+// Main loop.  K advances in stages of 128; operands move from HBM/L2 straight into LDS
+// with 16-byte LDS-DMA loads (no register staging), NBUF stages deep, so each stage's
+// loads are in flight while the previous one or two are multiplied.  Rows sit in LDS
+// without padding, their 16-byte chunks XOR-swizzled by row so that the fragment reads
+// (32 rows x one chunk per instruction) hit distinct banks.  A stage boundary is one
+// wait on this wave's own loads plus one barrier.
 // Epilogue: results are staged through LDS in row chunks so that each store instruction
 // writes contiguous 16-byte pieces of whole output rows.  Split-K (gridDim.z > 1) writes
 // int32 partial tiles the same way, and reduce_epilogue sums them.
@@ -46,115 +46,90 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
 
-constexpr int kThreads = 256;
 constexpr int kBN = 256;  // workgroup tile width (n)
-// tile height: 256 (one workgroup per CU) for INT4 x INT4, 128 (two per CU) for int8 x INT4
-template <bool A4> constexpr int tile_m() { return A4 ? 256 : 128; }
+constexpr int kKS = 128;  // K elements per stage
+#ifndef HQLSS_GEMM_FWD_BM
+#define HQLSS_GEMM_FWD_BM 128
+#endif
+#ifndef HQLSS_GEMM_GRAD_BM
+#define HQLSS_GEMM_GRAD_BM 128
+#endif
+template <bool A4> constexpr int tile_m() { return A4 ? HQLSS_GEMM_FWD_BM : HQLSS_GEMM_GRAD_BM; }
 
-template <int BM, int BN, bool A4, bool B4>
+template <int BM, bool A4>
 struct Cfg {
-  static constexpr int KS = (A4 && B4) ? 256 : 128;  // K elements per stage
-  static constexpr int A_ROW = A4 ? KS / 2 : KS;     // bytes per row per stage (128 or 64)
-  static constexpr int B_ROW = B4 ? KS / 2 : KS;
-  // 144-byte row pitch: the fragment reads (rows lane % 32, 16-byte column lane / 32) are
-  // free of LDS bank conflicts at this pitch (measured); 64-byte rows use it too.
-  // 128-row tiles run two workgroups per CU: their 64-byte INT4 rows take an 80-byte pitch
-  // (a few bank conflicts) so that two double-buffered stages fit in 80 KB.
-  static constexpr int A_PITCH = (BM == 128 && A_ROW == 64) ? 80 : 144;
-  static constexpr int B_PITCH = (BM == 128 && B_ROW == 64) ? 80 : 144;
+  static constexpr int BN = kBN;
+  static constexpr int WGM = BM / 64, WGN = 2, WAVES = WGM * WGN, THREADS = 64 * WAVES;
+  static constexpr int WM = 64, WN = 128, TI = 2, TJ = 4;
+  static constexpr int RA = A4 ? kKS / 2 : kKS;  // bytes of an A row per stage
+  static constexpr int RB = kKS / 2;             // B is always INT4
+  static constexpr int CPA = RA / 16, CPB = RB / 16;
+  static constexpr int A_BYTES = BM * RA, B_BYTES = BN * RB, STAGE = A_BYTES + B_BYTES;
+  static constexpr int A_BPW = A_BYTES / 1024 / WAVES, B_BPW = B_BYTES / 1024 / WAVES;
+  static constexpr int DMA = A_BPW + B_BPW;  // 1 KB LDS-DMA loads per wave per stage
   static constexpr int OCC = BM == 128 ? 2 : 1;  // workgroups per CU
-  static constexpr int A_BUF = BM * A_PITCH, B_BUF = BN * B_PITCH;
-  static constexpr int STAGE = A_BUF + B_BUF;
-  static constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
-  static constexpr int TI = WM / 32, TJ = WN / 32;
-  static constexpr int A_CPR = A_ROW / 16, B_CPR = B_ROW / 16;  // 16-byte chunks per row
-  static constexpr int A_CH = BM * A_CPR / kThreads, B_CH = BN * B_CPR / kThreads;
-  static constexpr int PAIRS = KS / 64;  // MFMA k-substep pairs per stage
-  static constexpr int SHIFT = (A4 ? 4 : 0) + (B4 ? 4 : 0);
+  static constexpr int NBUF = (OCC == 2 && !A4) ? 2 : 3;
+  static constexpr int LDS_MAIN = NBUF * STAGE;
+  static constexpr int SHIFT = (A4 ? 4 : 0) + 4;
+  static_assert(A_BYTES % (1024 * WAVES) == 0 && B_BYTES % (1024 * WAVES) == 0, "DMA split");
 };
 
-// LDS slot of B-tile row n_t (see the file comment): wave half wn, then within the wave
-// n_local = 16 j + r + (WN/2) h  ->  slot 32 j + 8 (r / 4) + 4 h + r % 4.
-template <int WN>
-__device__ __forceinline__ int b_slot(int n_t) {
-  const int wn = n_t / WN, nl = n_t % WN;
-  const int h = nl / (WN / 2), rem = nl % (WN / 2);
-  const int j = rem >> 4, r = rem & 15;
-  return wn * WN + 32 * j + 8 * (r >> 2) + 4 * h + (r & 3);
+// 16-byte chunk of row r that holds data chunk c (XOR swizzle; see the file comment).
+template <int RB>
+__device__ __forceinline__ int swz(int r) {
+  return RB == 64 ? ((r >> 2) & 3) : ((r >> 1) & 7);
 }
 
-// Raw bytes of the two MFMA fragments (k substeps 2q and 2q+1 of a pair) of one 32-row
-// operand tile: INT4 16 packed bytes (32 k), int8 32 bytes.  Row `row`, lane half g.
-template <bool INT4> struct Raw { uint4 w[INT4 ? 1 : 2]; };
-
-template <bool INT4, int PITCH>
-__device__ __forceinline__ Raw<INT4> read_raw(const uint8_t* buf, int row, int pair, int g) {
-  Raw<INT4> r;
-  if constexpr (INT4) {
-    r.w[0] = *reinterpret_cast<const uint4*>(buf + row * PITCH + pair * 32 + g * 16);
-  } else {
-    const uint8_t* p = buf + row * PITCH + pair * 64 + g * 32;
-    r.w[0] = *reinterpret_cast<const uint4*>(p);
-    r.w[1] = *reinterpret_cast<const uint4*>(p + 16);
-  }
-  return r;
+// B-tile LDS slot s -> tile row n_t (slot order puts a lane's 16 accumulators on 16
+// consecutive n): within a wave half of 128 rows, slot 32 j + t holds
+// n = 16 j + 4 (t / 8) + (t % 4) + 64 ((t / 4) % 2).
+__device__ __forceinline__ int b_row_of_slot(int s) {
+  const int wn = s >> 7, rem = s & 127, j = rem >> 5, t = rem & 31;
+  return wn * 128 + 16 * j + 4 * (t >> 3) + (t & 3) + 64 * ((t >> 2) & 1);
 }
 
-// Fragment of k substep `half` (0 or 1) of a raw pair; INT4 is widened to 16 x the code.
-template <bool INT4>
-__device__ __forceinline__ v4i frag_of(const Raw<INT4>& r, int half) {
+// Widen k step `half` of a 16-byte INT4 raw read to an int8 fragment (16 x the code).
+__device__ __forceinline__ v4i widen(const uint4& w, int half) {
+  const uint32_t a = half ? w.z : w.x, b = half ? w.w : w.y;
   v4i f;
-  if constexpr (INT4) {
-    const uint32_t a = half ? r.w[0].z : r.w[0].x, b = half ? r.w[0].w : r.w[0].y;
-    f[0] = (int)((a << 4) & 0xF0F0F0F0u);
-    f[1] = (int)(a & 0xF0F0F0F0u);
-    f[2] = (int)((b << 4) & 0xF0F0F0F0u);
-    f[3] = (int)(b & 0xF0F0F0F0u);
-  } else {
-    const uint4 w = r.w[half];
-    f[0] = (int)w.x; f[1] = (int)w.y; f[2] = (int)w.z; f[3] = (int)w.w;
-  }
+  f[0] = (int)((a << 4) & 0xF0F0F0F0u);
+  f[1] = (int)(a & 0xF0F0F0F0u);
+  f[2] = (int)((b << 4) & 0xF0F0F0F0u);
+  f[3] = (int)(b & 0xF0F0F0F0u);
+  return f;
+}
+__device__ __forceinline__ v4i as_frag(const uint4& w) {
+  v4i f;
+  f[0] = (int)w.x; f[1] = (int)w.y; f[2] = (int)w.z; f[3] = (int)w.w;
   return f;
 }
 
-// In-register Hadamard transform of one lane's n values of one m row:
-// v[j * 16 + r] is n = 16 j + r + (WN/2) h.  Strides 1..8 within r, 16.. within j, and
-// stride WN/2 across the lane halves.
-template <int TJ>
-__device__ __forceinline__ void fwht_lane(int* v, int b, int lane) {
-  constexpr int NV = TJ * 16;
+// In-register Hadamard transform (block 2^LOG2B) of one lane's 64 n values of one m row:
+// v[16 j + r] is n = 16 j + r + 64 h (h = lane / 32).  Strides 1..32 run in registers,
+// the stride 64 pairs lanes l and l ^ 32.
+template <int LOG2B>
+__device__ __forceinline__ void fwht_lane(int* v, int lane) {
+  constexpr int b = 1 << LOG2B;
 #pragma unroll
-  for (int h = 1; h < NV; h <<= 1) {
-    if (h < b) {
+  for (int h = 1; h < 64 && h < b; h <<= 1) {
 #pragma unroll
-      for (int e = 0; e < NV; ++e)
-        if ((e & h) == 0) {
-          const int a = v[e], c = v[e + h];
-          v[e] = a + c;
-          v[e + h] = a - c;
-        }
-    }
+    for (int e = 0; e < 64; ++e)
+      if ((e & h) == 0) {
+        const int a = v[e], c = v[e + h];
+        v[e] = a + c;
+        v[e + h] = a - c;
+      }
   }
-  if (b > NV) {  // stride WN/2: partner lane l ^ 32
+  if constexpr (b > 64) {
     const bool upper = (lane & 32) != 0;
 #pragma unroll
-    for (int e = 0; e < NV; ++e) {
+    for (int e = 0; e < 64; ++e) {
       const int p = __shfl_xor(v[e], 32);
       v[e] = upper ? (p - v[e]) : (v[e] + p);
     }
-  }
-}
-
-template <int DT>
-__device__ __forceinline__ void store16(void* out, int64_t idx, const float* f) {
-  char* p = static_cast<char*>(out) + idx * Elem<DT>::bytes;
-  if constexpr (DT == kF32) {
-    store_vec<DT, 8>(p, f);
-    store_vec<DT, 8>(p + 32, f + 8);
-  } else {
-    store_vec<DT, 8>(p, f);
-    store_vec<DT, 8>(p + 16, f + 8);
   }
 }
 
@@ -173,17 +148,25 @@ __device__ __forceinline__ void tile_of(int& tm, int& tn) {
   tn = Lp % tiles_n;
 }
 
-template <int BM, int BN, bool A4, bool B4, int EPI, int DT>
-__global__ __launch_bounds__(kThreads, (BM == 128 ? 2 : 1)) void gemm_kernel(GemmArgs g) {
-  using C_ = Cfg<BM, BN, A4, B4>;
-  constexpr int TI = C_::TI, TJ = C_::TJ;
-  // epilogue staging: rows of BN output elements of ES bytes, written back row-contiguous
+// s_waitcnt: vector-memory count <= n, LDS count 0 (gfx9 encoding: vmcnt [3:0] and
+// [15:14], expcnt [6:4] left at its maximum, lgkmcnt [11:8]).
+template <int n>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4));
+}
+
+template <int BM, bool A4, int EPI, int DT, int LOG2B>
+__global__ __launch_bounds__((Cfg<BM, A4>::THREADS), (Cfg<BM, A4>::OCC)) void gemm_kernel(GemmArgs g) {
+  using C_ = Cfg<BM, A4>;
+  constexpr int TI = C_::TI, TJ = C_::TJ, BN = C_::BN;
   constexpr bool RAW = (EPI == kEpiAcc || EPI == kEpiPartial);
   constexpr int ES = (RAW || DT == kF32) ? 4 : 2;
   constexpr int E_PITCH = BN * ES + 16;
-  constexpr int E_ROWS = (2 * C_::STAGE) / E_PITCH >= C_::WM ? C_::WM : C_::WM / 2;
-  constexpr int LDS = (2 * C_::STAGE > E_ROWS * E_PITCH) ? 2 * C_::STAGE : E_ROWS * E_PITCH;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[LDS];
+  constexpr int E_ROWS = (BM * E_PITCH <= C_::LDS_MAIN) ? BM
+                         : (BM / 2 * E_PITCH <= C_::LDS_MAIN) ? BM / 2
+                         : (BM / 4 * E_PITCH <= C_::LDS_MAIN) ? BM / 4 : BM / 8;
+  static_assert(E_ROWS >= 32 && E_ROWS * E_PITCH <= C_::LDS_MAIN, "epilogue staging");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[C_::LDS_MAIN];
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid >> 1, wn = wid & 1;
@@ -199,49 +182,66 @@ __global__ __launch_bounds__(kThreads, (BM == 128 ? 2 : 1)) void gemm_kernel(Gem
   int64_t K = g.K;
   if (g.k_dev) K = ((int64_t)*g.k_dev + 127) / 128 * 128;
   // split-K range of this workgroup (whole stages)
-  const int nst_all = (int)((K + C_::KS - 1) / C_::KS);
+  const int nst_all = (int)((K + kKS - 1) / kKS);
   const int per = (nst_all + (int)gridDim.z - 1) / (int)gridDim.z;
   const int st0 = (int)blockIdx.z * per;
   const int nst = max(0, min(nst_all, st0 + per) - st0);
-  const int64_t Ka = A4 ? K / 2 : K, Kb = B4 ? K / 2 : K;  // row extents in bytes
-  const uint8_t* __restrict__ gA = static_cast<const uint8_t*>(g.A);
-  const uint8_t* __restrict__ gB = static_cast<const uint8_t*>(g.B);
+  const int64_t Ka = A4 ? K / 2 : K, Kb = K / 2;  // row extents in bytes
 
-  uint4 ra[C_::A_CH], rb[C_::B_CH];
-  auto gload = [&](int st) {
-    const int64_t kbA = (int64_t)(st0 + st) * C_::A_ROW, kbB = (int64_t)(st0 + st) * C_::B_ROW;
-    // out-of-range pieces load a valid address (row 0, k 0) and are zeroed: no branches
+  // per-lane source pointers of this wave's DMA blocks (stage 0 of this split); rows past
+  // the end re-read the last row (their results are never stored)
+  const uint8_t* pa[C_::A_BPW];
+  const uint8_t* pb[C_::B_BPW];
+  int ca[C_::A_BPW], cb[C_::B_BPW];
 #pragma unroll
-    for (int c = 0; c < C_::A_CH; ++c) {
-      const int idx = tid + c * kThreads, r = idx / C_::A_CPR, cc = idx % C_::A_CPR;
-      const int64_t gm = m0 + r, kb = kbA + cc * 16;
-      const bool in = gm < M && kb < Ka;
-      uint4 v = *reinterpret_cast<const uint4*>(gA + (in ? gm * g.lda + kb : 0));
-      if (!in) v = make_uint4(0u, 0u, 0u, 0u);
-      ra[c] = v;
+  for (int x = 0; x < C_::A_BPW; ++x) {
+    const int r = (wid * C_::A_BPW + x) * (1024 / C_::RA) + lane / C_::CPA;
+    const int c = (lane % C_::CPA) ^ swz<C_::RA>(r);
+    int64_t gm = m0 + r;
+    gm = gm < M ? gm : M - 1;
+    ca[x] = c * 16;
+    pa[x] = static_cast<const uint8_t*>(g.A) + gm * g.lda + (int64_t)st0 * C_::RA + c * 16;
+  }
+#pragma unroll
+  for (int x = 0; x < C_::B_BPW; ++x) {
+    const int s = (wid * C_::B_BPW + x) * (1024 / C_::RB) + lane / C_::CPB;
+    const int c = (lane % C_::CPB) ^ swz<C_::RB>(s);
+    int64_t gn = n0 + b_row_of_slot(s);
+    gn = gn < g.N ? gn : g.N - 1;
+    cb[x] = c * 16;
+    pb[x] = static_cast<const uint8_t*>(g.B) + gn * g.ldb + (int64_t)st0 * C_::RB + c * 16;
+  }
+  // issue the loads of local stage st into buffer st % NBUF; chunks past K are zeroed
+  auto issue = [&](int st) {
+    uint8_t* sa = smem + (st % C_::NBUF) * C_::STAGE;
+    uint8_t* sb = sa + C_::A_BYTES;
+    const int64_t ka = (int64_t)(st0 + st) * C_::RA, kb = (int64_t)(st0 + st) * C_::RB;
+    if (ka + C_::RA <= Ka && kb + C_::RB <= Kb) {  // whole stage inside K: straight line
+#pragma unroll
+      for (int x = 0; x < C_::A_BPW; ++x)
+        __builtin_amdgcn_global_load_lds((glb_void*)(pa[x] + (int64_t)st * C_::RA),
+                                         (lds_void*)(sa + (wid * C_::A_BPW + x) * 1024), 16, 0, 0);
+#pragma unroll
+      for (int x = 0; x < C_::B_BPW; ++x)
+        __builtin_amdgcn_global_load_lds((glb_void*)(pb[x] + (int64_t)st * C_::RB),
+                                         (lds_void*)(sb + (wid * C_::B_BPW + x) * 1024), 16, 0, 0);
+      return;
     }
 #pragma unroll
-    for (int c = 0; c < C_::B_CH; ++c) {
-      const int idx = tid + c * kThreads, r = idx / C_::B_CPR, cc = idx % C_::B_CPR;
-      const int64_t gn = n0 + r, kb = kbB + cc * 16;
-      const bool in = gn < g.N && kb < Kb;
-      uint4 v = *reinterpret_cast<const uint4*>(gB + (in ? gn * g.ldb + kb : 0));
-      if (!in) v = make_uint4(0u, 0u, 0u, 0u);
-      rb[c] = v;
-    }
-  };
-  auto sstore = [&](int buf) {
-    uint8_t* sa = smem + buf * C_::STAGE;
-    uint8_t* sb = sa + C_::A_BUF;
-#pragma unroll
-    for (int c = 0; c < C_::A_CH; ++c) {
-      const int idx = tid + c * kThreads, r = idx / C_::A_CPR, cc = idx % C_::A_CPR;
-      *reinterpret_cast<uint4*>(sa + r * C_::A_PITCH + cc * 16) = ra[c];
+    for (int x = 0; x < C_::A_BPW; ++x) {
+      uint8_t* dst = sa + (wid * C_::A_BPW + x) * 1024;
+      if (ka + ca[x] < Ka)
+        __builtin_amdgcn_global_load_lds((glb_void*)(pa[x] + (int64_t)st * C_::RA), (lds_void*)dst, 16, 0, 0);
+      else
+        *reinterpret_cast<uint4*>(dst + lane * 16) = make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
-    for (int c = 0; c < C_::B_CH; ++c) {
-      const int idx = tid + c * kThreads, r = idx / C_::B_CPR, cc = idx % C_::B_CPR;
-      *reinterpret_cast<uint4*>(sb + b_slot<C_::WN>(r) * C_::B_PITCH + cc * 16) = rb[c];
+    for (int x = 0; x < C_::B_BPW; ++x) {
+      uint8_t* dst = sb + (wid * C_::B_BPW + x) * 1024;
+      if (kb + cb[x] < Kb)
+        __builtin_amdgcn_global_load_lds((glb_void*)(pb[x] + (int64_t)st * C_::RB), (lds_void*)dst, 16, 0, 0);
+      else
+        *reinterpret_cast<uint4*>(dst + lane * 16) = make_uint4(0u, 0u, 0u, 0u);
     }
   };
 
@@ -253,84 +253,133 @@ __global__ __launch_bounds__(kThreads, (BM == 128 ? 2 : 1)) void gemm_kernel(Gem
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
 
+  // fragment rows of this lane and their swizzles
   const int frow = lane & 31, fg = lane >> 5;
-  if (nst > 0) {
-    gload(0);
-    sstore(0);
-    __syncthreads();
+  int offa[TI], sza[TI], offb[TJ], szb[TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const int r = wm * C_::WM + 32 * i + frow;
+    offa[i] = r * C_::RA;
+    sza[i] = swz<C_::RA>(r);
   }
-  for (int st = 0; st < nst; ++st) {
-    const int cur = st & 1;
-    if (st + 1 < nst) gload(st + 1);
-    const uint8_t* sa = smem + cur * C_::STAGE;
-    const uint8_t* sb = sa + C_::A_BUF;
-    // Software pipeline over the stage's 32-k steps t (two steps per raw pair p = t / 2):
-    // the MFMAs of step t run interleaved with the widening of step t+1's fragments and
-    // with the LDS reads of pair p+2, issued two steps before their first use.
-    constexpr int STEPS = 2 * C_::PAIRS;
-    Raw<B4> rbn[2][TJ];
-    Raw<A4> ram[2][TI];
-    v4i fb[2][TJ], fa[2][TI];
 #pragma unroll
-    for (int p = 0; p < 2 && p < C_::PAIRS; ++p) {
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) rbn[p][j] = read_raw<B4, C_::B_PITCH>(sb, wn * C_::WN + 32 * j + frow, p, fg);
-#pragma unroll
-      for (int i = 0; i < TI; ++i) ram[p][i] = read_raw<A4, C_::A_PITCH>(sa, wm * C_::WM + 32 * i + frow, p, fg);
-    }
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) fb[0][j] = frag_of<B4>(rbn[0][j], 0);
-#pragma unroll
-    for (int i = 0; i < TI; ++i) fa[0][i] = frag_of<A4>(ram[0][i], 0);
-#pragma unroll
-    for (int t = 0; t < STEPS; ++t) {
-      const int p = t >> 1, h = t & 1, c = t & 1, n = c ^ 1;
-      if (t + 1 < STEPS) {
-        const int p1 = (t + 1) >> 1, h1 = (t + 1) & 1;
-#pragma unroll
-        for (int j = 0; j < TJ; ++j) fb[n][j] = frag_of<B4>(rbn[p1 & 1][j], h1);
-#pragma unroll
-        for (int i = 0; i < TI; ++i) fa[n][i] = frag_of<A4>(ram[p1 & 1][i], h1);
-      }
-      if (h == 1 && p + 2 < C_::PAIRS) {  // raw[p & 1] is fully widened now
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-          rbn[p & 1][j] = read_raw<B4, C_::B_PITCH>(sb, wn * C_::WN + 32 * j + frow, p + 2, fg);
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-          ram[p & 1][i] = read_raw<A4, C_::A_PITCH>(sa, wm * C_::WM + 32 * i + frow, p + 2, fg);
-      }
-#pragma unroll
-      for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[c][j], fa[c][i], acc[i][j], 0, 0, 0);
-      // interleave: each MFMA followed by a few VALU (widening) and at most one LDS read
-#pragma unroll
-      for (int q = 0; q < TI * TJ; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // up to 3 VALU
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // up to 1 DS read
-      }
-    }
-    if (st + 1 < nst) sstore(cur ^ 1);
-    __syncthreads();
+  for (int j = 0; j < TJ; ++j) {
+    const int r = wn * C_::WN + 32 * j + frow;
+    offb[j] = r * C_::RB;
+    szb[j] = swz<C_::RB>(r);
   }
 
+  // Software pipeline over the four 32-k MFMA steps of a stage.  While the 8 MFMAs of
+  // step t run, the next step's fragments are widened and the LDS reads of the pair after
+  // are issued, interleaved one MFMA at a time (the wave issues in order, so a burst of
+  // MFMAs would otherwise hold back its own VALU and LDS work).  Raw reads cover a pair
+  // of steps (16 bytes of INT4 per lane) and sit in slot 0 (steps 0, 1) or slot 1 (2, 3);
+  // the wait for the next stage's loads and the barrier come after step 1, when every
+  // read of the current stage has been issued, and that barrier frees the current buffer
+  // for the next load.
+  constexpr int RA_PAIR = A4 ? 1 : 2;  // 16-byte A reads per row per pair
+  uint4 rb[2][TJ], ra[2][RA_PAIR][TI];
+  v4i fb[2][TJ], fa[2][TI];
+  auto read_pair = [&](int slot, int st, int pp) {
+    const uint8_t* sa = smem + (st % C_::NBUF) * C_::STAGE;
+    const uint8_t* sb = sa + C_::A_BYTES;
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+      rb[slot][j] = *reinterpret_cast<const uint4*>(sb + offb[j] + (((2 * pp + fg) ^ szb[j]) << 4));
+#pragma unroll
+    for (int h = 0; h < RA_PAIR; ++h)
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int c = A4 ? 2 * pp + fg : 4 * pp + 2 * fg + h;
+        ra[slot][h][i] = *reinterpret_cast<const uint4*>(sa + offa[i] + ((c ^ sza[i]) << 4));
+      }
+  };
+  auto widen_step = [&](int f, int slot, int h) {
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) fb[f][j] = widen(rb[slot][j], h);
+#pragma unroll
+    for (int i = 0; i < TI; ++i) fa[f][i] = A4 ? widen(ra[slot][0][i], h) : as_frag(ra[slot][h][i]);
+  };
+  auto mfma_step = [&](int f) {
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fb[f][j], fa[f][i], acc[i][j], 0, 0, 0);
+  };
+  auto interleave = [&]() {
+#pragma unroll
+    for (int q = 0; q < TI * TJ; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // up to 5 VALU
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // up to 1 LDS read
+    }
+  };
+  auto stage_ready = [&](int st) {  // this wave's loads of stage st landed, then all waves'
+    if (C_::NBUF == 3 && st + 1 < nst) wait_vm_lgkm0<C_::DMA>();
+    else wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+    if (st + C_::NBUF - 1 < nst) issue(st + C_::NBUF - 1);
+  };
+#pragma unroll
+  for (int p = 0; p < C_::NBUF - 1; ++p)
+    if (p < nst) issue(p);
+  if (nst > 0) {
+    stage_ready(0);
+    read_pair(0, 0, 0);
+    widen_step(0, 0, 0);
+  }
+  for (int st = 0; st + 1 < nst; ++st) {  // stages with a successor: branch-free steps
+    // step 0: MFMAs on F0 || widen step 1, read pair 1
+    mfma_step(0);
+    widen_step(1, 0, 1);
+    read_pair(1, st, 1);
+    interleave();
+    // step 1: MFMAs on F1 || widen step 2 (pair 1 landed during step 0)
+    mfma_step(1);
+    widen_step(0, 1, 0);
+    interleave();
+    stage_ready(st + 1);
+    // step 2: MFMAs on F0 || widen step 3, read pair 0 of the next stage
+    mfma_step(0);
+    widen_step(1, 1, 1);
+    read_pair(0, st + 1, 0);
+    interleave();
+    // step 3: MFMAs on F1 || widen step 0 of the next stage
+    mfma_step(1);
+    widen_step(0, 0, 0);
+    interleave();
+  }
+  if (nst > 0) {  // last stage
+    mfma_step(0);
+    widen_step(1, 0, 1);
+    read_pair(1, nst - 1, 1);
+    interleave();
+    mfma_step(1);
+    widen_step(0, 1, 0);
+    interleave();
+    mfma_step(0);
+    widen_step(1, 1, 1);
+    interleave();
+    mfma_step(1);
+  }
+  wait_vm_lgkm0<0>();
+  __builtin_amdgcn_s_barrier();  // every wave is done with the stage buffers
+
   // ---------------------------------------------------------------- epilogue
-  // values of (i, j): row m = wm*WM + 32 i + (lane % 32), columns n = wn*WN + 16 j +
-  // (WN/2)(lane / 32) + r.  They go through LDS so that every store writes whole rows.
+  // values of (i, j): row m = wm*64 + 32 i + (lane % 32), columns n = wn*128 + 16 j +
+  // 64 (lane / 32) + r.  They go through LDS so that every store writes whole rows.
   const int ml = lane & 31;
-  const int nh = (C_::WN / 2) * (lane >> 5);
+  const int nh = 64 * (lane >> 5);
   float alpha = 0.f;
   if constexpr (EPI == kEpiFwd) {
-    // fl(alpha 2^-SHIFT * fl(acc)) == fl(alpha * fl(acc >> SHIFT)): both scalings are exact
+    // fl(alpha 2^-SHIFT * fl(acc)) == fl(alpha * fl(acc >> SHIFT)): acc is a multiple of
+    // 2^SHIFT and both scalings by powers of two are exact
     alpha = alpha_of(*g.amax1, *g.amax2, g.denom) * (1.0f / (float)(1 << C_::SHIFT));
   } else if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
     alpha = alpha_of(*g.amax1, *g.amax2, g.denom);
   }
   if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
-    const int b = 1 << g.log2b;
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
       int v[TJ * 16];
@@ -338,7 +387,7 @@ __global__ __launch_bounds__(kThreads, (BM == 128 ? 2 : 1)) void gemm_kernel(Gem
       for (int j = 0; j < TJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) v[16 * j + r] = acc[i][j][r] >> C_::SHIFT;
-      fwht_lane<TJ>(v, b, lane);  // every lane takes part (shuffles)
+      fwht_lane<LOG2B>(v, lane);
 #pragma unroll
       for (int j = 0; j < TJ; ++j)
 #pragma unroll
@@ -367,7 +416,7 @@ __global__ __launch_bounds__(kThreads, (BM == 128 ? 2 : 1)) void gemm_kernel(Gem
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
               const int a = acc[i][j][4 * q + t];
-              if constexpr (RAW) w[t] = (uint32_t)(EPI == kEpiPartial || EPI == kEpiAcc ? (a >> C_::SHIFT) : a);
+              if constexpr (RAW) w[t] = (uint32_t)(a >> C_::SHIFT);
               else w[t] = __float_as_uint(alpha * (float)a);
             }
             p[q] = make_uint4(w[0], w[1], w[2], w[3]);
@@ -382,7 +431,7 @@ __global__ __launch_bounds__(kThreads, (BM == 128 ? 2 : 1)) void gemm_kernel(Gem
       }
     }
     __syncthreads();
-    for (int idx = tid; idx < E_ROWS * PIECES; idx += kThreads) {
+    for (int idx = tid; idx < E_ROWS * PIECES; idx += C_::THREADS) {
       const int r = idx / PIECES, pc = idx % PIECES;
       const int64_t gm = m0 + r_lo + r;
       const int64_t gn = n0 + (int64_t)pc * (16 / ES);
@@ -466,13 +515,34 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
   }
 }
 
-template <int BM, int BN, bool A4, bool B4, int EPI, int DT>
+template <int BM, bool A4, int EPI, int DT, int LOG2B>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
-  dim3 grid((unsigned)((g.N + BN - 1) / BN), (unsigned)((g.M + BM - 1) / BM), (unsigned)splits);
+  using C_ = Cfg<BM, A4>;
+  dim3 grid((unsigned)((g.N + kBN - 1) / kBN), (unsigned)((g.M + BM - 1) / BM), (unsigned)splits);
   timing_begin(s);
-  gemm_kernel<BM, BN, A4, B4, EPI, DT><<<grid, kThreads, 0, s>>>(g);
+  gemm_kernel<BM, A4, EPI, DT, LOG2B><<<grid, C_::THREADS, 0, s>>>(g);
   timing_end(s, id);
   return hipGetLastError();
+}
+
+// the Hadamard block is a template parameter of the gradient epilogues
+template <int BM, bool A4, int EPI, int DT>
+hipError_t gemm_b(hipStream_t s, const GemmArgs& g, int splits, int id) {
+  if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
+    switch (g.log2b) {
+      case 0: return gemm_t<BM, A4, EPI, DT, 0>(s, g, splits, id);
+      case 1: return gemm_t<BM, A4, EPI, DT, 1>(s, g, splits, id);
+      case 2: return gemm_t<BM, A4, EPI, DT, 2>(s, g, splits, id);
+      case 3: return gemm_t<BM, A4, EPI, DT, 3>(s, g, splits, id);
+      case 4: return gemm_t<BM, A4, EPI, DT, 4>(s, g, splits, id);
+      case 5: return gemm_t<BM, A4, EPI, DT, 5>(s, g, splits, id);
+      case 6: return gemm_t<BM, A4, EPI, DT, 6>(s, g, splits, id);
+      case 7: return gemm_t<BM, A4, EPI, DT, 7>(s, g, splits, id);
+    }
+    return hipErrorInvalidValue;
+  } else {
+    return gemm_t<BM, A4, EPI, DT, 0>(s, g, splits, id);
+  }
 }
 
 template <int DT, int MODE>
@@ -487,29 +557,24 @@ hipError_t reduce_t(hipStream_t s, const int32_t* P, int S, const GemmArgs& g) {
   return hipGetLastError();
 }
 
-template <int EPI, int DT>
-hipError_t reduce_dt(hipStream_t s, const int32_t* P, int S, const GemmArgs& g) {
-  return reduce_t<DT, EPI>(s, P, S, g);
-}
-
-template <bool A4, bool B4, int EPI, int DT>
+template <bool A4, int EPI, int DT>
 hipError_t run(hipStream_t s, const GemmArgs& g, int splits, int32_t* partial, int id) {
-  if (splits <= 1) return gemm_t<tile_m<A4>(), kBN, A4, B4, EPI, DT>(s, g, 1, id);
+  constexpr int BM = tile_m<A4>();
+  if (splits <= 1) return gemm_b<BM, A4, EPI, DT>(s, g, 1, id);
   GemmArgs p = g;
   p.out = partial;
   p.ldo = g.N;
-  hipError_t e = gemm_t<tile_m<A4>(), kBN, A4, B4, kEpiPartial, DT>(s, p, splits, id);
+  hipError_t e = gemm_t<BM, A4, kEpiPartial, DT, 0>(s, p, splits, id);
   if (e != hipSuccess) return e;
-  GemmArgs r = g;
-  return reduce_dt<EPI, DT>(s, partial, splits, r);
+  return reduce_t<DT, EPI>(s, partial, splits, g);
 }
 
-template <bool A4, bool B4, int EPI>
+template <bool A4, int EPI>
 hipError_t run_dt(hipStream_t s, int dt, const GemmArgs& g, int splits, int32_t* partial, int id) {
   switch (dt) {
-    case kF32: return run<A4, B4, EPI, kF32>(s, g, splits, partial, id);
-    case kF16: return run<A4, B4, EPI, kF16>(s, g, splits, partial, id);
-    case kBF16: return run<A4, B4, EPI, kBF16>(s, g, splits, partial, id);
+    case kF32: return run<A4, EPI, kF32>(s, g, splits, partial, id);
+    case kF16: return run<A4, EPI, kF16>(s, g, splits, partial, id);
+    case kBF16: return run<A4, EPI, kBF16>(s, g, splits, partial, id);
   }
   return hipErrorInvalidValue;
 }
@@ -522,9 +587,10 @@ void gemm_set_split_override(int splits) { g_split_override = splits < 0 ? 0 : s
 int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4) {
   (void)b_int4;
   if (g_split_override) return g_split_override;
-  const int64_t bm = a_int4 ? 256 : 128, slots = a_int4 ? 256 : 512;  // workgroups in flight
+  const int64_t bm = a_int4 ? tile_m<true>() : tile_m<false>();
+  const int64_t slots = bm == 128 ? 512 : 256;  // workgroups in flight
   const int64_t tiles = ((M + bm - 1) / bm) * ((N + kBN - 1) / kBN);
-  const int64_t stages = (K + 127) / 128;  // in units of 128 k
+  const int64_t stages = (K + kKS - 1) / kKS;
   if (2 * tiles >= slots || stages < 16) return 1;
   int64_t s = (slots + tiles - 1) / tiles;  // about one workgroup per slot
   const int64_t smax = stages / 8;          // keep >= 8 stages per split
@@ -538,13 +604,14 @@ size_t gemm_partial_bytes(int64_t M, int64_t N, int splits) {
 
 hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4, const GemmArgs& g,
                        int splits, int32_t* partial) {
-  if (a_int4 && b_int4) {
-    if (epi == kEpiFwd) return run_dt<true, true, kEpiFwd>(s, dt, g, splits, partial, kKGemmFwd);
-    if (epi == kEpiAcc) return run<true, true, kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
-  } else if (!a_int4 && b_int4) {
-    if (epi == kEpiDx) return run_dt<false, true, kEpiDx>(s, dt, g, splits, partial, kKGemmDx);
-    if (epi == kEpiDw) return run_dt<false, true, kEpiDw>(s, dt, g, splits, partial, kKGemmDw);
-    if (epi == kEpiAcc) return run<false, true, kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
+  if (!b_int4) return hipErrorInvalidValue;
+  if (a_int4) {
+    if (epi == kEpiFwd) return run_dt<true, kEpiFwd>(s, dt, g, splits, partial, kKGemmFwd);
+    if (epi == kEpiAcc) return run<true, kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
+  } else {
+    if (epi == kEpiDx) return run_dt<false, kEpiDx>(s, dt, g, splits, partial, kKGemmDx);
+    if (epi == kEpiDw) return run_dt<false, kEpiDw>(s, dt, g, splits, partial, kKGemmDw);
+    if (epi == kEpiAcc) return run<false, kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
   }
   return hipErrorInvalidValue;
 }

@@ -7,7 +7,7 @@ namespace hqlss {
 
 // Kernel ids for the timing log (kept in sync with kernel_name()).
 enum KernelId : int {
-  kKZero = 0, kKAbsmax, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuildAg, kKBuildDw,
+  kKAbsmax = 0, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuildAg, kKBuildDw,
   kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKCount
 };
 const char* kernel_name(int id);
@@ -19,33 +19,57 @@ void timing_end(hipStream_t s, int id);
 // Plain device copy of `bytes` (a multiple of 16; both pointers 16-byte aligned).
 hipError_t launch_copy(hipStream_t s, const void* src, void* dst, int64_t bytes);
 
-// Zero up to four u32 buffers (counts in 32-bit words).
-hipError_t launch_zero(hipStream_t s, uint32_t* p0, int64_t n0, uint32_t* p1 = nullptr,
-                       int64_t n1 = 0, uint32_t* p2 = nullptr, int64_t n2 = 0,
-                       uint32_t* p3 = nullptr, int64_t n3 = 0);
+// One tensor for the row-group quantisers: rows x cols (cols a multiple of 64), processed
+// by `wg` workgroups of 512 threads with 2^log2g lanes per row.  Launchers choose `wg`
+// (a grid that is resident at once) and store it back into the job.
+constexpr int kQMaxWg = 1024;  // workgroups (= partial results) of one job at most
+struct QJob {
+  const void* src;
+  int64_t rows, cols;
+  int log2g;
+  int wg;
+};
+QJob make_job(const void* src, int64_t rows, int64_t cols);  // rows = 0: an empty job; wg unset
 
-// max |rows x cols block-FWHT(src)| -> atomicMax into kSlots zeroed slots (kSlotWords
-// words, fp32 bit patterns); consumers reduce the slots.
-hipError_t launch_fwht_absmax(hipStream_t s, int dt, int log2b, const void* src, int64_t rows,
-                              int64_t cols, uint32_t* slots);
-// codes of block-FWHT(src) -> packed [rows][cols/2]; optional per-row sum of squares;
-// the reduced maximum is also stored to *amax_out.
-hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const void* src, int64_t rows,
-                             int64_t cols, const uint32_t* slots, float* amax_out,
-                             uint8_t* packed, int32_t* row_sumsq);
+// Per-workgroup maxima of |block-FWHT(src)| of up to two tensors in one launch:
+// part0[0, j0.wg) and part1[0, j1.wg), plain stores (no initialisation needed).
+hipError_t launch_fwht_absmax(hipStream_t s, int dt, int log2b, QJob& j0, float* part0,
+                              QJob& j1, float* part1);
+// Codes of block-FWHT(src) at the maximum of the partials, packed [rows][cols/2]; optional
+// per-row sums of squares; the maximum itself is stored to *amax_out.
+struct QOut {
+  const float* part;
+  int nparts;
+  float* amax_out;
+  uint8_t* packed;
+  int32_t* row_sumsq;  // may be null
+};
+hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const QJob& j0, const QOut& o0,
+                             const QJob& j1, const QOut& o1);
 // packed [rows][cols/2] -> packed [cols][rows/2] (rows, cols multiples of 64).
 hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t rows, int64_t cols,
                                    uint8_t* dst);
-// bit split of dY [N][C] into two packed code planes and their row sums of squares.
-hipError_t launch_bit_split(hipStream_t s, int dt, const void* g, int64_t N, int64_t C,
-                            const uint32_t* slots, float* amax_out, uint8_t* qup, uint8_t* qdn,
-                            int32_t* sumsq_up, int32_t* sumsq_dn, uint64_t seed,
-                            uint64_t offset);
+// Bit split of dY [N][C] into two packed code planes, their row sums of squares, the
+// integer leverage scores scores[t] (upper row) and scores[score_pitch + t] (lower row),
+// and per-workgroup {count of non-zero scores, sum lo, sum hi, 0} in parts[0, j.wg).
+struct BsOut {
+  float* amax_out;
+  uint8_t* qup;
+  uint8_t* qdn;
+  int32_t* sumsq_up;
+  int32_t* sumsq_dn;
+  const int32_t* x_sumsq;
+  uint32_t* scores;
+  int64_t score_pitch;
+  uint4* parts;
+};
+hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, int nparts,
+                            const BsOut& o, uint64_t seed, uint64_t offset);
 // leverage scores, clamp-rescale, masks, compaction (one workgroup).
-hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const int32_t* sumsq_dn,
-                           const int32_t* x_sumsq, int64_t N, int64_t budget, uint64_t seed,
-                           uint64_t offset, uint8_t* w_up, uint8_t* w_dn, int32_t* kept,
-                           int32_t* n_kept);
+hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_t* scores,
+                           int64_t score_pitch, const uint4* parts, int nparts, int64_t N,
+                           int64_t budget, uint64_t seed, uint64_t offset, uint8_t* w_up,
+                           uint8_t* w_dn, int32_t* kept, int32_t* n_kept);
 // Gathered weighted rows A[i] (int8, K-interleaved) for i < round_up(n_kept, 128).
 // Also zeroes the rows of dX (if given, dtype dt) that belong to dropped tokens.
 hipError_t launch_build_ag(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,

@@ -1,19 +1,22 @@
 // Leverage-score sampling of the bit-split gradient rows and the GEMM operands it
 // selects (gfx950).
 //
-// lss_plan (one workgroup of 1024 threads, each owning a contiguous run of tokens):
-//   1. integer leverage scores of the 2N stacked rows (Sec. 4.2): with the common factor
-//      s_dn s_x dropped, c^2 = w^2 * sum q^2 * x_sumsq (w = 14 for the upper row of a token,
-//      1 for the lower one) and c = isqrt(c^2 * 2^16), exact;
-//   2. inclusion probabilities by the clamp-and-rescale loop of App. A.2 with sum p = B, in
-//      exact integers: clamp every row with (B - k) c >= S, then rescale the rest; repeat
-//      until nothing new is clamped.  If no more than B rows have c > 0, every such row has
-//      p = 1 (the "keep rows with norm > 0" rule the paper's implementation uses, App. A.6);
-//   3. upper rows are kept iff non-zero; a lower row with p* < 1 gets p~ = 2^-e >= p*, the
+// lss_plan (one workgroup of 1024 threads).  Its inputs are the integer leverage scores
+// of the 2N stacked rows, formed by the bit-split kernel (Sec. 4.2: with the common factor
+// s_dn s_x dropped, c^2 = w^2 sum q^2 x_sumsq, w = 14 for the upper row of a token and 1
+// for the lower one, c = isqrt(c^2 2^16)), and that kernel's per-workgroup totals:
+//   1. inclusion probabilities by the clamp-and-rescale loop of App. A.2 with sum p = B,
+//      in exact integers.  Thresholds S/R only fall from one round to the next, so the
+//      rows clamped after a round are exactly {c > 0 : R c >= S} for that round's (R, S):
+//      each round is one pass over the scores and needs no per-row state.  If no more
+//      than B rows have c > 0, every such row has p = 1 (the "keep rows with norm > 0"
+//      rule of the paper's implementation, App. A.6);
+//   2. upper rows are kept iff non-zero; a lower row with p* < 1 gets p~ = 2^-e >= p*, the
 //      smallest power of two (e <= 4, e <= 2 if the token's upper row is non-zero), and is
 //      kept iff u16 < 2^(16-e) (Philox stream 1), weight m/p~ = 2^e;
-//   4. kept tokens (w_up + w_dn > 0) are compacted in ascending order by a block-wide
-//      prefix scan (wave scans with shuffles, then one LDS pass over wave totals).
+//   3. kept tokens (w_up + w_dn > 0) are compacted in ascending order: each thread owns 8
+//      consecutive tokens per round of 8192 (vector loads and stores, one Philox block),
+//      and a block-wide scan of the per-thread counts places them.
 //
 // build_ag / build_dw_operands materialise, for the kept tokens only, the weighted integer
 // rows A_t = 14 w_up q_up[t] + w_dn q_dn[t] (|A| <= 126, one int8 operand that carries the
@@ -31,13 +34,6 @@ namespace {
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / kWave;
 
-__device__ __forceinline__ uint32_t isqrt64(uint64_t x) {
-  uint64_t r = (uint64_t)sqrt((double)x);
-  while (r * r > x) --r;
-  while ((r + 1) * (r + 1) <= x) ++r;
-  return (uint32_t)r;
-}
-
 __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
   v = wave_sum_u64(v);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
@@ -49,112 +45,125 @@ __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
   return t;
 }
 
-template <int TPT>
 __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
-    const int32_t* __restrict__ sumsq_up, const int32_t* __restrict__ sumsq_dn,
-    const int32_t* __restrict__ x_sumsq, int N, int64_t B, uint64_t seed, uint64_t offset,
-    uint8_t* __restrict__ w_up, uint8_t* __restrict__ w_dn, int32_t* __restrict__ kept,
-    int32_t* __restrict__ n_kept) {
+    const int32_t* __restrict__ sumsq_up, const uint32_t* __restrict__ scores, int64_t pitch,
+    const uint4* __restrict__ parts, int nparts, int N, int64_t B, uint64_t seed,
+    uint64_t offset, uint8_t* __restrict__ w_up, uint8_t* __restrict__ w_dn,
+    int32_t* __restrict__ kept, int32_t* __restrict__ n_kept) {
   __shared__ uint64_t red[kPlanWaves];
   __shared__ int wtot[kPlanWaves];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int t0 = tid * TPT;
 
-  uint32_t cu[TPT], cd[TPT];
-  uint64_t upmask = 0;  // bit j: the token's upper row is non-zero
-  int nnz = 0;
-#pragma unroll
-  for (int j = 0; j < TPT; ++j) {
-    const int t = t0 + j;
-    cu[j] = cd[j] = 0;
-    if (t < N) {
-      const uint64_t su = (uint32_t)sumsq_up[t], sd = (uint32_t)sumsq_dn[t];
-      const uint64_t sx = (uint32_t)x_sumsq[t];
-      cu[j] = isqrt64(((uint64_t)(kBsRatio * kBsRatio) * su * sx) << 16);
-      cd[j] = isqrt64((sd * sx) << 16);
-      if (su) upmask |= 1ull << j;
-    }
-    nnz += (cu[j] > 0) + (cd[j] > 0);
+  // totals of the bit-split workgroups: non-zero rows and the score sum
+  uint64_t nz = 0, st = 0;
+  for (int i = tid; i < nparts; i += kPlanThreads) {
+    const uint4 p = parts[i];
+    nz += p.x;
+    st += ((uint64_t)p.z << 32) | p.y;
   }
-  const bool all_nonzero_kept = (int64_t)block_sum_u64((uint64_t)nnz, red) <= B;
+  nz = block_sum_u64(nz, red);
+  const uint64_t S_all = block_sum_u64(st, red);
+  const bool all_nonzero_kept = (int64_t)nz <= B;
 
-  uint64_t clamp_u = 0, clamp_d = 0;
-  int64_t R = 0;
-  uint64_t S = 0;
+  // App. A.2 clamp-and-rescale (uniform across the block)
+  uint64_t S = S_all;
+  int64_t R = B;
   if (!all_nonzero_kept) {
-    uint64_t loc = 0;
-#pragma unroll
-    for (int j = 0; j < TPT; ++j) loc += (uint64_t)cu[j] + cd[j];
-    S = block_sum_u64(loc, red);
     int64_t k = 0;
-    for (;;) {  // App. A.2: clamp p >= 1, rescale the rest, repeat (uniform across the block)
+    for (;;) {
       R = B - k;
       uint64_t cnt = 0, sum = 0;
-#pragma unroll
-      for (int j = 0; j < TPT; ++j) {
-        if (cu[j] && !((clamp_u >> j) & 1) && (uint64_t)R * cu[j] >= S) {
-          clamp_u |= 1ull << j; ++cnt; sum += cu[j];
-        }
-        if (cd[j] && !((clamp_d >> j) & 1) && (uint64_t)R * cd[j] >= S) {
-          clamp_d |= 1ull << j; ++cnt; sum += cd[j];
-        }
+      for (int64_t i = tid; i < 2 * (int64_t)N; i += kPlanThreads) {
+        const uint32_t c = scores[i < N ? i : pitch + (i - N)];
+        if (c && (uint64_t)R * c >= S) { ++cnt; sum += c; }
       }
-      const uint64_t ncl = block_sum_u64(cnt, red);
-      if (ncl == 0) break;
-      k += (int64_t)ncl;
-      S -= block_sum_u64(sum, red);
+      cnt = block_sum_u64(cnt, red);
+      sum = block_sum_u64(sum, red);
+      if ((int64_t)cnt == k) break;  // nothing newly clamped
+      k = (int64_t)cnt;
+      S = S_all - sum;
     }
-    R = B - k;
   }
 
-  // weights and keep flags
-  uint64_t keepmask = 0;
-  int nkeep = 0;
-  U4 rnd{0, 0, 0, 0};
+  // weights, masks and compaction, 8 consecutive tokens per thread per round
+  int base = 0;
+  const uint32_t* cdn = scores + pitch;
+  for (int r0 = 0; r0 < N; r0 += 8 * kPlanThreads) {
+    const int t0 = r0 + 8 * tid;
+    const int n8 = t0 < N ? (N - t0 < 8 ? N - t0 : 8) : 0;
+    uint32_t su[8], cd[8];
+    if (n8 == 8) {
+      const uint4 a0 = *reinterpret_cast<const uint4*>(sumsq_up + t0);
+      const uint4 a1 = *reinterpret_cast<const uint4*>(sumsq_up + t0 + 4);
+      const uint4 b0 = *reinterpret_cast<const uint4*>(cdn + t0);
+      const uint4 b1 = *reinterpret_cast<const uint4*>(cdn + t0 + 4);
+      su[0] = a0.x; su[1] = a0.y; su[2] = a0.z; su[3] = a0.w;
+      su[4] = a1.x; su[5] = a1.y; su[6] = a1.z; su[7] = a1.w;
+      cd[0] = b0.x; cd[1] = b0.y; cd[2] = b0.z; cd[3] = b0.w;
+      cd[4] = b1.x; cd[5] = b1.y; cd[6] = b1.z; cd[7] = b1.w;
+    } else {
 #pragma unroll
-  for (int j = 0; j < TPT; ++j) {
-    const int t = t0 + j;
-    if (t >= N) continue;
-    if (j == 0 || (t & 7) == 0) rnd = philox_block(seed, offset, 1u, (uint64_t)(t & ~7));
-    const uint32_t wu = (upmask >> j) & 1;
-    uint32_t wd = 0;
-    if (cd[j]) {
-      if (all_nonzero_kept || ((clamp_d >> j) & 1)) {
-        wd = 1;
-      } else {
-        const int cap = wu ? 2 : 4;
+      for (int j = 0; j < 8; ++j) {
+        su[j] = j < n8 ? (uint32_t)sumsq_up[t0 + j] : 0u;
+        cd[j] = j < n8 ? cdn[t0 + j] : 0u;
+      }
+    }
+    const U4 rnd = philox_block(seed, offset, 1u, (uint64_t)(t0 > 0 ? t0 : 0));
+    uint32_t wu8[2] = {0u, 0u}, wd8[2] = {0u, 0u};
+    uint32_t keepmask = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t wu = su[j] ? 1u : 0u;
+      uint32_t wd = 0;
+      if (cd[j]) {
         const uint64_t rc = (uint64_t)R * cd[j];
-        int e = 0;
-        while (e < cap && (rc << (e + 1)) <= S) ++e;
-        const uint32_t u = u16_of(rnd, t & 7);
-        wd = (u < (1u << (16 - e))) ? (1u << e) : 0u;
+        if (all_nonzero_kept || rc >= S) {
+          wd = 1;
+        } else {
+          const int cap = wu ? 2 : 4;
+          int e = 0;
+          while (e < cap && (rc << (e + 1)) <= S) ++e;
+          wd = (u16_of(rnd, j) < (1u << (16 - e))) ? (1u << e) : 0u;
+        }
+      }
+      if (j >= n8) wd = 0;
+      wu8[j >> 2] |= wu << (8 * (j & 3));
+      wd8[j >> 2] |= wd << (8 * (j & 3));
+      if (wu + wd) keepmask |= 1u << j;
+    }
+    if (n8 == 8) {
+      *reinterpret_cast<uint2*>(w_up + t0) = make_uint2(wu8[0], wu8[1]);
+      *reinterpret_cast<uint2*>(w_dn + t0) = make_uint2(wd8[0], wd8[1]);
+    } else {
+      for (int j = 0; j < n8; ++j) {
+        w_up[t0 + j] = (uint8_t)(wu8[j >> 2] >> (8 * (j & 3)));
+        w_dn[t0 + j] = (uint8_t)(wd8[j >> 2] >> (8 * (j & 3)));
       }
     }
-    w_up[t] = (uint8_t)wu;
-    w_dn[t] = (uint8_t)wd;
-    if (wu + wd) { keepmask |= 1ull << j; ++nkeep; }
-  }
-
-  // block-wide exclusive scan of the per-thread keep counts
-  int x = nkeep;
+    // block-wide exclusive scan of the per-thread keep counts
+    const int nkeep = __builtin_popcount(keepmask);
+    int x = nkeep;
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wtot[wid] = x;
-  __syncthreads();
-  int base = 0, total = 0;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wtot[wid] = x;
+    __syncthreads();
+    int pre = 0, total = 0;
 #pragma unroll
-  for (int i = 0; i < kPlanWaves; ++i) {
-    base += (i < wid) ? wtot[i] : 0;
-    total += wtot[i];
-  }
-  int pos = base + x - nkeep;
+    for (int i = 0; i < kPlanWaves; ++i) {
+      pre += (i < wid) ? wtot[i] : 0;
+      total += wtot[i];
+    }
+    __syncthreads();
+    int pos = base + pre + x - nkeep;
 #pragma unroll
-  for (int j = 0; j < TPT; ++j)
-    if ((keepmask >> j) & 1) kept[pos++] = t0 + j;
-  if (tid == 0) *n_kept = total;
+    for (int j = 0; j < 8; ++j)
+      if ((keepmask >> j) & 1) kept[pos++] = t0 + j;
+    base += total;
+  }
+  if (tid == 0) *n_kept = base;
 }
 
 __device__ __forceinline__ int sext4(uint32_t n) { return (int)(n ^ 8u) - 8; }
@@ -278,35 +287,17 @@ __global__ __launch_bounds__(256) void build_dw_operands_kernel(
   }
 }
 
-template <int TPT>
-hipError_t plan_t(hipStream_t s, const int32_t* su, const int32_t* sd, const int32_t* sx, int64_t N,
-                  int64_t B, uint64_t seed, uint64_t offset, uint8_t* wu, uint8_t* wd,
-                  int32_t* kept, int32_t* nk) {
-  timing_begin(s);
-  lss_plan_kernel<TPT><<<1, kPlanThreads, 0, s>>>(su, sd, sx, (int)N, B, seed, offset, wu, wd,
-                                                   kept, nk);
-  timing_end(s, kKPlan);
-  return hipGetLastError();
-}
-
 }  // namespace
 
-hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const int32_t* sumsq_dn,
-                           const int32_t* x_sumsq, int64_t N, int64_t budget, uint64_t seed,
-                           uint64_t offset, uint8_t* w_up, uint8_t* w_dn, int32_t* kept,
-                           int32_t* n_kept) {
-  const int64_t tpt = (N + kPlanThreads - 1) / kPlanThreads;
-#define HQLSS_PLAN(T) \
-  if (tpt <= T) return plan_t<T>(s, sumsq_up, sumsq_dn, x_sumsq, N, budget, seed, offset, w_up, w_dn, kept, n_kept)
-  HQLSS_PLAN(1);
-  HQLSS_PLAN(2);
-  HQLSS_PLAN(4);
-  HQLSS_PLAN(8);
-  HQLSS_PLAN(16);
-  HQLSS_PLAN(32);
-  HQLSS_PLAN(64);
-#undef HQLSS_PLAN
-  return hipErrorInvalidValue;
+hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_t* scores,
+                           int64_t score_pitch, const uint4* parts, int nparts, int64_t N,
+                           int64_t budget, uint64_t seed, uint64_t offset, uint8_t* w_up,
+                           uint8_t* w_dn, int32_t* kept, int32_t* n_kept) {
+  timing_begin(s);
+  lss_plan_kernel<<<1, kPlanThreads, 0, s>>>(sumsq_up, scores, score_pitch, parts, nparts, (int)N,
+                                             budget, seed, offset, w_up, w_dn, kept, n_kept);
+  timing_end(s, kKPlan);
+  return hipGetLastError();
 }
 
 hipError_t launch_build_ag(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,

@@ -4,41 +4,70 @@
 //    unnormalised Hadamard transform of each row (radix-2 butterflies, strides ascending,
 //    fp32), then per-tensor absmax and INT4 codes clamp(rint(v * fl(7/a)), -7, 7)
 //    (Sec. 3.1, Eq. 2), packed two per byte (App. A.6) with per-row sums of squares
-//    (the ||X_i|| factor of the leverage score, Sec. 4.2).
+//    (the ||X_i|| factor of the leverage score, Sec. 4.2).  One launch serves X and W.
 //  * bit_split: bit splitting of the output gradient (Sec. 4.2, Eq. 4): upper codes by
 //    round-to-nearest at s_up = a/7, lower codes by stochastic rounding of 14 x the exact
-//    residual (s_dn = s_up / 14), Philox stream 0.
+//    residual (s_dn = s_up / 14), Philox stream 0.  It also forms the integer leverage
+//    scores of both stacked rows of every token and per-workgroup totals of them, which
+//    is all the sampler needs.
 //
-// Work decomposition: a wave owns one (row, 512-column chunk) item at a time; each lane
-// holds 8 consecutive elements (one 16- or 32-byte load).  A Hadamard block of
-// b = 2^k <= 128 columns then lives in b/8 consecutive lanes, so strides 1..4 run in
-// registers and strides 8..64 across lanes.  Per-row results reduce inside the wave and
-// land with one integer atomic per (row, chunk); per-tensor maxima with one atomic per
-// workgroup into one of 64 slots.  All loads are 16-byte vectors, coalesced along the row.
+// Work decomposition: a row belongs to a group of G lanes (G = the largest power of two
+// <= 64 dividing cols/16), so a wave holds 64/G rows and every per-row result (sum of
+// squares, scores) is one plain store: no atomics, nothing to pre-zero.  Each lane loads
+// 16 consecutive elements per step and keeps several steps in flight.  A Hadamard block
+// of b = 2^k <= 128 columns lives in b/16 consecutive lanes of one group (b/16 <= G for
+// every admitted shape), so strides 1..8 run in registers and strides 16..64 are lane
+// exchanges folded into the butterfly add (DPP) or a swizzle.  Per-tensor maxima leave
+// each workgroup as one plain store of a partial; consumers reduce the partials.
+//
+// These kernels are bound by vector-ALU issue as much as by HBM, so the per-element work
+// is kept to a handful of instructions: codes come from the magic-number form of
+// round-half-even (x + 1.5 * 2^23 leaves rint(x) in the low mantissa bits, exact for
+// |x| < 2^22), packing uses byte permutes, and the sums of squares of the codes are dot
+// products of the packed INT4 words with themselves.
 #include "common.h"
 #include "launch.h"
+
+#include <mutex>
+#include <unordered_map>
 
 namespace hqlss {
 
 namespace {
 
-constexpr int kChunk = 512;  // columns per wave item (64 lanes x 8)
-constexpr int kThreads = 256;
+constexpr int kQThreads = 512;
+constexpr int kQWaves = kQThreads / kWave;
+constexpr int kVE = 16;  // elements per lane per step
+constexpr float kRne = 12582912.0f;  // 1.5 * 2^23
 
-// Per-tensor maxima land in kSlots words, one 128-byte line apart, so that the
-// workgroups' atomics spread over many L2 channels; a consumer wave reduces them
-// (one slot per lane).
-__device__ __forceinline__ float read_slots(const uint32_t* __restrict__ slots) {
-  return wave_max(__uint_as_float(slots[(threadIdx.x & 63) * kSlotStride]));
+template <int DT>
+__device__ __forceinline__ void load16(const char* p, float v[16]) {
+  load8<DT>(p, v);
+  load8<DT>(p + 8 * Elem<DT>::bytes, v + 8);
 }
 
+// Value of lane (lane ^ M), M in {1, 2, 4}, added to x: DPP quad permutations (folded into
+// the add) or a ds_swizzle swap of 4-lane groups.
+template <int M>
+__device__ __forceinline__ float add_xor_lane(float v, float x) {
+  const int i = __float_as_int(v);
+  if constexpr (M == 1) return __int_as_float(__builtin_amdgcn_update_dpp(0, i, 0xB1, 0xF, 0xF, true)) + x;
+  else if constexpr (M == 2) return __int_as_float(__builtin_amdgcn_update_dpp(0, i, 0x4E, 0xF, 0xF, true)) + x;
+  else return __int_as_float(__builtin_amdgcn_ds_swizzle(i, (4 << 10) | 0x1F)) + x;
+}
+
+// In-place unnormalised FWHT of blocks of 2^LOG2B consecutive elements; the lane holds 16
+// consecutive elements, the lanes of one block are consecutive.  Pairs (a, c) at stride h
+// become (a + c, a - c), strides ascending.  Across lanes the lower lane adds its
+// partner's value and the upper lane adds its own negated value to the partner's (a - c
+// = a + (-c) exactly), so both take one DPP add.
 template <int LOG2B>
-__device__ __forceinline__ void fwht8(float v[8], int lane) {
+__device__ __forceinline__ void fwht16(float v[16], int lane) {
   constexpr int b = 1 << LOG2B;
 #pragma unroll
-  for (int h = 1; h < 8 && h < b; h <<= 1) {
+  for (int h = 1; h < 16 && h < b; h <<= 1) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < 16; ++j) {
       if ((j & h) == 0) {
         const float a = v[j], c = v[j + h];
         v[j] = a + c;
@@ -46,128 +75,200 @@ __device__ __forceinline__ void fwht8(float v[8], int lane) {
       }
     }
   }
-#pragma unroll
-  for (int h = 8; h < b; h <<= 1) {
-    const int m = h >> 3;
-    const bool upper = (lane & m) != 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float p = __shfl_xor(v[j], m);
-      v[j] = upper ? (p - v[j]) : (v[j] + p);  // (a+c, a-c) with a the lower lane
-    }
+#define HQLSS_XSTAGE(M)                                                       \
+  if constexpr (16 * (M) < b) {                                               \
+    const uint32_t sgn = (lane & (M)) ? 0x80000000u : 0u;                     \
+    _Pragma("unroll") for (int j = 0; j < 16; ++j) {                          \
+      const float own = __uint_as_float(__float_as_uint(v[j]) ^ sgn);         \
+      v[j] = add_xor_lane<M>(v[j], own);                                      \
+    }                                                                         \
   }
+  HQLSS_XSTAGE(1)
+  HQLSS_XSTAGE(2)
+  HQLSS_XSTAGE(4)
+#undef HQLSS_XSTAGE
 }
 
-__device__ __forceinline__ int code_of(float v, float inv) {
-  float q = rintf(v * inv);
-  q = fminf(fmaxf(q, -7.0f), 7.0f);
-  return (int)q;
-}
+// Bits of fl(x + 1.5 * 2^23): rint(x) (half-to-even) sits in the low mantissa bits.
+__device__ __forceinline__ uint32_t rne_bits(float x) { return __float_as_uint(x + kRne); }
 
-__device__ __forceinline__ uint32_t pack8(const int q[8]) {
-  uint32_t w = 0;
+// Pack 8 codes given as rne_bits (low nibbles) into one word, element j at bits 4j.
+__device__ __forceinline__ uint32_t pack8_bits(const uint32_t y[8]) {
+  uint32_t b[4];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) w |= (uint32_t)(q[j] & 15) << (4 * j);
-  return w;
+  for (int i = 0; i < 4; ++i) b[i] = (y[2 * i + 1] << 4) | (y[2 * i] & 15u);  // valid low byte
+  const uint32_t lo = __builtin_amdgcn_perm(b[1], b[0], 0x0C0C0400u);  // [b0, b1, 0, 0]
+  const uint32_t hi = __builtin_amdgcn_perm(b[3], b[2], 0x0C0C0400u);  // [b2, b3, 0, 0]
+  return __builtin_amdgcn_perm(hi, lo, 0x05040100u);                  // [b0, b1, b2, b3]
+}
+
+// Sum of squares of the eight signed nibbles of a packed word, accumulated into acc.
+__device__ __forceinline__ int sumsq8(uint32_t w, int acc) {
+  return __builtin_amdgcn_sdot8((int)w, (int)w, acc, false);
+}
+
+// Sum over the G lanes of a row group (G a power of two; every lane of the group active).
+__device__ __forceinline__ int group_sum(int v, int G) {
+  for (int o = G >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Row-group geometry of one job (one tensor).  The wave walks a uniform sequence of steps
+// (row k of its groups, 16-column chunk it), kept several steps ahead in loads whatever
+// the row boundaries; group rows past the end re-read the last row and store nothing.
+struct Geo {
+  int lane, sub, grp, G, rpw, iters;
+  int64_t first_row, row_step, rows, steps;
+  __device__ Geo(const QJob& j, int wg) {
+    lane = threadIdx.x & 63;
+    G = 1 << j.log2g;
+    sub = lane & (G - 1);
+    grp = lane >> j.log2g;
+    rpw = 64 >> j.log2g;
+    iters = (int)((j.cols / kVE) >> j.log2g);
+    const int64_t wave_row0 = ((int64_t)wg * kQWaves + (threadIdx.x >> 6)) * rpw;
+    first_row = wave_row0 + grp;
+    row_step = (int64_t)j.wg * kQWaves * rpw;
+    rows = j.rows;
+    steps = wave_row0 < rows ? (rows - wave_row0 + row_step - 1) / row_step * iters : 0;
+  }
+  // row of step (k, it) for this lane's group, clamped into the tensor
+  __device__ int64_t row_of(int64_t k) const {
+    const int64_t r = first_row + k * row_step;
+    return r < rows ? r : rows - 1;
+  }
+  __device__ bool valid(int64_t k) const { return first_row + k * row_step < rows; }
+};
+
+// max over the first n partial maxima (every thread of the workgroup gets it).
+__device__ __forceinline__ float reduce_parts(const float* __restrict__ part, int n) {
+  __shared__ float red[kQWaves];
+  float m = 0.f;
+  for (int i = threadIdx.x; i < n; i += kQThreads) m = fmaxf(m, part[i]);
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  m = red[0];
+#pragma unroll
+  for (int i = 1; i < kQWaves; ++i) m = fmaxf(m, red[i]);
+  return m;
 }
 
 // Plain 16-byte copy: the reference kernel against which hardware traffic counters are
 // calibrated (its bytes read and written are known exactly).
-__global__ __launch_bounds__(kThreads) void copy_kernel(const uint4* __restrict__ src,
-                                                        uint4* __restrict__ dst, int64_t n) {
+__global__ __launch_bounds__(256) void copy_kernel(const uint4* __restrict__ src,
+                                                   uint4* __restrict__ dst, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
     dst[i] = src[i];
 }
 
-__global__ __launch_bounds__(kThreads) void zero_kernel(uint32_t* p0, int64_t n0, uint32_t* p1,
-                                                        int64_t n1, uint32_t* p2, int64_t n2,
-                                                        uint32_t* p3, int64_t n3) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (int64_t i = t; i < n0; i += stride) p0[i] = 0;
-  for (int64_t i = t; i < n1; i += stride) p1[i] = 0;
-  for (int64_t i = t; i < n2; i += stride) p2[i] = 0;
-  for (int64_t i = t; i < n3; i += stride) p3[i] = 0;
-}
-
+// Workgroups [0, j0.wg) serve job 0 and [j0.wg, j0.wg + j1.wg) job 1; each writes the
+// maximum |FWHT| of its rows to part[its index within the job].
 template <int DT, int LOG2B>
-__global__ __launch_bounds__(kThreads) void fwht_absmax_kernel(const void* __restrict__ src,
-                                                               int64_t rows, int64_t cols,
-                                                               uint32_t* __restrict__ slots) {
-  __shared__ float wmax[kThreads / kWave];
-  const int lane = threadIdx.x & 63;
-  const uint32_t chunks = (uint32_t)((cols + kChunk - 1) / kChunk);
-  const uint32_t items = (uint32_t)rows * chunks;
-  const uint32_t nwaves = gridDim.x * (kThreads / kWave);
+__global__ __launch_bounds__(kQThreads) void fwht_absmax_kernel(QJob j0, QJob j1,
+                                                                float* __restrict__ part0,
+                                                                float* __restrict__ part1) {
+  constexpr int U = 4;  // steps in flight
+  __shared__ float red[kQWaves];
+  const bool second = (int)blockIdx.x >= j0.wg;
+  const QJob& j = second ? j1 : j0;
+  const int wg = second ? (int)blockIdx.x - j0.wg : (int)blockIdx.x;
+  const Geo g(j, wg);
+  constexpr int EB = Elem<DT>::bytes;
   float m = 0.f;
-  for (uint32_t it = blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items; it += nwaves) {
-    const uint32_t row = it / chunks;
-    const int64_t col = (int64_t)(it - row * chunks) * kChunk + lane * 8;
-    float v[8];
-    if (col < cols) {
-      load8<DT>(static_cast<const char*>(src) + ((int64_t)row * cols + col) * Elem<DT>::bytes, v);
-    } else {
+  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  int64_t k = 0;
+  int it = 0;
+  for (int64_t s0 = 0; s0 < g.steps; s0 += U) {
+    float v[U][kVE];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = 0.f;
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        if (++it == g.iters) { it = 0; ++k; }
+      }
     }
-    fwht8<LOG2B>(v, lane);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(v[j]));
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {  // duplicated rows leave the maximum unchanged
+        fwht16<LOG2B>(v[u], g.lane);
+#pragma unroll
+        for (int e = 0; e < kVE; e += 2) m = fmaxf(m, fmaxf(fabsf(v[u][e]), fabsf(v[u][e + 1])));
+      }
+    }
   }
   m = wave_max(m);
-  if (lane == 0) wmax[threadIdx.x >> 6] = m;
+  if (g.lane == 0) red[threadIdx.x >> 6] = m;
   __syncthreads();
   if (threadIdx.x == 0) {
-    m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
-    // one atomic per workgroup, spread over kSlots cache lines; |v| >= 0: uint order
-    if (m > 0.f) atomicMax(slots + (blockIdx.x % kSlots) * kSlotStride, __float_as_uint(m));
+#pragma unroll
+    for (int i = 1; i < kQWaves; ++i) m = fmaxf(m, red[i]);
+    m = fmaxf(m, red[0]);
+    (second ? part1 : part0)[wg] = m;
   }
 }
 
+// Codes of FWHT(rows) at the reduced maximum a; the first workgroup of each job also
+// stores a.  Row sums of squares are plain stores by the group's first lane.  The clamp
+// to +-7 of the definition never engages here: |v| <= a gives |v * fl(7/a)| <= 7 (1 + 2^-24),
+// which rounds to at most 7.
 template <int DT, int LOG2B>
-__global__ __launch_bounds__(kThreads) void fwht_quant_kernel(
-    const void* __restrict__ src, int64_t rows, int64_t cols, const uint32_t* __restrict__ slots,
-    float* __restrict__ amax_out, uint8_t* __restrict__ packed, int32_t* __restrict__ row_sumsq) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t chunks = (uint32_t)((cols + kChunk - 1) / kChunk);
-  const uint32_t items = (uint32_t)rows * chunks;
-  const uint32_t nwaves = gridDim.x * (kThreads / kWave);
-  const float a = read_slots(slots);
-  if (blockIdx.x == 0 && threadIdx.x == 0) *amax_out = a;
+__global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1, QOut o0, QOut o1) {
+  constexpr int U = 4;
+  const bool second = (int)blockIdx.x >= j0.wg;
+  const QJob& j = second ? j1 : j0;
+  const QOut& o = second ? o1 : o0;
+  const int wg = second ? (int)blockIdx.x - j0.wg : (int)blockIdx.x;
+  const float a = reduce_parts(o.part, o.nparts);
+  if (wg == 0 && threadIdx.x == 0) *o.amax_out = a;
   const float inv = a > 0.f ? 7.0f / a : 0.f;
-  for (uint32_t it = blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items; it += nwaves) {
-    const uint32_t row = it / chunks;
-    const int64_t col = (int64_t)(it - row * chunks) * kChunk + lane * 8;
-    const bool live = col < cols;
-    float v[8];
-    if (live) {
-      load8<DT>(static_cast<const char*>(src) + ((int64_t)row * cols + col) * Elem<DT>::bytes, v);
-    } else {
+  const Geo g(j, wg);
+  constexpr int EB = Elem<DT>::bytes;
+  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  int64_t k = 0, kp = 0;  // load and process positions
+  int it = 0, ip = 0;
+  int ss = 0;
+  for (int64_t s0 = 0; s0 < g.steps; s0 += U) {
+    float v[U][kVE];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = 0.f;
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        if (++it == g.iters) { it = 0; ++k; }
+      }
     }
-    fwht8<LOG2B>(v, lane);
-    int q[8];
-    int ss = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      q[j] = code_of(v[j], inv);
-      ss += q[j] * q[j];
-    }
-    if (live) *reinterpret_cast<uint32_t*>(packed + (int64_t)row * (cols / 2) + col / 2) = pack8(q);
-    if (row_sumsq) {
-      ss = wave_sum(ss);
-      if (lane == 0 && ss) atomicAdd(row_sumsq + row, ss);
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        fwht16<LOG2B>(v[u], g.lane);
+        uint32_t y[kVE];
+#pragma unroll
+        for (int e = 0; e < kVE; ++e) y[e] = rne_bits(v[u][e] * inv);
+        const uint32_t w0 = pack8_bits(y), w1 = pack8_bits(y + 8);
+        ss = sumsq8(w1, sumsq8(w0, ss));
+        const bool ok = g.valid(kp);
+        const int64_t r = g.row_of(kp);
+        if (ok) reinterpret_cast<uint2*>(o.packed + r * (j.cols / 2))[(int64_t)ip * g.G + g.sub] = make_uint2(w0, w1);
+        if (++ip == g.iters) {  // end of the group's row
+          if (o.row_sumsq) {
+            ss = group_sum(ss, g.G);
+            if (ok && g.sub == 0) o.row_sumsq[r] = ss;
+          }
+          ss = 0;
+          ip = 0;
+          ++kp;
+        }
+      }
     }
   }
 }
 
 __device__ __forceinline__ int sext4(uint32_t n) { return (int)(n ^ 8u) - 8; }
 
-__global__ __launch_bounds__(kThreads) void transpose_packed_kernel(const uint8_t* __restrict__ src,
-                                                                    int64_t rows, int64_t cols,
-                                                                    uint8_t* __restrict__ dst) {
+__global__ __launch_bounds__(256) void transpose_packed_kernel(const uint8_t* __restrict__ src,
+                                                               int64_t rows, int64_t cols,
+                                                               uint8_t* __restrict__ dst) {
   __shared__ int8_t t[64][65];  // codes [row_local][col_local]
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
   const int tid = threadIdx.x;
@@ -195,86 +296,110 @@ __global__ __launch_bounds__(kThreads) void transpose_packed_kernel(const uint8_
   }
 }
 
+// Bit split of dY [N][C] (no transform: the gradient is split as it is, Sec. 4.2) and the
+// integer leverage scores of the two stacked rows of every token:
+//   c_up = isqrt(14^2 sum q_up^2 * x_sumsq * 2^16),  c_dn = isqrt(sum q_dn^2 * x_sumsq * 2^16)
+// (the common factor s_dn s_x dropped).  Each workgroup stores the count of non-zero scores
+// and their sum (u64) of its rows as one partial.
 template <int DT>
-__global__ __launch_bounds__(kThreads) void bit_split_kernel(
-    const void* __restrict__ g, int64_t N, int64_t C, const uint32_t* __restrict__ slots,
-    float* __restrict__ amax_out, uint8_t* __restrict__ qup, uint8_t* __restrict__ qdn,
-    int32_t* __restrict__ sumsq_up, int32_t* __restrict__ sumsq_dn, uint64_t seed,
-    uint64_t offset) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t chunks = (uint32_t)((C + kChunk - 1) / kChunk);
-  const uint32_t items = (uint32_t)N * chunks;
-  const uint32_t nwaves = gridDim.x * (kThreads / kWave);
-  const float a = read_slots(slots);
-  if (blockIdx.x == 0 && threadIdx.x == 0) *amax_out = a;
+__global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const float* __restrict__ part,
+                                                              int nparts, BsOut o, uint64_t seed,
+                                                              uint64_t offset) {
+  constexpr int U = 2;
+  __shared__ uint64_t red_s[kQWaves];
+  __shared__ uint32_t red_n[kQWaves];
+  const int wg = blockIdx.x;
+  const float a = reduce_parts(part, nparts);
+  if (wg == 0 && threadIdx.x == 0) *o.amax_out = a;
   const float inv = a > 0.f ? 7.0f / a : 0.f;
-  for (uint32_t it = blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); it < items; it += nwaves) {
-    const int64_t row = it / chunks;
-    const int64_t col = (int64_t)(it - (uint32_t)row * chunks) * kChunk + lane * 8;
-    const bool live = col < C;
-    float v[8];
-    if (live) {
-      load8<DT>(static_cast<const char*>(g) + (row * C + col) * Elem<DT>::bytes, v);
-    } else {
+  const Geo g(j, wg);
+  const int64_t C = j.cols;
+  constexpr int EB = Elem<DT>::bytes;
+  uint32_t nnz = 0;
+  uint64_t ssum = 0;
+  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  int64_t k = 0, kp = 0;
+  int it = 0, ip = 0;
+  int su = 0, sd = 0;
+  for (int64_t s0 = 0; s0 < g.steps; s0 += U) {
+    float v[U][kVE];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = 0.f;
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        load16<DT>(base + (g.row_of(k) * C + (int64_t)it * g.G * kVE) * EB, v[u]);
+        if (++it == g.iters) { it = 0; ++k; }
+      }
     }
-    const U4 rnd = philox_block(seed, offset, 0u, (uint64_t)(row * C + col));
-    int qu[8], qd[8];
-    int su = 0, sd = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float x = v[j] * inv;
-      const float up = rintf(x);          // |x| <= 7 (1 + 2^-23): |up| <= 7
-      const float w = 14.0f * (x - up);   // residual exact; |w| <= 7
-      const float fl = floorf(w);
-      const float thr = (w - fl) * 65536.0f;
-      const int dn = (int)fl + (((float)u16_of(rnd, j) < thr) ? 1 : 0);
-      qu[j] = (int)up;
-      qd[j] = dn;
-      su += qu[j] * qu[j];
-      sd += dn * dn;
-    }
-    if (live) {
-      const int64_t o = row * (C / 2) + col / 2;
-      *reinterpret_cast<uint32_t*>(qup + o) = pack8(qu);
-      *reinterpret_cast<uint32_t*>(qdn + o) = pack8(qd);
-    }
-    su = wave_sum(su);
-    sd = wave_sum(sd);
-    if (lane == 0) {
-      if (su) atomicAdd(sumsq_up + row, su);
-      if (sd) atomicAdd(sumsq_dn + row, sd);
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        const bool ok = g.valid(kp);
+        const int64_t r = g.row_of(kp);
+        const int64_t col = ((int64_t)ip * g.G + g.sub) * kVE;
+        uint32_t yu[kVE], yd[kVE];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const U4 rnd = philox_block(seed, offset, 0u, (uint64_t)(r * C + col + 8 * h));
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float x = v[u][8 * h + e] * inv;
+            const uint32_t bu = rne_bits(x);                  // |x| <= 7 (1 + 2^-23)
+            const float up = __uint_as_float(bu) - kRne;      // rint(x), exact
+            const float w = 14.0f * (x - up);                 // residual exact; |w| <= 7
+            const float fl = floorf(w);
+            const float thr = (w - fl) * 65536.0f;
+            const uint32_t bd = __float_as_uint(fl + kRne);   // floor(w) in the low bits
+            yu[8 * h + e] = bu;
+            yd[8 * h + e] = bd + (((float)u16_of(rnd, e) < thr) ? 1u : 0u);
+          }
+        }
+        const uint32_t u0 = pack8_bits(yu), u1 = pack8_bits(yu + 8);
+        const uint32_t d0 = pack8_bits(yd), d1 = pack8_bits(yd + 8);
+        su = sumsq8(u1, sumsq8(u0, su));
+        sd = sumsq8(d1, sumsq8(d0, sd));
+        if (ok) {
+          const int64_t o8 = r * (C / 16) + (int64_t)ip * g.G + g.sub;  // uint2 index
+          reinterpret_cast<uint2*>(o.qup)[o8] = make_uint2(u0, u1);
+          reinterpret_cast<uint2*>(o.qdn)[o8] = make_uint2(d0, d1);
+        }
+        if (++ip == g.iters) {  // end of the group's row
+          su = group_sum(su, g.G);
+          sd = group_sum(sd, g.G);
+          if (ok && g.sub == 0) {
+            o.sumsq_up[r] = su;
+            o.sumsq_dn[r] = sd;
+            const uint64_t sx = (uint32_t)o.x_sumsq[r];
+            const uint32_t cu = isqrt64(((uint64_t)(kBsRatio * kBsRatio) * (uint32_t)su * sx) << 16);
+            const uint32_t cd = isqrt64(((uint64_t)(uint32_t)sd * sx) << 16);
+            o.scores[r] = cu;
+            o.scores[o.score_pitch + r] = cd;
+            nnz += (cu > 0) + (cd > 0);
+            ssum += (uint64_t)cu + cd;
+          }
+          su = sd = 0;
+          ip = 0;
+          ++kp;
+        }
+      }
     }
   }
-}
-
-// Enough waves to fill the chip several times over; every wave loops over items.
-int grid_for(int64_t items) {
-  int64_t wg = (items + (kThreads / kWave) - 1) / (kThreads / kWave);
-  if (wg > 2048) wg = 2048;
-  if (wg < 1) wg = 1;
-  return (int)wg;
-}
-
-template <int DT, int LOG2B>
-hipError_t absmax_t(hipStream_t s, const void* src, int64_t rows, int64_t cols, uint32_t* slots) {
-  const int64_t items = rows * ((cols + kChunk - 1) / kChunk);
-  timing_begin(s);
-  fwht_absmax_kernel<DT, LOG2B><<<grid_for(items), kThreads, 0, s>>>(src, rows, cols, slots);
-  timing_end(s, kKAbsmax);
-  return hipGetLastError();
-}
-
-template <int DT, int LOG2B>
-hipError_t quant_t(hipStream_t s, const void* src, int64_t rows, int64_t cols,
-                   const uint32_t* slots, float* amax_out, uint8_t* packed, int32_t* row_sumsq) {
-  const int64_t items = rows * ((cols + kChunk - 1) / kChunk);
-  timing_begin(s);
-  fwht_quant_kernel<DT, LOG2B>
-      <<<grid_for(items), kThreads, 0, s>>>(src, rows, cols, slots, amax_out, packed, row_sumsq);
-  timing_end(s, kKQuant);
-  return hipGetLastError();
+  nnz = (uint32_t)wave_sum((int)nnz);
+  ssum = wave_sum_u64(ssum);
+  if (g.lane == 0) {
+    red_n[threadIdx.x >> 6] = nnz;
+    red_s[threadIdx.x >> 6] = ssum;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t n = 0;
+    uint64_t t = 0;
+#pragma unroll
+    for (int i = 0; i < kQWaves; ++i) {
+      n += red_n[i];
+      t += red_s[i];
+    }
+    o.parts[wg] = make_uint4(n, (uint32_t)t, (uint32_t)(t >> 32), 0u);
+  }
 }
 
 template <template <int, int> class F, int DT, typename... Args>
@@ -292,65 +417,112 @@ hipError_t dispatch_block(int log2b, Args... args) {
   return hipErrorInvalidValue;
 }
 
+// Workgroups of kernel f that fit on the device at once (cached per kernel).
+int resident_wgs(const void* f) {
+  static std::mutex mu;
+  static std::unordered_map<const void*, int> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(f);
+  if (it != cache.end()) return it->second;
+  int dev = 0, cus = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, f, kQThreads, 0) != hipSuccess)
+    return 256;
+  int n = (per > 0 ? per : 1) * (cus > 0 ? cus : 1);
+  if (n > kQMaxWg) n = kQMaxWg;
+  cache.emplace(f, n);
+  return n;
+}
+
+int64_t wgs_needed(const QJob& j) {
+  if (j.rows <= 0) return 0;
+  const int64_t per = (int64_t)(64 >> j.log2g) * kQWaves;
+  return (j.rows + per - 1) / per;
+}
+
+// Share one resident grid between two jobs: all they need if it fits, else in proportion
+// to their sizes (each at least one workgroup).
+void fit_grid(QJob& a, QJob& b, int cap) {
+  const int64_t na = wgs_needed(a), nb = wgs_needed(b);
+  if (na + nb <= cap) {
+    a.wg = (int)na;
+    b.wg = (int)nb;
+    return;
+  }
+  const double ba = (double)a.rows * a.cols, bb = (double)b.rows * b.cols;
+  int64_t wb = nb ? (int64_t)(cap * bb / (ba + bb) + 0.5) : 0;
+  if (nb && wb < 1) wb = 1;
+  if (wb > nb) wb = nb;
+  int64_t wa = cap - wb;
+  if (na && wa < 1) wa = 1;
+  if (wa > na) wa = na;
+  a.wg = (int)wa;
+  b.wg = (int)wb;
+}
+
 template <int DT, int LOG2B> struct AbsmaxF {
-  static hipError_t run(hipStream_t s, const void* src, int64_t r, int64_t c, uint32_t* a) {
-    return absmax_t<DT, LOG2B>(s, src, r, c, a);
+  static hipError_t run(hipStream_t s, QJob& j0, QJob& j1, float* p0, float* p1) {
+    const void* f = reinterpret_cast<const void*>(&fwht_absmax_kernel<DT, LOG2B>);
+    fit_grid(j0, j1, resident_wgs(f));
+    timing_begin(s);
+    fwht_absmax_kernel<DT, LOG2B><<<j0.wg + j1.wg, kQThreads, 0, s>>>(j0, j1, p0, p1);
+    timing_end(s, kKAbsmax);
+    return hipGetLastError();
   }
 };
 template <int DT, int LOG2B> struct QuantF {
-  static hipError_t run(hipStream_t s, const void* src, int64_t r, int64_t c, const uint32_t* a,
-                        float* ao, uint8_t* p, int32_t* ss) {
-    return quant_t<DT, LOG2B>(s, src, r, c, a, ao, p, ss);
+  static hipError_t run(hipStream_t s, QJob j0, QJob j1, QOut o0, QOut o1) {
+    const void* f = reinterpret_cast<const void*>(&fwht_quant_kernel<DT, LOG2B>);
+    fit_grid(j0, j1, resident_wgs(f));
+    timing_begin(s);
+    fwht_quant_kernel<DT, LOG2B><<<j0.wg + j1.wg, kQThreads, 0, s>>>(j0, j1, o0, o1);
+    timing_end(s, kKQuant);
+    return hipGetLastError();
   }
 };
 
+int log2_group(int64_t cols) {
+  const int64_t v = cols / kVE;
+  int l = 0;
+  while (l < 6 && v % (int64_t(2) << l) == 0) ++l;
+  return l;
+}
+
 }  // namespace
 
-hipError_t launch_zero(hipStream_t s, uint32_t* p0, int64_t n0, uint32_t* p1, int64_t n1,
-                       uint32_t* p2, int64_t n2, uint32_t* p3, int64_t n3) {
-  int64_t n = n0 > n1 ? n0 : n1;
-  n = n > n2 ? n : n2;
-  n = n > n3 ? n : n3;
-  int64_t wg = (n + kThreads - 1) / kThreads;
-  if (wg > 1024) wg = 1024;
-  if (wg < 1) wg = 1;
-  timing_begin(s);
-  zero_kernel<<<(int)wg, kThreads, 0, s>>>(p0, n0, p1, n1, p2, n2, p3, n3);
-  timing_end(s, kKZero);
-  return hipGetLastError();
+QJob make_job(const void* src, int64_t rows, int64_t cols) {
+  QJob j{src, rows > 0 ? rows : 0, cols, log2_group(cols), 0};
+  return j;
 }
 
 hipError_t launch_copy(hipStream_t s, const void* src, void* dst, int64_t bytes) {
   const int64_t n = bytes / 16;
-  int64_t wg = (n + kThreads - 1) / kThreads;
+  int64_t wg = (n + 255) / 256;
   if (wg > 4096) wg = 4096;
   if (wg < 1) wg = 1;
   timing_begin(s);
-  copy_kernel<<<(int)wg, kThreads, 0, s>>>(static_cast<const uint4*>(src), static_cast<uint4*>(dst), n);
+  copy_kernel<<<(int)wg, 256, 0, s>>>(static_cast<const uint4*>(src), static_cast<uint4*>(dst), n);
   timing_end(s, kKCopy);
   return hipGetLastError();
 }
 
-hipError_t launch_fwht_absmax(hipStream_t s, int dt, int log2b, const void* src, int64_t rows,
-                              int64_t cols, uint32_t* amax_bits) {
+hipError_t launch_fwht_absmax(hipStream_t s, int dt, int log2b, QJob& j0, float* part0,
+                              QJob& j1, float* part1) {
   switch (dt) {
-    case kF32: return dispatch_block<AbsmaxF, kF32>(log2b, s, src, rows, cols, amax_bits);
-    case kF16: return dispatch_block<AbsmaxF, kF16>(log2b, s, src, rows, cols, amax_bits);
-    case kBF16: return dispatch_block<AbsmaxF, kBF16>(log2b, s, src, rows, cols, amax_bits);
+    case kF32: return dispatch_block<AbsmaxF, kF32, hipStream_t, QJob&, QJob&, float*, float*>(log2b, s, j0, j1, part0, part1);
+    case kF16: return dispatch_block<AbsmaxF, kF16, hipStream_t, QJob&, QJob&, float*, float*>(log2b, s, j0, j1, part0, part1);
+    case kBF16: return dispatch_block<AbsmaxF, kBF16, hipStream_t, QJob&, QJob&, float*, float*>(log2b, s, j0, j1, part0, part1);
   }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const void* src, int64_t rows,
-                             int64_t cols, const uint32_t* slots, float* amax_out, uint8_t* packed,
-                             int32_t* row_sumsq) {
+hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const QJob& j0, const QOut& o0,
+                             const QJob& j1, const QOut& o1) {
   switch (dt) {
-    case kF32:
-      return dispatch_block<QuantF, kF32>(log2b, s, src, rows, cols, slots, amax_out, packed, row_sumsq);
-    case kF16:
-      return dispatch_block<QuantF, kF16>(log2b, s, src, rows, cols, slots, amax_out, packed, row_sumsq);
-    case kBF16:
-      return dispatch_block<QuantF, kBF16>(log2b, s, src, rows, cols, slots, amax_out, packed, row_sumsq);
+    case kF32: return dispatch_block<QuantF, kF32>(log2b, s, j0, j1, o0, o1);
+    case kF16: return dispatch_block<QuantF, kF16>(log2b, s, j0, j1, o0, o1);
+    case kBF16: return dispatch_block<QuantF, kBF16>(log2b, s, j0, j1, o0, o1);
   }
   return hipErrorInvalidValue;
 }
@@ -359,30 +531,28 @@ hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t ro
                                    uint8_t* dst) {
   dim3 grid((unsigned)(cols / 64), (unsigned)(rows / 64));
   timing_begin(s);
-  transpose_packed_kernel<<<grid, kThreads, 0, s>>>(src, rows, cols, dst);
+  transpose_packed_kernel<<<grid, 256, 0, s>>>(src, rows, cols, dst);
   timing_end(s, kKTranspose);
   return hipGetLastError();
 }
 
-hipError_t launch_bit_split(hipStream_t s, int dt, const void* g, int64_t N, int64_t C,
-                            const uint32_t* slots, float* amax_out, uint8_t* qup, uint8_t* qdn,
-                            int32_t* sumsq_up, int32_t* sumsq_dn, uint64_t seed,
-                            uint64_t offset) {
-  const int64_t items = N * ((C + kChunk - 1) / kChunk);
-  const int grid = grid_for(items);
+hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, int nparts,
+                            const BsOut& o, uint64_t seed, uint64_t offset) {
+  const void* f = dt == kF32 ? reinterpret_cast<const void*>(&bit_split_kernel<kF32>)
+                  : dt == kF16 ? reinterpret_cast<const void*>(&bit_split_kernel<kF16>)
+                               : reinterpret_cast<const void*>(&bit_split_kernel<kBF16>);
+  QJob none = make_job(nullptr, 0, j.cols);
+  fit_grid(j, none, resident_wgs(f));
   timing_begin(s);
   switch (dt) {
     case kF32:
-      bit_split_kernel<kF32><<<grid, kThreads, 0, s>>>(g, N, C, slots, amax_out, qup, qdn, sumsq_up,
-                                                      sumsq_dn, seed, offset);
+      bit_split_kernel<kF32><<<j.wg, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
       break;
     case kF16:
-      bit_split_kernel<kF16><<<grid, kThreads, 0, s>>>(g, N, C, slots, amax_out, qup, qdn, sumsq_up,
-                                                      sumsq_dn, seed, offset);
+      bit_split_kernel<kF16><<<j.wg, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
       break;
     case kBF16:
-      bit_split_kernel<kBF16><<<grid, kThreads, 0, s>>>(g, N, C, slots, amax_out, qup, qdn, sumsq_up,
-                                                       sumsq_dn, seed, offset);
+      bit_split_kernel<kBF16><<<j.wg, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
       break;
     default:
       return hipErrorInvalidValue;
