@@ -193,12 +193,26 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   const float denom = (float)(kBsRatio * (int64_t(1) << k));
   const bool want_dx = dX || (acc && which_acc == 1);
   const bool want_dw = dW || (acc && which_acc == 2);
+  const int64_t Kp = rup(N, kPad);
+  int8_t* Ag = nullptr;
+  int32_t* part_dx = nullptr;
+  const int sp_dx = gemm_splits(N, D, C, false, true);
   if (want_dx) {
-    int8_t* Ag = w.take<int8_t>(rup(N, kPad) * C);
-    const int sp = gemm_splits(N, D, C, false, true);
-    int32_t* part = w.take<int32_t>(gemm_partial_bytes(N, D, sp));
-    HQ_TRY(launch_build_ag(s, dt, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept, N, C, D,
-                           Ag, dX));
+    Ag = w.take<int8_t>(Kp * C);
+    part_dx = w.take<int32_t>(gemm_partial_bytes(N, D, sp_dx));
+  }
+  int8_t* At = nullptr;
+  uint8_t* XtT = nullptr;
+  int32_t* part_dw = nullptr;
+  const int sp_dw = gemm_splits(C, D, Kp, false, true);
+  if (want_dw) {
+    At = w.take<int8_t>(C * Kp);
+    XtT = w.take<uint8_t>(D * Kp / 2);
+    part_dw = w.take<int32_t>(gemm_partial_bytes(C, D, sp_dw));
+  }
+  HQ_TRY(launch_build_operands(s, dt, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept, sv->xq,
+                               N, C, D, Ag, At, XtT, dX));
+  if (want_dx) {
     GemmArgs g{};
     g.A = Ag; g.lda = C;
     g.B = sv->wqT; g.ldb = C / 2;
@@ -207,21 +221,14 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     g.amax1 = ag; g.amax2 = amax + 1; g.denom = denom; g.log2b = k;
     if (dX) {
       g.out = dX; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiDx, dt, false, true, g, sp, part));
+      HQ_TRY(launch_gemm(s, kEpiDx, dt, false, true, g, sp_dx, part_dx));
     }
     if (acc && which_acc == 1) {
       g.out = acc; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g, sp, part));
+      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g, sp_dx, part_dx));
     }
   }
   if (want_dw) {
-    const int64_t Kp = rup(N, kPad);
-    int8_t* At = w.take<int8_t>(C * Kp);
-    uint8_t* XtT = w.take<uint8_t>(D * Kp / 2);
-    const int sp = gemm_splits(C, D, Kp, false, true);
-    int32_t* part = w.take<int32_t>(gemm_partial_bytes(C, D, sp));
-    HQ_TRY(launch_build_dw_operands(s, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept,
-                                    sv->xq, N, C, D, At, XtT));
     GemmArgs g{};
     g.A = At; g.lda = Kp;
     g.B = XtT; g.ldb = Kp / 2;
@@ -229,11 +236,11 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     g.amax1 = ag; g.amax2 = amax; g.denom = denom; g.log2b = k;
     if (dW) {
       g.out = dW; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiDw, dt, false, true, g, sp, part));
+      HQ_TRY(launch_gemm(s, kEpiDw, dt, false, true, g, sp_dw, part_dw));
     }
     if (acc && which_acc == 2) {
       g.out = acc; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g, sp, part));
+      HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g, sp_dw, part_dw));
     }
   }
   return HQLSS_OK;
@@ -259,7 +266,7 @@ namespace hqlss {
 
 const char* kernel_name(int id) {
   static const char* names[kKCount] = {"fwht_absmax", "fwht_quant", "transpose_packed",
-                                       "bit_split", "lss_plan", "build_ag", "build_dw_operands",
+                                       "bit_split", "lss_plan", "build_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
                                        "gemm_reduce", "copy"};
   return (id >= 0 && id < kKCount) ? names[id] : "?";

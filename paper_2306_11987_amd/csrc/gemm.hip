@@ -592,8 +592,8 @@ int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4) {
   const int64_t tiles = ((M + bm - 1) / bm) * ((N + kBN - 1) / kBN);
   const int64_t stages = (K + kKS - 1) / kKS;
   if (2 * tiles >= slots || stages < 16) return 1;
-  int64_t s = (slots + tiles - 1) / tiles;  // about one workgroup per slot
-  const int64_t smax = stages / 8;          // keep >= 8 stages per split
+  int64_t s = slots / tiles;        // all splits resident at once (no second round)
+  const int64_t smax = stages / 8;  // keep >= 8 stages per split
   if (s > smax) s = smax;
   return (int)(s < 1 ? 1 : s);
 }

@@ -7,7 +7,7 @@ namespace hqlss {
 
 // Kernel ids for the timing log (kept in sync with kernel_name()).
 enum KernelId : int {
-  kKAbsmax = 0, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuildAg, kKBuildDw,
+  kKAbsmax = 0, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuild,
   kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKCount
 };
 const char* kernel_name(int id);
@@ -70,18 +70,15 @@ hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_
                            int64_t score_pitch, const uint4* parts, int nparts, int64_t N,
                            int64_t budget, uint64_t seed, uint64_t offset, uint8_t* w_up,
                            uint8_t* w_dn, int32_t* kept, int32_t* n_kept);
-// Gathered weighted rows A[i] (int8, K-interleaved) for i < round_up(n_kept, 128).
-// Also zeroes the rows of dX (if given, dtype dt) that belong to dropped tokens.
-hipError_t launch_build_ag(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
-                           const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
-                           const int32_t* n_kept, int64_t N, int64_t C, int64_t D, int8_t* Ag,
-                           void* dX);
-// A^T [C][Kp] (int8, K-interleaved) and X^_T^T [D][Kp/2] (packed), Kp = round_up(N, 128).
-hipError_t launch_build_dw_operands(hipStream_t s, const uint8_t* qup, const uint8_t* qdn,
-                                    const uint8_t* w_up, const uint8_t* w_dn,
-                                    const int32_t* kept, const int32_t* n_kept,
-                                    const uint8_t* xq, int64_t N, int64_t C, int64_t D,
-                                    int8_t* At, uint8_t* XtT);
+// GEMM operands of the kept tokens in one pass (any of Ag, At, XtT, dX may be null):
+// Ag [round_up(N,128)][C] weighted rows (int8, K-interleaved; rows < round_up(n_kept,128)
+// written), At [C][Kp] the same transposed and XtT [D][Kp/2] the gathered X^ rows
+// transposed (packed), Kp = round_up(N, 128); rows of dX (dtype dt) of dropped tokens are
+// zeroed.
+hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
+                                 const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
+                                 const int32_t* n_kept, const uint8_t* xq, int64_t N, int64_t C,
+                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX);
 
 // Integer GEMM  acc[m][n] = sum_k A[m][k] B[n][k]  (both operands K-contiguous rows).
 enum Epi : int { kEpiFwd = 0, kEpiDx = 1, kEpiDw = 2, kEpiAcc = 3, kEpiPartial = 4 };

@@ -18,7 +18,7 @@
 //      consecutive tokens per round of 8192 (vector loads and stores, one Philox block),
 //      and a block-wide scan of the per-thread counts places them.
 //
-// build_ag / build_dw_operands materialise, for the kept tokens only, the weighted integer
+// build_operands materialises, for the kept tokens only, the weighted integer
 // rows A_t = 14 w_up q_up[t] + w_dn q_dn[t] (|A| <= 126, one int8 operand that carries the
 // bit split and the 1/p factors together) and the gathered X^ rows, in the K-contiguous
 // layouts the MFMA GEMM reads.  int8 operands use the "K-interleaved" byte order of the
@@ -185,59 +185,43 @@ __device__ __forceinline__ void weighted8(uint32_t up, uint32_t dn, int wu, int 
     a[j] = kBsRatio * wu * sext4((up >> (4 * j)) & 15u) + wd * sext4((dn >> (4 * j)) & 15u);
 }
 
+// One pass over the kept tokens builds every GEMM operand the sample selects: workgroup
+// (x, y) takes kept indices [64 x, 64 x + 64) and one 64-column block.  Blocks of the C
+// columns read q_up, q_dn and the weights, form A_t and write it row-major into Ag
+// (the dX operand) and, through an LDS transpose, column-major into At (the dW operand);
+// blocks of the D columns gather X^ rows into XtT.  The last block row zeroes the rows
+// of dX that belong to dropped tokens.  Rows of Ag and columns of At / XtT between n_kept
+// and the next multiple of 128 are written as zeros (the GEMMs read whole K steps).
 template <int DT>
-__global__ __launch_bounds__(256) void build_ag_kernel(
-    const uint8_t* __restrict__ qup, const uint8_t* __restrict__ qdn,
-    const uint8_t* __restrict__ w_up, const uint8_t* __restrict__ w_dn,
-    const int32_t* __restrict__ kept, const int32_t* __restrict__ n_kept, int64_t N, int64_t C,
-    int64_t D, int8_t* __restrict__ Ag, void* __restrict__ dX) {
-  const int lane = threadIdx.x & 63;
-  const int64_t nk = *n_kept;
-  const int64_t rows = (nk + 127) / 128 * 128;  // GEMM row tiles read zeros past n_kept
-  const int64_t nwaves = (int64_t)gridDim.x * 4;
-  const int64_t last = rows > N ? rows : N;
-  for (int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); i < last; i += nwaves) {
-    if (i < rows) {
-      const bool live = i < nk;
-      const int64_t t = live ? kept[i] : 0;
-      const int wu = live ? w_up[t] : 0, wd = live ? w_dn[t] : 0;
-      for (int64_t c = lane * 8; c < C; c += 512) {
-        uint2 o = make_uint2(0u, 0u);
-        if (live) {
-          const uint32_t up = *reinterpret_cast<const uint32_t*>(qup + t * (C / 2) + c / 2);
-          const uint32_t dn = *reinterpret_cast<const uint32_t*>(qdn + t * (C / 2) + c / 2);
-          int a[8];
-          weighted8(up, dn, wu, wd, a);
-          o = interleave8(a);
-        }
-        *reinterpret_cast<uint2*>(Ag + i * C + c) = o;
-      }
-    }
-    // rows of dX that belong to dropped tokens are exactly zero
-    if (dX && i < N && (w_up[i] + w_dn[i]) == 0) {
-      const int64_t bytes = D * Elem<DT>::bytes;
-      char* row = static_cast<char*>(dX) + i * bytes;
-      for (int64_t o = lane * 16; o < bytes; o += 64 * 16)
-        *reinterpret_cast<uint4*>(row + o) = make_uint4(0u, 0u, 0u, 0u);
-    }
-  }
-}
-
-__global__ __launch_bounds__(256) void build_dw_operands_kernel(
+__global__ __launch_bounds__(256) void build_operands_kernel(
     const uint8_t* __restrict__ qup, const uint8_t* __restrict__ qdn,
     const uint8_t* __restrict__ w_up, const uint8_t* __restrict__ w_dn,
     const int32_t* __restrict__ kept, const int32_t* __restrict__ n_kept,
-    const uint8_t* __restrict__ xq, int64_t N, int64_t C, int64_t D, int8_t* __restrict__ At,
-    uint8_t* __restrict__ XtT) {
+    const uint8_t* __restrict__ xq, int64_t N, int64_t C, int64_t D, int8_t* __restrict__ Ag,
+    int8_t* __restrict__ At, uint8_t* __restrict__ XtT, void* __restrict__ dX) {
   __shared__ int8_t tile[64][65];  // [kept index][column]
+  const int tid = threadIdx.x;
+  const int64_t cb = C / 64, db = D / 64;
+  if ((int64_t)blockIdx.y == cb + db) {  // zero the dX rows of dropped tokens
+    if (!dX) return;
+    const int64_t bytes = D * Elem<DT>::bytes;
+    const int64_t t1 = (int64_t)blockIdx.x * 64 + 64 < N ? (int64_t)blockIdx.x * 64 + 64 : N;
+    for (int64_t t = (int64_t)blockIdx.x * 64 + (tid >> 6); t < t1; t += 4) {
+      if (w_up[t] + w_dn[t]) continue;
+      char* row = static_cast<char*>(dX) + t * bytes;
+      for (int64_t o = (tid & 63) * 16; o < bytes; o += 64 * 16)
+        *reinterpret_cast<uint4*>(row + o) = make_uint4(0u, 0u, 0u, 0u);
+    }
+    return;
+  }
   const int64_t nk = *n_kept;
   const int64_t kp = (nk + 127) / 128 * 128;
   const int64_t i0 = (int64_t)blockIdx.x * 64;
   if (i0 >= kp) return;
   const int64_t pitch = (N + 127) / 128 * 128;  // K pitch of At (bytes) and 2x of XtT
-  const bool isA = (int64_t)blockIdx.y < C / 64;
-  const int64_t col0 = isA ? (int64_t)blockIdx.y * 64 : ((int64_t)blockIdx.y - C / 64) * 64;
-  const int tid = threadIdx.x;
+  const bool isA = (int64_t)blockIdx.y < cb;
+  if (isA ? (!Ag && !At) : !XtT) return;
+  const int64_t col0 = isA ? (int64_t)blockIdx.y * 64 : ((int64_t)blockIdx.y - cb) * 64;
   {
     const int r = tid >> 2, q = (tid & 3) * 16;  // 64 kept rows x 4 x 16 columns
     const int64_t i = i0 + r;
@@ -261,6 +245,11 @@ __global__ __launch_bounds__(256) void build_dw_operands_kernel(
         }
       }
     }
+    if (isA && Ag) {
+      const uint2 lo = interleave8(v), hi = interleave8(v + 8);
+      *reinterpret_cast<uint4*>(Ag + i * C + col0 + q) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+    if (isA && !At) return;  // uniform: no transpose wanted
 #pragma unroll
     for (int j = 0; j < 16; ++j) tile[r][q + j] = (int8_t)v[j];
   }
@@ -300,41 +289,27 @@ hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_
   return hipGetLastError();
 }
 
-hipError_t launch_build_ag(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
-                           const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
-                           const int32_t* n_kept, int64_t N, int64_t C, int64_t D, int8_t* Ag,
-                           void* dX) {
-  int64_t wg = (N + 3) / 4;
-  if (wg > 4096) wg = 4096;
+hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
+                                 const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
+                                 const int32_t* n_kept, const uint8_t* xq, int64_t N, int64_t C,
+                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX) {
+  const int64_t pitch = (N + 127) / 128 * 128;
+  dim3 grid((unsigned)(pitch / 64), (unsigned)(C / 64 + D / 64 + 1));
   timing_begin(s);
   switch (dt) {
     case kF32:
-      build_ag_kernel<kF32><<<(int)wg, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, N, C, D, Ag, dX);
+      build_operands_kernel<kF32><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, At, XtT, dX);
       break;
     case kF16:
-      build_ag_kernel<kF16><<<(int)wg, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, N, C, D, Ag, dX);
+      build_operands_kernel<kF16><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, At, XtT, dX);
       break;
     case kBF16:
-      build_ag_kernel<kBF16><<<(int)wg, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, N, C, D, Ag, dX);
+      build_operands_kernel<kBF16><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, At, XtT, dX);
       break;
     default:
       return hipErrorInvalidValue;
   }
-  timing_end(s, kKBuildAg);
-  return hipGetLastError();
-}
-
-hipError_t launch_build_dw_operands(hipStream_t s, const uint8_t* qup, const uint8_t* qdn,
-                                    const uint8_t* w_up, const uint8_t* w_dn,
-                                    const int32_t* kept, const int32_t* n_kept,
-                                    const uint8_t* xq, int64_t N, int64_t C, int64_t D,
-                                    int8_t* At, uint8_t* XtT) {
-  const int64_t pitch = (N + 127) / 128 * 128;
-  dim3 grid((unsigned)(pitch / 64), (unsigned)(C / 64 + D / 64));
-  timing_begin(s);
-  build_dw_operands_kernel<<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D,
-                                                At, XtT);
-  timing_end(s, kKBuildDw);
+  timing_end(s, kKBuild);
   return hipGetLastError();
 }
 
