@@ -59,11 +59,12 @@ constexpr int kKS = 128;  // K elements per stage
 #endif
 template <bool A4> constexpr int tile_m() { return A4 ? HQLSS_GEMM_FWD_BM : HQLSS_GEMM_GRAD_BM; }
 
-template <int BM, bool A4>
+template <int BM, bool A4, int WN_ = 128>
 struct Cfg {
   static constexpr int BN = kBN;
-  static constexpr int WGM = BM / 64, WGN = 2, WAVES = WGM * WGN, THREADS = 64 * WAVES;
-  static constexpr int WM = 64, WN = 128, TI = 2, TJ = 4;
+  static constexpr int WAVES = BM / 32, THREADS = 64 * WAVES;
+  static constexpr int WN = WN_, WGN = BN / WN, WGM = WAVES / WGN;
+  static constexpr int WM = BM / WGM, TI = WM / 32, TJ = WN / 32;
   static constexpr int RA = A4 ? kKS / 2 : kKS;  // bytes of an A row per stage
   static constexpr int RB = kKS / 2;             // B is always INT4
   static constexpr int CPA = RA / 16, CPB = RB / 16;
@@ -84,11 +85,12 @@ __device__ __forceinline__ int swz(int r) {
 }
 
 // B-tile LDS slot s -> tile row n_t (slot order puts a lane's 16 accumulators on 16
-// consecutive n): within a wave half of 128 rows, slot 32 j + t holds
-// n = 16 j + 4 (t / 8) + (t % 4) + 64 ((t / 4) % 2).
+// consecutive n): within the WN rows of a wave, slot 32 j + t holds
+// n = 16 j + 4 (t / 8) + (t % 4) + (WN / 2) ((t / 4) % 2).
+template <int WN>
 __device__ __forceinline__ int b_row_of_slot(int s) {
-  const int wn = s >> 7, rem = s & 127, j = rem >> 5, t = rem & 31;
-  return wn * 128 + 16 * j + 4 * (t >> 3) + (t & 3) + 64 * ((t >> 2) & 1);
+  const int wn = s / WN, rem = s % WN, j = rem >> 5, t = rem & 31;
+  return wn * WN + 16 * j + 4 * (t >> 3) + (t & 3) + (WN / 2) * ((t >> 2) & 1);
 }
 
 // Widen k step `half` of a 16-byte INT4 raw read to an int8 fragment (16 x the code).
@@ -107,26 +109,27 @@ __device__ __forceinline__ v4i as_frag(const uint4& w) {
   return f;
 }
 
-// In-register Hadamard transform (block 2^LOG2B) of one lane's 64 n values of one m row:
-// v[16 j + r] is n = 16 j + r + 64 h (h = lane / 32).  Strides 1..32 run in registers,
-// the stride 64 pairs lanes l and l ^ 32.
-template <int LOG2B>
+// In-register Hadamard transform (block 2^LOG2B <= 2 NV) of one lane's NV n values of one
+// m row: v[16 j + r] is n = 16 j + r + NV h (h = lane / 32).  Strides below NV run in
+// registers, the stride NV pairs lanes l and l ^ 32.
+template <int LOG2B, int NV>
 __device__ __forceinline__ void fwht_lane(int* v, int lane) {
   constexpr int b = 1 << LOG2B;
+  static_assert(b <= 2 * NV, "Hadamard block wider than a wave tile");
 #pragma unroll
-  for (int h = 1; h < 64 && h < b; h <<= 1) {
+  for (int h = 1; h < NV && h < b; h <<= 1) {
 #pragma unroll
-    for (int e = 0; e < 64; ++e)
+    for (int e = 0; e < NV; ++e)
       if ((e & h) == 0) {
         const int a = v[e], c = v[e + h];
         v[e] = a + c;
         v[e + h] = a - c;
       }
   }
-  if constexpr (b > 64) {
+  if constexpr (b > NV) {
     const bool upper = (lane & 32) != 0;
 #pragma unroll
-    for (int e = 0; e < 64; ++e) {
+    for (int e = 0; e < NV; ++e) {
       const int p = __shfl_xor(v[e], 32);
       v[e] = upper ? (p - v[e]) : (v[e] + p);
     }
@@ -155,9 +158,9 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4));
 }
 
-template <int BM, bool A4, int EPI, int DT, int LOG2B>
-__global__ __launch_bounds__((Cfg<BM, A4>::THREADS), (Cfg<BM, A4>::OCC)) void gemm_kernel(GemmArgs g) {
-  using C_ = Cfg<BM, A4>;
+template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B>
+__global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC)) void gemm_kernel(GemmArgs g) {
+  using C_ = Cfg<BM, A4, WN>;
   constexpr int TI = C_::TI, TJ = C_::TJ, BN = C_::BN;
   constexpr bool RAW = (EPI == kEpiAcc || EPI == kEpiPartial);
   constexpr int ES = (RAW || DT == kF32) ? 4 : 2;
@@ -169,7 +172,7 @@ __global__ __launch_bounds__((Cfg<BM, A4>::THREADS), (Cfg<BM, A4>::OCC)) void ge
   __shared__ __attribute__((aligned(1024))) uint8_t smem[C_::LDS_MAIN];
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
+  const int wm = wid / C_::WGN, wn = wid % C_::WGN;
   int tm, tn;
   tile_of(tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
@@ -206,7 +209,7 @@ __global__ __launch_bounds__((Cfg<BM, A4>::THREADS), (Cfg<BM, A4>::OCC)) void ge
   for (int x = 0; x < C_::B_BPW; ++x) {
     const int s = (wid * C_::B_BPW + x) * (1024 / C_::RB) + lane / C_::CPB;
     const int c = (lane % C_::CPB) ^ swz<C_::RB>(s);
-    int64_t gn = n0 + b_row_of_slot(s);
+    int64_t gn = n0 + b_row_of_slot<C_::WN>(s);
     gn = gn < g.N ? gn : g.N - 1;
     cb[x] = c * 16;
     pb[x] = static_cast<const uint8_t*>(g.B) + gn * g.ldb + (int64_t)st0 * C_::RB + c * 16;
@@ -367,10 +370,10 @@ __global__ __launch_bounds__((Cfg<BM, A4>::THREADS), (Cfg<BM, A4>::OCC)) void ge
   __builtin_amdgcn_s_barrier();  // every wave is done with the stage buffers
 
   // ---------------------------------------------------------------- epilogue
-  // values of (i, j): row m = wm*64 + 32 i + (lane % 32), columns n = wn*128 + 16 j +
-  // 64 (lane / 32) + r.  They go through LDS so that every store writes whole rows.
+  // values of (i, j): row m = wm*WM + 32 i + (lane % 32), columns n = wn*WN + 16 j +
+  // (WN/2) (lane / 32) + r.  They go through LDS so that every store writes whole rows.
   const int ml = lane & 31;
-  const int nh = 64 * (lane >> 5);
+  const int nh = (C_::WN / 2) * (lane >> 5);
   float alpha = 0.f;
   if constexpr (EPI == kEpiFwd) {
     // fl(alpha 2^-SHIFT * fl(acc)) == fl(alpha * fl(acc >> SHIFT)): acc is a multiple of
@@ -387,7 +390,7 @@ __global__ __launch_bounds__((Cfg<BM, A4>::THREADS), (Cfg<BM, A4>::OCC)) void ge
       for (int j = 0; j < TJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) v[16 * j + r] = acc[i][j][r] >> C_::SHIFT;
-      fwht_lane<LOG2B>(v, lane);
+      fwht_lane<LOG2B, TJ * 16>(v, lane);
 #pragma unroll
       for (int j = 0; j < TJ; ++j)
 #pragma unroll
@@ -515,12 +518,17 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
   }
 }
 
+// wave tile width: int8 x INT4 GEMMs widen only the n-side operand, so their waves take
+// 128 m x 64 n (half the widening per MFMA) unless the Hadamard block needs 128 columns
+template <bool A4, int LOG2B> constexpr int wave_n() { return (A4 || LOG2B == 7) ? 128 : 64; }
+
 template <int BM, bool A4, int EPI, int DT, int LOG2B>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
-  using C_ = Cfg<BM, A4>;
+  constexpr int WN = wave_n<A4, LOG2B>();
+  using C_ = Cfg<BM, A4, WN>;
   dim3 grid((unsigned)((g.N + kBN - 1) / kBN), (unsigned)((g.M + BM - 1) / BM), (unsigned)splits);
   timing_begin(s);
-  gemm_kernel<BM, A4, EPI, DT, LOG2B><<<grid, C_::THREADS, 0, s>>>(g);
+  gemm_kernel<BM, A4, WN, EPI, DT, LOG2B><<<grid, C_::THREADS, 0, s>>>(g);
   timing_end(s, id);
   return hipGetLastError();
 }
