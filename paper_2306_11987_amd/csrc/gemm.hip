@@ -182,6 +182,15 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
     M = md < M ? md : M;
   }
   if (m0 >= M) return;  // whole workgroup: uniform exit before any barrier
+  // the scale is read up front so that its latency hides behind the main loop
+  float alpha = 0.f;
+  if constexpr (EPI == kEpiFwd) {
+    // fl(alpha 2^-SHIFT * fl(acc)) == fl(alpha * fl(acc >> SHIFT)): acc is a multiple of
+    // 2^SHIFT and both scalings by powers of two are exact
+    alpha = alpha_of(*g.amax1, *g.amax2, g.denom) * (1.0f / (float)(1 << C_::SHIFT));
+  } else if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
+    alpha = alpha_of(*g.amax1, *g.amax2, g.denom);
+  }
   int64_t K = g.K;
   if (g.k_dev) K = ((int64_t)*g.k_dev + 127) / 128 * 128;
   // split-K range of this workgroup (whole stages)
@@ -374,14 +383,6 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   // (WN/2) (lane / 32) + r.  They go through LDS so that every store writes whole rows.
   const int ml = lane & 31;
   const int nh = (C_::WN / 2) * (lane >> 5);
-  float alpha = 0.f;
-  if constexpr (EPI == kEpiFwd) {
-    // fl(alpha 2^-SHIFT * fl(acc)) == fl(alpha * fl(acc >> SHIFT)): acc is a multiple of
-    // 2^SHIFT and both scalings by powers of two are exact
-    alpha = alpha_of(*g.amax1, *g.amax2, g.denom) * (1.0f / (float)(1 << C_::SHIFT));
-  } else if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
-    alpha = alpha_of(*g.amax1, *g.amax2, g.denom);
-  }
   if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
 #pragma unroll
     for (int i = 0; i < TI; ++i) {

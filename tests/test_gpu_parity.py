@@ -133,22 +133,31 @@ def test_exact_reconstruction_on_gpu():
     assert np.array_equal(to_np(Y).astype(np.float64), exact)
 
 
-@pytest.mark.parametrize("li", [0, 1])
-def test_bench_workload_full_size_sampled(li):
-    """BERT-base FFN pair at full size (N = 16384, fp16, b = 32), in the configuration the
-    benchmark times: codes of sampled rows, the whole sample, and sampled output blocks are
-    checked against the oracle computing them one by one."""
+# (workload id, linear index) at full size: the benchmark's BERT-base FFN pair, and one
+# or two linears of each other workload (GPT-2-medium b = 128, the bf16 square/rectangular
+# sweep, the BERT-large block)
+FULL_SIZE = [(1, 0), (1, 1), (2, 0), (2, 3), (3, 2), (4, 0), (4, 4)]
+
+
+@pytest.mark.parametrize("case", FULL_SIZE, ids=lambda c: f"w{c[0]}_{synth.workload(c[0]).linears[c[1]].name}")
+def test_full_size_sampled(case):
+    """A linear of a named workload at full size, in the configuration the benchmark uses
+    (budget N): codes of every row, the whole sample, and sampled output blocks checked
+    against the oracle computing them one by one."""
     H = need_gpu()
-    lin = synth.workload(1).linears[li]
+    cid, li = case
+    lin = synth.workload(cid).linears[li]
     N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
-    say(f"full-size sampled parity {lin.name} N={N} D={D} C={C}")
-    X, W, G = synth.linear_inputs(lin, 1, li)
+    say(f"full-size sampled parity {lin.name} N={N} D={D} C={C} b={1 << k} {dt}")
+    X, W, G = synth.linear_inputs(lin, cid, li)
     saved, Y = run_forward(H, X, W, k, dt)
-    f = O.hq_forward(X, W, k, compute_output=False)  # codes of every row (cheap)
+    f = O.hq_forward(X, W, k, compute_output=False)  # codes of every row
     torch.cuda.synchronize()
+    assert to_np(saved.amax)[0] == f.amax_x and to_np(saved.amax)[1] == f.amax_w
     assert np.array_equal(to_np(saved.xq), O.pack_int4(f.xq))
     assert np.array_equal(to_np(saved.wq), O.pack_int4(f.wq))
-    rng = np.random.default_rng(0)
+    assert np.array_equal(to_np(saved.x_sumsq), f.x_sumsq.astype(np.int32))
+    rng = np.random.default_rng(cid * 10 + li)
     rows = rng.choice(N, 64, replace=False)
     ref = float(f.s_x) * float(f.s_w) * 2.0 ** -k * (f.xq[rows].astype(np.float64) @ f.wq.T.astype(np.float64))
     check_float_output("Y rows", Y[torch.from_numpy(rows).cuda()], ref, dt)
@@ -160,7 +169,6 @@ def test_bench_workload_full_size_sampled(li):
     say(f"  kept {nk}/{N}")
     A = b.A.astype(np.float64)
     kept = b.plan.kept
-    bsz = 1 << k
     a_dx, a_dw = b.alpha_dx, b.alpha_dw
     # dX on sampled kept tokens and dropped tokens
     toks = rng.choice(kept, 32, replace=False)
@@ -175,7 +183,25 @@ def test_bench_workload_full_size_sampled(li):
     accw = A[kept][:, cs].T @ f.xq[kept].astype(np.float64)
     refw = a_dw * O.fwht_rows(accw.astype(np.int64), k).astype(np.float64)
     check_float_output("dW rows", dW[torch.from_numpy(cs).cuda()], refw, dt)
-    assert bsz == 32
+
+
+def test_sampler_max_tokens():
+    """The largest admitted token count (N = 65536, eight rounds of the one-workgroup
+    sampler) with the clamp-and-rescale loop and the Bernoulli draws live (budget N/8):
+    plan and both gradients against the oracle."""
+    H = need_gpu()
+    lin, X, W, G = _case((65536, 64, 128, 5, "bf16", "lognormal"), seed=6)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    say(f"sampler at N={N}")
+    saved, _ = run_forward(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)
+    b = O.lss_backward(G, f, N // 8, 3, 11)
+    assert b.plan.R > 0 and (b.plan.e_dn > 0).any()
+    _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N // 8, 3, 11)
+    check_plan(plan, b)
+    check_backward_acc(H, plan, saved, b, N, D, C)
+    check_float_output("dX", dX, b.dX, dt)
+    check_float_output("dW", dW, b.dW, dt)
 
 
 @pytest.mark.parametrize("splits", [2, 3])
