@@ -173,6 +173,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid / C_::WGN, wn = wid % C_::WGN;
+
   int tm, tn;
   tile_of(tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
@@ -328,7 +329,10 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
     }
   };
   auto stage_ready = [&](int st) {  // this wave's loads of stage st landed, then all waves'
-    if (C_::NBUF == 3 && st + 1 < nst) wait_vm_lgkm0<C_::DMA>();
+    // loads of later stages may stay in flight: min(NBUF - 2, nst - 1 - st) of them
+    const int later = nst - 1 - st;
+    if (C_::NBUF >= 4 && later >= 2) wait_vm_lgkm0<2 * C_::DMA>();
+    else if (C_::NBUF >= 3 && later >= 1) wait_vm_lgkm0<C_::DMA>();
     else wait_vm_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
     if (st + C_::NBUF - 1 < nst) issue(st + C_::NBUF - 1);
