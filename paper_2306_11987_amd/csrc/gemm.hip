@@ -171,7 +171,9 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   static_assert(E_ROWS >= 32 && E_ROWS * E_PITCH <= C_::LDS_MAIN, "epilogue staging");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[C_::LDS_MAIN];
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // wave index as a scalar: the LDS-DMA destinations (M0) then need no lane-to-scalar moves
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / C_::WGN, wn = wid % C_::WGN;
 
   int tm, tn;
