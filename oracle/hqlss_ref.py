@@ -49,12 +49,16 @@ QMAX = 7  # Q_N = Q_P = 7 (Sec. 3.1)
 BS_RATIO = 14  # s_up / s_dn (bit-split reading)
 STREAM_SR = 0  # Philox stream of the lower-half stochastic rounding
 STREAM_MASK = 1  # Philox stream of the LSS Bernoulli masks
+MAX_LOG2_BLOCK = 7  # largest Hadamard block 2^k searched (App. A.5)
+KEEP_NONZERO = -1  # budget value selecting the keep-every-non-zero-row rule (App. A.6)
 
 __all__ = [
     "QMAX", "BS_RATIO", "fwht_rows", "hadamard_matrix_sylvester", "absmax", "quantize_int4",
     "pack_int4", "unpack_int4", "HQForward", "hq_forward", "BitSplit", "bit_split",
     "leverage_scores", "clamp_rescale", "LSSPlan", "lss_plan", "LSSBackward",
-    "lss_backward", "weighted_rows", "stochastic_round",
+    "lss_backward", "weighted_rows", "stochastic_round", "MAX_LOG2_BLOCK", "KEEP_NONZERO",
+    "resolve_budget", "hadamard_reconstruction", "hadamard_mse", "HadamardChoice",
+    "choose_hadamard_size",
 ]
 
 
@@ -180,6 +184,70 @@ def hq_forward(X: np.ndarray, W: np.ndarray, log2_block: int, compute_output: bo
 
 
 # --------------------------------------------------------------------------
+# Choice of the Hadamard block size (App. A.5)
+# --------------------------------------------------------------------------
+def hadamard_reconstruction(V: np.ndarray, log2_block: int) -> np.ndarray:
+    """V_bar = s int_s(V H) H^T (App. A.5) in float64.
+
+    The codes and the step are those of the forward quantiser (module notes: V H_u in
+    float32, s = a/7, codes rint(v * fl(7/a))).  With H_u = 2^{k/2} H the normalised
+    form gives the same codes, and V_bar = s q H_u^T / 2^k; H_u is symmetric, so the
+    product with H_u^T is the transform of the code rows, taken exactly in int64."""
+    k = int(log2_block)
+    v = fwht_rows(np.asarray(V, dtype=np.float32), k)
+    q, s = quantize_int4(v, absmax(v))
+    back = fwht_rows(q.astype(np.int64), k).astype(np.float64)
+    return float(s) * back / float(1 << k)
+
+
+def hadamard_mse(V: np.ndarray, log2_block: int) -> float:
+    """MSE(V_bar, V): mean of the squared entries of V_bar - V (0 for an empty tensor)."""
+    V = np.asarray(V, dtype=np.float32)
+    if V.size == 0:
+        return 0.0
+    d = hadamard_reconstruction(V, log2_block) - V.astype(np.float64)
+    return float(np.mean(d * d))
+
+
+@dataclass
+class HadamardChoice:
+    log2_block: int
+    mse_x: np.ndarray  # float64 [MAX_LOG2_BLOCK + 1]; nan where 2^k is not a candidate
+    mse_w: np.ndarray
+
+    @property
+    def objective(self) -> np.ndarray:
+        return self.mse_x * self.mse_w
+
+
+def choose_hadamard_size(X: np.ndarray, W: np.ndarray,
+                         max_log2_block: int = MAX_LOG2_BLOCK) -> HadamardChoice:
+    """The k minimising MSE(X_bar, X) x MSE(W_bar, W) (App. A.5).
+
+    Candidates are 0 <= k <= min(max_log2_block, 7) with D a multiple of 2^k (Sec. 3.3:
+    H is block-diagonal in 2^k blocks).  Equal objectives go to the smaller k, the
+    cheaper transform (Sec. 3.3 trade-off)."""
+    X = np.asarray(X, dtype=np.float32)
+    W = np.asarray(W, dtype=np.float32)
+    D = X.shape[1]
+    assert W.shape[1] == D
+    n = MAX_LOG2_BLOCK + 1
+    mse_x = np.full(n, np.nan)
+    mse_w = np.full(n, np.nan)
+    best, best_obj = None, None
+    for k in range(0, min(int(max_log2_block), MAX_LOG2_BLOCK) + 1):
+        if D % (1 << k):
+            continue
+        mse_x[k] = hadamard_mse(X, k)
+        mse_w[k] = hadamard_mse(W, k)
+        obj = mse_x[k] * mse_w[k]
+        if best is None or obj < best_obj:
+            best, best_obj = k, obj
+    assert best is not None
+    return HadamardChoice(best, mse_x, mse_w)
+
+
+# --------------------------------------------------------------------------
 # Bit splitting (Sec. 4.2, Eq. 4)
 # --------------------------------------------------------------------------
 @dataclass
@@ -268,6 +336,19 @@ def clamp_rescale(c: np.ndarray, budget: int):
     return np.array(clamped, dtype=bool), budget - k, S
 
 
+def resolve_budget(budget: int, N: int) -> int:
+    """0 selects B = N (Sec. 4.2: sum p_i = N).  KEEP_NONZERO selects B = 2N: no more than
+    2N rows are non-zero, so every non-zero row gets p = 1 and the sample is the
+    deterministic rule of the paper's implementation, keep the rows of non-zero norm
+    (App. A.6)."""
+    if budget == 0:
+        return N
+    if budget == KEEP_NONZERO:
+        return 2 * N
+    assert 0 < budget <= 2 * N
+    return int(budget)
+
+
 @dataclass
 class LSSPlan:
     budget: int
@@ -296,6 +377,7 @@ def lss_plan(sumsq_up, sumsq_dn, x_sumsq, budget: int, seed: int, offset: int,
       (at 2 when the token's up row is non-zero so |14 q_up + 2^e q_dn| <= 126);
     * m ~ Bern(p~) from Philox stream 1 as [u16 < 2^(16-e)]; the weight m/p~ = m 2^e."""
     N = len(sumsq_up)
+    budget = resolve_budget(budget, N)
     c = leverage_scores(sumsq_up, sumsq_dn, x_sumsq)
     clamped, R, S = clamp_rescale(c, budget)
     su = np.asarray(sumsq_up, dtype=np.int64)

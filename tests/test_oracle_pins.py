@@ -311,13 +311,21 @@ def test_keep_nonzero_special_case():
     lin = synth.small_linear(24, 32, 16, 3, grad_kind="lognormal")
     X, W, G = synth.linear_inputs(lin, 3)
     f = O.hq_forward(X, W, 3, compute_output=False)
+    assert O.resolve_budget(O.KEEP_NONZERO, 24) == 48 and O.resolve_budget(0, 24) == 24
     for seed in range(3):
-        bw = O.lss_backward(G, f, budget=48, seed=seed, offset=0)
+        bw = O.lss_backward(G, f, budget=O.KEEP_NONZERO, seed=seed, offset=0)
+        assert bw.plan.budget == 48
         assert (bw.plan.e_dn == 0).all()
         assert (f.x_sumsq > 0).all()
         nzdn = np.abs(bw.bs.q_dn).sum(1) > 0
         assert np.array_equal(bw.plan.w_dn, nzdn.astype(int))
         assert np.array_equal(bw.A, bw.bs.combined())  # exactly the bit-split product
+        # a deterministic rule: for fixed codes the masks' uniforms play no part
+        su = (bw.bs.q_up.astype(np.int64) ** 2).sum(1)
+        sd = (bw.bs.q_dn.astype(np.int64) ** 2).sum(1)
+        for mseed in range(1, 4):
+            p2 = O.lss_plan(su, sd, f.x_sumsq, O.KEEP_NONZERO, mseed, 7)
+            assert np.array_equal(p2.kept, bw.plan.kept) and np.array_equal(p2.w_dn, bw.plan.w_dn)
 
 
 # ---------------------------------------------------------------- LSS estimator (Sec. 4.2)
@@ -444,3 +452,101 @@ def test_weighted_rows_fit_int8():
         plan = O.lss_plan(su, sd, f.x_sumsq, B, 0, off)
         A = O.weighted_rows(bs, plan)
         assert np.abs(A).max() <= 126
+
+
+# ---------------------------------------------------------------- Hadamard size (App. A.5)
+def test_hadamard_mse_closed_form():
+    """x = [1, 1/2, 0, ..., 0] (D = 8), worked by hand.  k = 0: a = 1, codes (7, 4) (rint
+    of 3.5 is 4), error 4/7 - 1/2 = 1/14 on one entry: MSE = 1/14^2/8 = 1/1568.  k >= 1:
+    the first block of x H_u is (3/2, 1/2) repeated, a = 3/2, codes (7, 2), error
+    3/7 - 1/2 = -1/14 on half of the block's entries; back in the x domain the squared
+    error is divided by 2^k (H_u H_u^T = 2^k I): MSE = 1/3136 for k = 1, 2, 3."""
+    x = np.zeros((1, 8), dtype=np.float32)
+    x[0, :2] = (1.0, 0.5)
+    want = [1 / 1568, 1 / 3136, 1 / 3136, 1 / 3136]
+    for k, m in enumerate(want):
+        assert O.hadamard_mse(x, k) == pytest.approx(m, rel=1e-6)  # s = fl(a/7): ~1e-7
+    # X = W = x: objectives 1/1568^2 > 1/3136^2 (k = 1, 2, 3 tie): the smallest tied k wins
+    c = O.choose_hadamard_size(x, x, 3)
+    assert c.log2_block == 1
+    assert np.all(np.isnan(c.mse_x[4:]))
+
+
+@pytest.mark.parametrize("k", range(0, 8))
+def test_hadamard_reconstruction_matches_dense_matrices(k):
+    """V_bar = s q H^T with H the orthonormal block-diagonal matrix built from scipy's
+    Hadamard matrix (normalised, explicit dense product, codes from V H)."""
+    b, D = 1 << k, 256
+    rng = np.random.default_rng(40 + k)
+    V = rng.standard_normal((6, D)).astype(np.float32)
+    V[:, 7] *= 30
+    Hn = np.kron(np.eye(D // b), scipy.linalg.hadamard(b) / math.sqrt(b))
+    VH = V.astype(np.float64) @ Hn
+    a = np.abs(VH).max()
+    q = np.clip(np.round(VH / (a / 7)), -7, 7)
+    ref = (a / 7) * q @ Hn.T
+    got = O.hadamard_reconstruction(V, k)
+    # codes agree (no value of VH sits within rounding of a half-integer step here)
+    assert np.abs(got - ref).max() <= 1e-5 * np.abs(ref).max()
+    assert O.hadamard_mse(V, k) == pytest.approx(np.mean((ref - V) ** 2), rel=1e-5)
+
+
+@pytest.mark.parametrize("k", [0, 3, 5, 7])
+def test_hadamard_mse_parseval(k):
+    """Parseval: ||V_bar - V||^2 = ||s q - V H_u||^2 / 2^k (H_u / 2^{k/2} orthogonal), the
+    transform-domain form of the error."""
+    rng = np.random.default_rng(k)
+    V = (rng.standard_normal((16, 384)) * rng.lognormal(0, 1, size=384)).astype(np.float32)
+    v = O.fwht_rows(V, k).astype(np.float64)
+    a = np.abs(v).max()
+    q = np.rint(v * np.float32(7.0) / np.float32(a))  # only the codes matter; ties absent
+    e = (a / 7) * q - v
+    assert O.hadamard_mse(V, k) == pytest.approx(np.sum(e * e) / (1 << k) / V.size, rel=1e-5)
+
+
+def test_hadamard_mse_k0_textbook():
+    """k = 0 is plain per-tensor absmax RTN to [-7, 7]: mean((s round(x/s) - x)^2)."""
+    rng = np.random.default_rng(5)
+    V = rng.standard_normal((32, 64)).astype(np.float32)
+    s = float(np.abs(V).max()) / 7
+    ref = np.mean((s * np.round(V / s) - V) ** 2)
+    assert O.hadamard_mse(V, 0) == pytest.approx(ref, rel=1e-6)
+
+
+def test_choose_hadamard_size_exact_grid_picks_zero():
+    """X on the INT4 grid of its own absmax is exact at k = 0 (MSE 0, objective 0), and a
+    transform can only keep or lose that: k = 0 wins, ties included."""
+    rng = np.random.default_rng(6)
+    X = (rng.integers(-7, 8, size=(16, 128)) * 0.375).astype(np.float32)
+    X[0, 0] = 7 * 0.375
+    W = rng.standard_normal((32, 128)).astype(np.float32)
+    c = O.choose_hadamard_size(X, W)
+    assert c.mse_x[0] == 0.0 and c.log2_block == 0
+
+
+def test_choose_hadamard_size_outlier_channel_prefers_large_blocks():
+    """One input channel 100x the rest (the outlier structure of Sec. 3.2): a larger block
+    spreads it over more entries (Sec. 3.3), MSE_X falls with every k, and k = 7 wins."""
+    rng = np.random.default_rng(0)
+    X = rng.standard_normal((64, 128), dtype=np.float32)
+    X[:, 5] *= 100
+    W = rng.standard_normal((96, 128), dtype=np.float32) * np.float32(0.02)
+    c = O.choose_hadamard_size(X, W)
+    assert np.all(np.diff(c.mse_x) < 0)
+    assert c.log2_block == 7
+
+
+def test_choose_hadamard_size_candidates_and_scale_invariance():
+    """Only 2^k dividing D are candidates (D = 96: k <= 5), max_log2_block caps the search,
+    and scaling X by 2^j (exact) scales MSE_X by 4^j without moving the choice."""
+    rng = np.random.default_rng(8)
+    X = rng.standard_normal((8, 96), dtype=np.float32)
+    X[:, 3] *= 40
+    W = rng.standard_normal((16, 96), dtype=np.float32)
+    c = O.choose_hadamard_size(X, W)
+    assert c.log2_block <= 5 and np.all(np.isnan(c.mse_x[6:])) and not np.isnan(c.mse_x[5])
+    c2 = O.choose_hadamard_size(X, W, 2)
+    assert c2.log2_block <= 2 and np.all(np.isnan(c2.mse_x[3:]))
+    c4 = O.choose_hadamard_size(X * np.float32(8), W)
+    assert np.allclose(c4.mse_x[:6], 64 * c.mse_x[:6], rtol=1e-12)
+    assert c4.log2_block == c.log2_block
