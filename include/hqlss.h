@@ -97,9 +97,12 @@ typedef struct {
   float *amax_g;     /* [1]       a_g = max|dY|  (s_up = a_g / 7, s_dn = s_up / 14)      */
 } lss_plan_t;
 
+/* budget_rows value selecting the keep-every-non-zero-row sample (see lss_grad_plan). */
+#define HQLSS_BUDGET_KEEP_NONZERO (-1)
+
 /* Workspace sizes (bytes) for the entry points below, which = HQLSS_WS_*. */
 enum { HQLSS_WS_FWD = 0, HQLSS_WS_BWD_DX = 1, HQLSS_WS_BWD_DW = 2, HQLSS_WS_BWD = 3,
-       HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5 };
+       HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5, HQLSS_WS_HSIZE = 6 };
 size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C);
 
 /* HQ-MM forward (Sec. 3.3, Eq. 3; Procedure HQ-MM).
@@ -121,7 +124,11 @@ hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int
  *   p* by the clamp-and-rescale loop of App. A.2 with sum p* = budget (exact integers);
  *   upper rows: kept iff non-zero; lower rows: p~ = 2^-e >= p* (e <= 4, <= 2 if the upper
  *   row is non-zero), m = [u16 < 2^(16-e)] (stream 1), weight m 2^e.
- * budget_rows <= 0 selects budget = N (Sec. 4.2: sum p_i = N).  dY [N][C] input; saved is
+ * budget_rows: 1 .. 2N, or 0 for budget = N (Sec. 4.2: sum p_i = N), or
+ * HQLSS_BUDGET_KEEP_NONZERO for budget = 2N, which keeps every non-zero row with weight 1
+ * whatever the masks draw: the deterministic rule of the paper's implementation (App. A.6,
+ * keep the rows of non-zero norm); dX and dW are then the bit-split product itself.  Any
+ * other value is HQLSS_ERR_ARG.  dY [N][C] input; saved is
  * read (x_sumsq); plan: outputs (all fields required); ws: scratch of at least
  * hqlss_workspace_bytes(HQLSS_WS_PLAN, ...) bytes. */
 hqlss_status lss_grad_plan(const void *dY, const hqlss_saved_t *saved, const lss_plan_t *plan,
@@ -159,6 +166,21 @@ hqlss_status lss_linear_bwd_dw(const void *dY, const hqlss_saved_t *saved, void 
                                int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
                                int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
                                size_t ws_bytes, void *stream);
+
+/* Choice of the Hadamard block size (App. A.5).  For every candidate k (0 <= k <=
+ * max_log2_block <= 7, D a multiple of 2^k) the reconstructions V_bar = s int_s(V H) H^T of
+ * V = X and V = W, with the forward's codes and steps (fp32 transform, s = fl(a/7), codes
+ * rint(v * fl(7/a))), give MSE(V_bar, V) = ||s q - V H_u||^2 / (2^k numel) (Parseval; fp32
+ * per-element differences, fp64 sums); the k minimising MSE(X_bar, X) MSE(W_bar, W) is
+ * written to *log2_block_out, ties to the smaller k.  X [N][D], W [C][D] inputs (dtype dt,
+ * shapes as for hq_linear_fwd); log2_block_out: device int32[1]; mse_out: device
+ * double[16], MSE_X(k) at [k] and MSE_W(k) at [8 + k], NaN where k is no candidate (8-byte
+ * aligned).  ws: scratch of at least hqlss_workspace_bytes(HQLSS_WS_HSIZE, ...) bytes.
+ * Deterministic for a given device.  max_log2_block outside 0..7 is HQLSS_ERR_BLOCK. */
+hqlss_status hq_choose_hadamard_size(const void *X, const void *W, int64_t N, int64_t D,
+                                     int64_t C, hqlss_dtype dt, int max_log2_block,
+                                     int32_t *log2_block_out, double *mse_out, void *ws,
+                                     size_t ws_bytes, void *stream);
 
 /* Philox blocks one stream consumes per backward call: advance `offset` by at least this
  * much between calls that must draw independent randomness. */

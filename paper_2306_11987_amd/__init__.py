@@ -6,6 +6,7 @@ current HIP stream); every step of the operator runs in the library's HIP kernel
 Importing this package fails loudly when the library has not been built.
 """
 from ._binding import (  # noqa: F401
+    BUDGET_KEEP_NONZERO,
     DTYPE_CODES,
     HQLSSError,
     Plan,
@@ -13,6 +14,7 @@ from ._binding import (  # noqa: F401
     debug_copy,
     debug_gemm_acc,
     debug_set_gemm_splits,
+    hq_choose_hadamard_size,
     hq_linear_fwd,
     kernel_name,
     lib,
@@ -33,4 +35,5 @@ from ._binding import (  # noqa: F401
     WS_BWD,
     WS_FROM_PLAN,
     WS_PLAN,
+    WS_HSIZE,
 )

@@ -11,7 +11,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhqlss.so")
 
-WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN = 0, 1, 2, 3, 4, 5
+WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN, WS_HSIZE = 0, 1, 2, 3, 4, 5, 6
+BUDGET_KEEP_NONZERO = -1  # HQLSS_BUDGET_KEEP_NONZERO: keep every non-zero gradient row
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
 _vp, _i64, _u64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int, ctypes.c_size_t
@@ -45,6 +46,8 @@ def _load() -> ctypes.CDLL:
                                    _i64, _u64, _u64, _vp, _sz, _vp]),
         "lss_linear_bwd_dw": (st, [_vp, ctypes.POINTER(_SavedC), _vp, _i64, _i64, _i64, _int, _int,
                                    _i64, _u64, _u64, _vp, _sz, _vp]),
+        "hq_choose_hadamard_size": (st, [_vp, _vp, _i64, _i64, _i64, _int, _int, _vp, _vp, _vp, _sz,
+                                         _vp]),
         "lss_philox_offset_advance": (_u64, [_i64, _i64]),
         "hqlss_status_string": (ctypes.c_char_p, [_int]),
         "hqlss_debug_gemm_acc": (st, [_int, ctypes.POINTER(_PlanC), ctypes.POINTER(_SavedC), _vp, _i64,
@@ -173,6 +176,27 @@ def hq_linear_fwd(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Save
     sv = saved.c()
     _check(lib.hq_linear_fwd(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
                              ctypes.byref(sv), p, n, _stream(X)), "hq_linear_fwd")
+
+
+def hq_choose_hadamard_size(X: torch.Tensor, W: torch.Tensor, max_log2_block: int = 7,
+                            log2_block_out: Optional[torch.Tensor] = None,
+                            mse_out: Optional[torch.Tensor] = None,
+                            ws: Optional[torch.Tensor] = None):
+    """Enqueues the block-size search; returns (log2_block int32 [1], mse float64 [16]) on
+    the device: MSE_X(k) at [k], MSE_W(k) at [8 + k], NaN where k is no candidate."""
+    N, D = X.shape
+    C = W.shape[0]
+    if log2_block_out is None:
+        log2_block_out = torch.empty(1, dtype=torch.int32, device=X.device)
+    if mse_out is None:
+        mse_out = torch.empty(16, dtype=torch.float64, device=X.device)
+    if ws is None:
+        ws = workspace(WS_HSIZE, N, D, C, X.device)
+    p, n = _ws(ws)
+    _check(lib.hq_choose_hadamard_size(_ptr(X), _ptr(W), N, D, C, _dt(X), int(max_log2_block),
+                                       _ptr(log2_block_out), _ptr(mse_out), p, n, _stream(X)),
+           "hq_choose_hadamard_size")
+    return log2_block_out, mse_out
 
 
 def lss_grad_plan(dY: torch.Tensor, saved: Saved, plan: Plan, D: int, budget: int = 0, seed: int = 0,

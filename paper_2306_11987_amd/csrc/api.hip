@@ -96,6 +96,10 @@ size_t plan_scratch_bytes(int64_t N) {
 size_t plan_bytes(int64_t N, int64_t C) {
   return al(N * C / 2) * 2 + al(4 * N) * 2 + al(N) * 2 + al(4 * N) + al(4) * 2;
 }
+// block-size search: per-workgroup maxima (float) and error sums (double) of X and W
+constexpr size_t kHsizeMaxBytes = size_t(kQMaxWg) * 8 * sizeof(float);
+constexpr size_t kHsizeErrBytes = size_t(kQMaxWg) * 8 * sizeof(double);
+size_t hsize_bytes() { return 2 * al(kHsizeMaxBytes) + 2 * al(kHsizeErrBytes); }
 size_t dx_bytes(int64_t N, int64_t D, int64_t C) {
   return al(rup(N, kPad) * C) + dx_gemm_partial(N, D, C);
 }
@@ -256,8 +260,15 @@ hqlss_status check_bwd_common(const void* dY, const hqlss_saved_t* saved, int64_
   if ((st = check_saved(saved))) return st;
   if (!a16(dY)) return HQLSS_ERR_ALIGN;
   if ((st = check_bwd_overflow(N, D, C, log2_block))) return st;
-  if (budget > 2 * N) return HQLSS_ERR_ARG;
+  if (budget > 2 * N || budget < HQLSS_BUDGET_KEEP_NONZERO) return HQLSS_ERR_ARG;
   return HQLSS_OK;
+}
+
+// 0 -> N (Sec. 4.2), HQLSS_BUDGET_KEEP_NONZERO -> 2N (every non-zero row kept), else itself.
+int64_t resolve_budget(int64_t budget_rows, int64_t N) {
+  if (budget_rows == 0) return N;
+  if (budget_rows == HQLSS_BUDGET_KEEP_NONZERO) return 2 * N;
+  return budget_rows;
 }
 
 }  // namespace
@@ -268,7 +279,8 @@ const char* kernel_name(int id) {
   static const char* names[kKCount] = {"fwht_absmax", "fwht_quant", "transpose_packed",
                                        "bit_split", "lss_plan", "build_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
-                                       "gemm_reduce", "copy"};
+                                       "gemm_reduce", "copy", "hsize_max", "hsize_err",
+                                       "hsize_pick"};
   return (id >= 0 && id < kKCount) ? names[id] : "?";
 }
 
@@ -298,6 +310,7 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
       return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C) + dw_bytes(N, D, C);
     case HQLSS_WS_FROM_PLAN: return dx_bytes(N, D, C) + dw_bytes(N, D, C);
     case HQLSS_WS_PLAN: return plan_scratch_bytes(N);
+    case HQLSS_WS_HSIZE: return hsize_bytes();
   }
   return 0;
 }
@@ -339,6 +352,31 @@ hqlss_status hq_linear_fwd(const void* X, const void* W, void* Y, int64_t N, int
   return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
 }
 
+hqlss_status hq_choose_hadamard_size(const void* X, const void* W, int64_t N, int64_t D,
+                                     int64_t C, hqlss_dtype dt, int max_log2_block,
+                                     int32_t* log2_block_out, double* mse_out, void* ws,
+                                     size_t ws_bytes, void* stream) {
+  if (!X || !W || !log2_block_out || !mse_out) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if (max_log2_block < 0 || max_log2_block > 7) return HQLSS_ERR_BLOCK;
+  if ((st = check_dtype(dt))) return st;
+  if (!a16(X) || !a16(W) || !a4(log2_block_out) ||
+      (reinterpret_cast<uintptr_t>(mse_out) & 7) != 0)
+    return HQLSS_ERR_ALIGN;
+  if (!ws || ws_bytes < hsize_bytes()) return HQLSS_ERR_WORKSPACE;
+  if (!a16(ws)) return HQLSS_ERR_ALIGN;
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  float* mx0 = w.take<float>(kHsizeMaxBytes);
+  float* mx1 = w.take<float>(kHsizeMaxBytes);
+  double* e0 = w.take<double>(kHsizeErrBytes);
+  double* e1 = w.take<double>(kHsizeErrBytes);
+  QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
+  HQ_TRY(launch_hsize_search(static_cast<hipStream_t>(stream), dt, jx, jw, mx0, mx1, e0, e1,
+                             max_log2_block, log2_block_out, mse_out));
+  return HQLSS_OK;
+}
+
 hqlss_status lss_grad_plan(const void* dY, const hqlss_saved_t* saved, const lss_plan_t* plan,
                            int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int64_t budget_rows,
                            uint64_t seed, uint64_t offset, void* ws, size_t ws_bytes,
@@ -348,7 +386,7 @@ hqlss_status lss_grad_plan(const void* dY, const hqlss_saved_t* saved, const lss
   if ((st = check_plan(plan))) return st;
   if (!ws || ws_bytes < plan_scratch_bytes(N)) return HQLSS_ERR_WORKSPACE;
   if (!a16(ws)) return HQLSS_ERR_ALIGN;
-  const int64_t B = budget_rows <= 0 ? N : budget_rows;
+  const int64_t B = resolve_budget(budget_rows, N);
   Carve w{static_cast<char*>(ws), 0, ws_bytes};
   return do_plan(dY, saved, plan, N, C, dt, B, seed, offset, w, static_cast<hipStream_t>(stream));
 }
@@ -388,7 +426,7 @@ static hqlss_status bwd_impl(const void* dY, const hqlss_saved_t* saved, void* d
   Carve w{static_cast<char*>(ws), 0, ws_bytes};
   lss_plan_t p;
   plan_from_ws(w, N, C, &p);
-  const int64_t B = budget_rows <= 0 ? N : budget_rows;
+  const int64_t B = resolve_budget(budget_rows, N);
   if ((st = do_plan(dY, saved, &p, N, C, dt, B, seed, offset, w, s))) return st;
   return do_grads(&p, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w, s);
 }

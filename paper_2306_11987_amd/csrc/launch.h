@@ -8,7 +8,8 @@ namespace hqlss {
 // Kernel ids for the timing log (kept in sync with kernel_name()).
 enum KernelId : int {
   kKAbsmax = 0, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuild,
-  kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKCount
+  kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKHsizeMax, kKHsizeErr,
+  kKHsizePick, kKCount
 };
 const char* kernel_name(int id);
 
@@ -65,6 +66,13 @@ struct BsOut {
 };
 hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, int nparts,
                             const BsOut& o, uint64_t seed, uint64_t offset);
+// Hadamard block-size search of X (j0) and W (j1), equal cols (App. A.5): maxima of all
+// nested transforms k = 0..7 into mx[wg][8], error sums into err[wg][8] (each buffer
+// kQMaxWg * 8 entries), then *k_out and mse_out[16] (MSE_X(k), then MSE_W(k); NaN for k
+// not a candidate: k > kmax or cols % 2^k != 0).
+hipError_t launch_hsize_search(hipStream_t s, int dt, QJob& j0, QJob& j1, float* mx0, float* mx1,
+                               double* err0, double* err1, int kmax, int32_t* k_out,
+                               double* mse_out);
 // leverage scores, clamp-rescale, masks, compaction (one workgroup).
 hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_t* scores,
                            int64_t score_pitch, const uint4* parts, int nparts, int64_t N,

@@ -402,6 +402,234 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
   }
 }
 
+// ---------------------------------------------------------------- block-size search
+// Choice of the Hadamard block 2^k (App. A.5): k minimising MSE(X_bar, X) MSE(W_bar, W),
+// V_bar = s int_s(V H) H^T.  The transform with strides ascending is nested: after the
+// stages of strides 1 .. 2^(k-1) every 2^k block holds its own FWHT, so one pass over the
+// data yields the transforms of all k = 0..7 in turn.  The error is taken in the transform
+// domain, ||V_bar - V||^2 = ||s q - V H_u||^2 / 2^k (H_u / 2^(k/2) is orthogonal), so it
+// needs no inverse transform.  For D not a multiple of 128 the deepest stages mix blocks
+// that are no candidates; their values are computed and never used.
+constexpr int kLevels = 8;  // k = 0 .. 7
+static_assert(kQWaves == kLevels, "pass 2 reduces one level per wave");
+
+// One butterfly stage at stride H (in-lane for H < 16, else across lanes H / 16 apart).
+template <int H>
+__device__ __forceinline__ void fwht_stage(float v[16], int lane) {
+  if constexpr (H < 16) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if ((j & H) == 0) {
+        const float a = v[j], c = v[j + H];
+        v[j] = a + c;
+        v[j + H] = a - c;
+      }
+    }
+  } else {
+    constexpr int M = H / 16;
+    const uint32_t sgn = (lane & M) ? 0x80000000u : 0u;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const float own = __uint_as_float(__float_as_uint(v[j]) ^ sgn);
+      v[j] = add_xor_lane<M>(v[j], own);
+    }
+  }
+}
+
+// Calls f(level, v) for level 0 (the input) and after each of the 7 stages.
+template <class F>
+__device__ __forceinline__ void fwht_nested(float v[16], int lane, F&& f) {
+  f(0, v);
+  fwht_stage<1>(v, lane);  f(1, v);
+  fwht_stage<2>(v, lane);  f(2, v);
+  fwht_stage<4>(v, lane);  f(3, v);
+  fwht_stage<8>(v, lane);  f(4, v);
+  fwht_stage<16>(v, lane); f(5, v);
+  fwht_stage<32>(v, lane); f(6, v);
+  fwht_stage<64>(v, lane); f(7, v);
+}
+
+// Pass 1: per-workgroup maxima of |FWHT_k(rows)| for every k, part[wg * 8 + k].
+template <int DT>
+__global__ __launch_bounds__(kQThreads) void hsize_max_kernel(QJob j0, QJob j1,
+                                                              float* __restrict__ part0,
+                                                              float* __restrict__ part1) {
+  constexpr int U = 2;
+  __shared__ float red[kQWaves][kLevels];
+  const bool second = (int)blockIdx.x >= j0.wg;
+  const QJob& j = second ? j1 : j0;
+  const int wg = second ? (int)blockIdx.x - j0.wg : (int)blockIdx.x;
+  const Geo g(j, wg);
+  constexpr int EB = Elem<DT>::bytes;
+  float m[kLevels];
+#pragma unroll
+  for (int l = 0; l < kLevels; ++l) m[l] = 0.f;
+  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  int64_t k = 0;
+  int it = 0;
+  for (int64_t s0 = 0; s0 < g.steps; s0 += U) {
+    float v[U][kVE];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        if (++it == g.iters) { it = 0; ++k; }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {  // duplicated rows leave the maxima unchanged
+        fwht_nested(v[u], g.lane, [&](int l, const float* x) {
+#pragma unroll
+          for (int e = 0; e < kVE; e += 2) m[l] = fmaxf(m[l], fmaxf(fabsf(x[e]), fabsf(x[e + 1])));
+        });
+      }
+    }
+  }
+#pragma unroll
+  for (int l = 0; l < kLevels; ++l) {
+    const float w = wave_max(m[l]);
+    if (g.lane == 0) red[threadIdx.x >> 6][l] = w;
+  }
+  __syncthreads();
+  if (threadIdx.x < kLevels) {
+    float r = red[0][threadIdx.x];
+#pragma unroll
+    for (int i = 1; i < kQWaves; ++i) r = fmaxf(r, red[i][threadIdx.x]);
+    (second ? part1 : part0)[wg * kLevels + threadIdx.x] = r;
+  }
+}
+
+// Pass 2: per-workgroup sums over valid rows of (s_k q - v)^2 for every k, with
+// s_k = fl(a_k / 7) and q = rint(v fl(7 / a_k)) the forward quantiser's codes (no clamp
+// needed, as there).  Each 16-element chunk is summed in fp32 (one fused multiply-add
+// per element on the correctly rounded difference), chunks in fp64; err[wg * 8 + k].
+template <int DT>
+__global__ __launch_bounds__(kQThreads) void hsize_err_kernel(QJob j0, QJob j1,
+                                                              const float* __restrict__ mx0, int n0,
+                                                              const float* __restrict__ mx1, int n1,
+                                                              double* __restrict__ err0,
+                                                              double* __restrict__ err1) {
+  constexpr int U = 2;
+  __shared__ float amax[kLevels];
+  __shared__ double red[kQWaves][kLevels];
+  const bool second = (int)blockIdx.x >= j0.wg;
+  const QJob& j = second ? j1 : j0;
+  const int wg = second ? (int)blockIdx.x - j0.wg : (int)blockIdx.x;
+  {  // a_k = max over the pass-1 partials of this tensor: 64 lanes per level
+    const float* mx = second ? mx1 : mx0;
+    const int n = second ? n1 : n0;
+    const int l = threadIdx.x >> 6, lane = threadIdx.x & 63;  // 8 waves = 8 levels
+    float r = 0.f;
+    for (int i = lane; i < n; i += 64) r = fmaxf(r, mx[i * kLevels + l]);
+    r = wave_max(r);
+    if (lane == 0) amax[l] = r;
+    __syncthreads();
+  }
+  float inv[kLevels], st[kLevels];
+#pragma unroll
+  for (int l = 0; l < kLevels; ++l) {
+    const float a = amax[l];
+    inv[l] = a > 0.f ? 7.0f / a : 0.f;
+    st[l] = a / 7.0f;
+  }
+  const Geo g(j, wg);
+  constexpr int EB = Elem<DT>::bytes;
+  double acc[kLevels];
+#pragma unroll
+  for (int l = 0; l < kLevels; ++l) acc[l] = 0.0;
+  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  int64_t k = 0, kp = 0;
+  int it = 0, ip = 0;
+  for (int64_t s0 = 0; s0 < g.steps; s0 += U) {
+    float v[U][kVE];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        if (++it == g.iters) { it = 0; ++k; }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        const bool ok = g.valid(kp);
+        fwht_nested(v[u], g.lane, [&](int l, const float* x) {
+          float e2 = 0.f;
+#pragma unroll
+          for (int e = 0; e < kVE; ++e) {
+            const float q = __builtin_rintf(x[e] * inv[l]);
+            const float d = __builtin_fmaf(st[l], q, -x[e]);
+            e2 = __builtin_fmaf(d, d, e2);
+          }
+          acc[l] += ok ? (double)e2 : 0.0;
+        });
+        if (++ip == g.iters) { ip = 0; ++kp; }
+      }
+    }
+  }
+#pragma unroll
+  for (int l = 0; l < kLevels; ++l) {
+    double w = acc[l];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) w += __shfl_xor(w, o);
+    if (g.lane == 0) red[threadIdx.x >> 6][l] = w;
+  }
+  __syncthreads();
+  if (threadIdx.x < kLevels) {
+    double r = red[0][threadIdx.x];
+#pragma unroll
+    for (int i = 1; i < kQWaves; ++i) r += red[i][threadIdx.x];
+    (second ? err1 : err0)[wg * kLevels + threadIdx.x] = r;
+  }
+}
+
+// Pass 3 (one workgroup of 256): MSE_k = sum / (2^k numel) per tensor, the candidates
+// k <= kmax with cols % 2^k == 0, and the argmin of MSE_X MSE_W (ties to the smaller k).
+// mse_out[k] = MSE_X(k), mse_out[8 + k] = MSE_W(k), NaN for k not a candidate.
+__global__ __launch_bounds__(256) void hsize_pick_kernel(const double* __restrict__ err0, int n0,
+                                                         const double* __restrict__ err1, int n1,
+                                                         double numel0, double numel1, int64_t cols,
+                                                         int kmax, int32_t* __restrict__ k_out,
+                                                         double* __restrict__ mse_out) {
+  __shared__ double red[2][32][kLevels];
+  const int l = threadIdx.x & 7, slot = threadIdx.x >> 3;  // 32 slots per level
+  double a = 0.0, b = 0.0;
+  for (int i = slot; i < n0; i += 32) a += err0[i * kLevels + l];
+  for (int i = slot; i < n1; i += 32) b += err1[i * kLevels + l];
+  red[0][slot][l] = a;
+  red[1][slot][l] = b;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int best = 0;
+    double best_obj = 0.0;
+    bool any = false;
+    for (int k = 0; k < kLevels; ++k) {
+      double sx = 0.0, sw = 0.0;
+      for (int i = 0; i < 32; ++i) {
+        sx += red[0][i][k];
+        sw += red[1][i][k];
+      }
+      const double scale = (double)(1 << k);
+      const double mx = numel0 > 0 ? sx / (scale * numel0) : 0.0;
+      const double mw = numel1 > 0 ? sw / (scale * numel1) : 0.0;
+      const bool cand = k <= kmax && cols % (int64_t(1) << k) == 0;
+      const double nan = __longlong_as_double(0x7FF8000000000000LL);
+      mse_out[k] = cand ? mx : nan;
+      mse_out[kLevels + k] = cand ? mw : nan;
+      if (cand) {
+        const double obj = mx * mw;
+        if (!any || obj < best_obj) {
+          best = k;
+          best_obj = obj;
+          any = true;
+        }
+      }
+    }
+    *k_out = best;
+  }
+}
+
 template <template <int, int> class F, int DT, typename... Args>
 hipError_t dispatch_block(int log2b, Args... args) {
   switch (log2b) {
@@ -558,6 +786,48 @@ hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, i
       return hipErrorInvalidValue;
   }
   timing_end(s, kKBitSplit);
+  return hipGetLastError();
+}
+
+
+hipError_t launch_hsize_search(hipStream_t s, int dt, QJob& j0, QJob& j1, float* mx0, float* mx1,
+                               double* err0, double* err1, int kmax, int32_t* k_out,
+                               double* mse_out) {
+  const void* fm = dt == kF32 ? reinterpret_cast<const void*>(&hsize_max_kernel<kF32>)
+                   : dt == kF16 ? reinterpret_cast<const void*>(&hsize_max_kernel<kF16>)
+                                : reinterpret_cast<const void*>(&hsize_max_kernel<kBF16>);
+  const void* fe = dt == kF32 ? reinterpret_cast<const void*>(&hsize_err_kernel<kF32>)
+                   : dt == kF16 ? reinterpret_cast<const void*>(&hsize_err_kernel<kF16>)
+                                : reinterpret_cast<const void*>(&hsize_err_kernel<kBF16>);
+  if (dt != kF32 && dt != kF16 && dt != kBF16) return hipErrorInvalidValue;
+  QJob a0 = j0, a1 = j1;
+  fit_grid(a0, a1, resident_wgs(fm));
+  timing_begin(s);
+  if (dt == kF32) hsize_max_kernel<kF32><<<a0.wg + a1.wg, kQThreads, 0, s>>>(a0, a1, mx0, mx1);
+  else if (dt == kF16) hsize_max_kernel<kF16><<<a0.wg + a1.wg, kQThreads, 0, s>>>(a0, a1, mx0, mx1);
+  else hsize_max_kernel<kBF16><<<a0.wg + a1.wg, kQThreads, 0, s>>>(a0, a1, mx0, mx1);
+  timing_end(s, kKHsizeMax);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  QJob b0 = j0, b1 = j1;
+  fit_grid(b0, b1, resident_wgs(fe));
+  timing_begin(s);
+  if (dt == kF32)
+    hsize_err_kernel<kF32><<<b0.wg + b1.wg, kQThreads, 0, s>>>(b0, b1, mx0, a0.wg, mx1, a1.wg, err0, err1);
+  else if (dt == kF16)
+    hsize_err_kernel<kF16><<<b0.wg + b1.wg, kQThreads, 0, s>>>(b0, b1, mx0, a0.wg, mx1, a1.wg, err0, err1);
+  else
+    hsize_err_kernel<kBF16><<<b0.wg + b1.wg, kQThreads, 0, s>>>(b0, b1, mx0, a0.wg, mx1, a1.wg, err0, err1);
+  timing_end(s, kKHsizeErr);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  timing_begin(s);
+  hsize_pick_kernel<<<1, 256, 0, s>>>(err0, b0.wg, err1, b1.wg, (double)j0.rows * (double)j0.cols,
+                                      (double)j1.rows * (double)j1.cols, j0.cols, kmax, k_out,
+                                      mse_out);
+  timing_end(s, kKHsizePick);
+  j0.wg = b0.wg;
+  j1.wg = b1.wg;
   return hipGetLastError();
 }
 

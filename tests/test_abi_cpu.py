@@ -114,6 +114,7 @@ def test_bwd_argument_errors():
     assert bwd(dt=7) == DTYPE
     assert bwd(dX=FAKE + 2) == ALIGN
     assert bwd(budget=1000) == ARG  # budget > 2N
+    assert bwd(budget=-2) == ARG  # below HQLSS_BUDGET_KEEP_NONZERO
     assert bwd(ws=None) == WS
     assert bwd(nbytes=100) == WS
     assert bwd(N=70000) == SHAPE  # sampler limit
@@ -123,6 +124,33 @@ def test_bwd_argument_errors():
                                  FAKE, 1 << 40, None) == NULL
     assert lib.lss_linear_bwd_dw(FAKE, ctypes.byref(_saved()), None, 128, 256, 256, 0, 5, 0, 0, 0,
                                  FAKE, 1 << 40, None) == NULL
+
+
+def test_budget_keep_nonzero_constant():
+    txt = open(HEADER).read()
+    m = re.search(r"#define HQLSS_BUDGET_KEEP_NONZERO \((-?\d+)\)", txt)
+    assert m and int(m.group(1)) == H.BUDGET_KEEP_NONZERO == -1
+
+
+def hsize(X=FAKE, W=FAKE, N=128, D=256, C=256, dt=0, kmax=7, k_out=FAKE, mse=FAKE, ws=FAKE,
+          nbytes=1 << 40):
+    return lib.hq_choose_hadamard_size(X, W, N, D, C, dt, kmax, k_out, mse, ws, nbytes, None)
+
+
+def test_choose_hadamard_size_argument_errors():
+    assert H.workspace_bytes(H.WS_HSIZE, 128, 256, 256) == H.workspace_bytes(H.WS_HSIZE, 1 << 20, 4096, 4096) > 0
+    assert hsize(X=None) == NULL
+    assert hsize(mse=None) == NULL
+    assert hsize(k_out=None) == NULL
+    assert hsize(N=0) == SHAPE
+    assert hsize(D=96) == SHAPE
+    assert hsize(kmax=8) == BLOCK
+    assert hsize(kmax=-1) == BLOCK
+    assert hsize(dt=3) == DTYPE
+    assert hsize(W=FAKE + 4) == ALIGN
+    assert hsize(mse=FAKE + 4) == ALIGN
+    assert hsize(ws=None) == WS
+    assert hsize(nbytes=1024) == WS
 
 
 def test_debug_acc_errors():
