@@ -32,17 +32,91 @@ __device__ __forceinline__ uint32_t f2bf(float f) {
   return u >> 16;
 }
 
+// ---------------------------------------------------------------- streaming access
+// Loads and stores of data that is touched once per kernel (inputs streamed through a
+// quantiser, outputs written for a later kernel) carry the non-temporal hint: they do not
+// allocate in the caches, so they neither evict operands other kernels reuse nor wait for
+// the write-back of dirty lines a previous kernel left behind.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+template <bool NT = true>
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+  if constexpr (NT) {
+    const u32x4 v = __builtin_nontemporal_load(static_cast<const u32x4*>(p));
+    return make_uint4(v[0], v[1], v[2], v[3]);
+  } else {
+    return *static_cast<const uint4*>(p);
+  }
+}
+template <bool NT = true>
+__device__ __forceinline__ uint2 ld_stream2(const void* p) {
+  if constexpr (NT) {
+    const u32x2 v = __builtin_nontemporal_load(static_cast<const u32x2*>(p));
+    return make_uint2(v[0], v[1]);
+  } else {
+    return *static_cast<const uint2*>(p);
+  }
+}
+template <bool NT = true>
+__device__ __forceinline__ void st_stream(void* p, uint4 v) {
+  if constexpr (NT) {
+    const u32x4 w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, static_cast<u32x4*>(p));
+  } else {
+    *static_cast<uint4*>(p) = v;
+  }
+}
+template <bool NT = true>
+__device__ __forceinline__ void st_stream2(void* p, uint2 v) {
+  if constexpr (NT) {
+    const u32x2 w = {v.x, v.y};
+    __builtin_nontemporal_store(w, static_cast<u32x2*>(p));
+  } else {
+    *static_cast<uint2*>(p) = v;
+  }
+}
+// Cache policy per access site (1 = streaming, 0 = cached)
+#ifndef HQ_NT_ABS_LD
+#define HQ_NT_ABS_LD 1
+#endif
+#ifndef HQ_NT_Q_LD
+#define HQ_NT_Q_LD 1
+#endif
+#ifndef HQ_NT_Q_ST
+#define HQ_NT_Q_ST 0
+#endif
+#ifndef HQ_NT_BS_LD
+#define HQ_NT_BS_LD 1
+#endif
+#ifndef HQ_NT_BS_ST
+#define HQ_NT_BS_ST 0
+#endif
+#ifndef HQ_NT_B_LD
+#define HQ_NT_B_LD 0
+#endif
+#ifndef HQ_NT_B_ST
+#define HQ_NT_B_ST 0
+#endif
+#ifndef HQ_NT_G_ST
+#define HQ_NT_G_ST 1
+#endif
+#ifndef HQ_NT_R_LD
+#define HQ_NT_R_LD 0
+#endif
+#ifndef HQ_NT_P_ST
+#define HQ_NT_P_ST 0
+#endif
+
 // Load 8 consecutive elements starting at p (16-byte aligned for fp16/bf16,
-// 32-byte aligned for fp32) and widen them to fp32.
-template <int DT>
+// 32-byte aligned for fp32; streaming) and widen them to fp32.
+template <int DT, bool NT = true>
 __device__ __forceinline__ void load8(const void* p, float v[8]) {
   if constexpr (DT == kF32) {
-    const float4* q = reinterpret_cast<const float4*>(p);
-    float4 a = q[0], b = q[1];
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    const uint4 a = ld_stream<NT>(p), b = ld_stream<NT>(static_cast<const char*>(p) + 16);
+    v[0] = __uint_as_float(a.x); v[1] = __uint_as_float(a.y); v[2] = __uint_as_float(a.z); v[3] = __uint_as_float(a.w);
+    v[4] = __uint_as_float(b.x); v[5] = __uint_as_float(b.y); v[6] = __uint_as_float(b.z); v[7] = __uint_as_float(b.w);
   } else {
-    uint4 a = *reinterpret_cast<const uint4*>(p);
+    uint4 a = ld_stream<NT>(p);
     uint32_t w[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -78,6 +152,24 @@ __device__ __forceinline__ void store_vec(void* p, const float* v) {
       for (int j = 0; j < NV / 2; j += 2)
         reinterpret_cast<uint2*>(p)[j / 2] = make_uint2(w[j], w[j + 1]);
     }
+  }
+}
+
+// store_vec to global memory with the streaming hint (NV = 8).
+template <int DT, bool NT = true>
+__device__ __forceinline__ void store8_stream(void* p, const float* v) {
+  if constexpr (DT == kF32) {
+    st_stream<NT>(p, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])));
+    st_stream<NT>(static_cast<char*>(p) + 16,
+              make_uint4(__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]), __float_as_uint(v[7])));
+  } else {
+    uint32_t w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (DT == kF16) w[j] = f2h(v[2 * j]) | (f2h(v[2 * j + 1]) << 16);
+      else w[j] = f2bf(v[2 * j]) | (f2bf(v[2 * j + 1]) << 16);
+    }
+    st_stream<NT>(p, make_uint4(w[0], w[1], w[2], w[3]));
   }
 }
 

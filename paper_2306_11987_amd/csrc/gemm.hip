@@ -47,7 +47,6 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(1))) void glb_void;
 
 constexpr int kBN = 256;  // workgroup tile width (n)
 constexpr int kKS = 128;  // K elements per stage
@@ -151,6 +150,17 @@ __device__ __forceinline__ void tile_of(int& tm, int& tn) {
   tn = Lp % tiles_n;
 }
 
+// 16-byte LDS-DMA load (global_load_lds_dwordx4): each lane's 16 bytes at g land at
+// lds_base + 16 * lane.  Issued as inline assembly with a memory clobber: the compiler
+// keeps it in program order with every other memory access, but does not treat it as a
+// pending LDS write; it would otherwise wait for every such load before any later LDS
+// read, including the loads just issued for a later stage.  The stage pipeline waits for
+// exactly the loads each stage needs.
+__device__ __forceinline__ void dma16(const void* g, void* lds_base) {
+  const uint32_t l = (uint32_t)(uintptr_t)(lds_void*)lds_base;
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(l) : "memory");
+}
+
 // s_waitcnt: vector-memory count <= n, LDS count 0 (gfx9 encoding: vmcnt [3:0] and
 // [15:14], expcnt [6:4] left at its maximum, lgkmcnt [11:8]).
 template <int n>
@@ -234,19 +244,17 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
     if (ka + C_::RA <= Ka && kb + C_::RB <= Kb) {  // whole stage inside K: straight line
 #pragma unroll
       for (int x = 0; x < C_::A_BPW; ++x)
-        __builtin_amdgcn_global_load_lds((glb_void*)(pa[x] + (int64_t)st * C_::RA),
-                                         (lds_void*)(sa + (wid * C_::A_BPW + x) * 1024), 16, 0, 0);
+        dma16(pa[x] + (int64_t)st * C_::RA, sa + (wid * C_::A_BPW + x) * 1024);
 #pragma unroll
       for (int x = 0; x < C_::B_BPW; ++x)
-        __builtin_amdgcn_global_load_lds((glb_void*)(pb[x] + (int64_t)st * C_::RB),
-                                         (lds_void*)(sb + (wid * C_::B_BPW + x) * 1024), 16, 0, 0);
+        dma16(pb[x] + (int64_t)st * C_::RB, sb + (wid * C_::B_BPW + x) * 1024);
       return;
     }
 #pragma unroll
     for (int x = 0; x < C_::A_BPW; ++x) {
       uint8_t* dst = sa + (wid * C_::A_BPW + x) * 1024;
       if (ka + ca[x] < Ka)
-        __builtin_amdgcn_global_load_lds((glb_void*)(pa[x] + (int64_t)st * C_::RA), (lds_void*)dst, 16, 0, 0);
+        dma16(pa[x] + (int64_t)st * C_::RA, dst);
       else
         *reinterpret_cast<uint4*>(dst + lane * 16) = make_uint4(0u, 0u, 0u, 0u);
     }
@@ -254,7 +262,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
     for (int x = 0; x < C_::B_BPW; ++x) {
       uint8_t* dst = sb + (wid * C_::B_BPW + x) * 1024;
       if (kb + cb[x] < Kb)
-        __builtin_amdgcn_global_load_lds((glb_void*)(pb[x] + (int64_t)st * C_::RB), (lds_void*)dst, 16, 0, 0);
+        dma16(pb[x] + (int64_t)st * C_::RB, dst);
       else
         *reinterpret_cast<uint4*>(dst + lane * 16) = make_uint4(0u, 0u, 0u, 0u);
     }
@@ -447,8 +455,8 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
       const int64_t gn = n0 + (int64_t)pc * (16 / ES);
       if (gm < M && gn < g.N) {
         const int64_t orow = (EPI == kEpiDx) ? (int64_t)g.out_rows[gm] : gm;
-        *reinterpret_cast<uint4*>(out + (out_plane + orow * g.ldo + gn) * ES) =
-            *reinterpret_cast<const uint4*>(smem + r * E_PITCH + pc * 16);
+        st_stream<(EPI == kEpiPartial) ? (bool)HQ_NT_P_ST : (bool)HQ_NT_G_ST>(out + (out_plane + orow * g.ldo + gn) * ES,
+                  *reinterpret_cast<const uint4*>(smem + r * E_PITCH + pc * 16));
       }
     }
     __syncthreads();
@@ -481,8 +489,10 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
     int v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (live) {
       for (int z = 0; z < S; ++z) {
-        const int4* p = reinterpret_cast<const int4*>(P + z * plane + m * g.ldo + n);
-        const int4 x0 = p[0], x1 = p[1];
+        const int32_t* p = P + z * plane + m * g.ldo + n;
+        const uint4 u0 = ld_stream<HQ_NT_R_LD>(p), u1 = ld_stream<HQ_NT_R_LD>(p + 4);
+        const int4 x0 = make_int4((int)u0.x, (int)u0.y, (int)u0.z, (int)u0.w);
+        const int4 x1 = make_int4((int)u1.x, (int)u1.y, (int)u1.z, (int)u1.w);
         v[0] += x0.x; v[1] += x0.y; v[2] += x0.z; v[3] += x0.w;
         v[4] += x1.x; v[5] += x1.y; v[6] += x1.z; v[7] += x1.w;
       }
@@ -512,15 +522,15 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
     }
     if (!live) continue;
     if constexpr (MODE == kEpiAcc) {
-      int4* p = reinterpret_cast<int4*>(static_cast<int32_t*>(g.out) + m * g.ldo + n);
-      p[0] = make_int4(v[0], v[1], v[2], v[3]);
-      p[1] = make_int4(v[4], v[5], v[6], v[7]);
+      int32_t* p = static_cast<int32_t*>(g.out) + m * g.ldo + n;
+      st_stream<HQ_NT_G_ST>(p, make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]));
+      st_stream<HQ_NT_G_ST>(p + 4, make_uint4((uint32_t)v[4], (uint32_t)v[5], (uint32_t)v[6], (uint32_t)v[7]));
     } else {
       const int64_t orow = (MODE == kEpiDx) ? (int64_t)g.out_rows[m] : m;
       float f[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) f[e] = alpha * (float)v[e];
-      store_vec<DT, 8>(static_cast<char*>(g.out) + (orow * g.ldo + n) * Elem<DT>::bytes, f);
+      store8_stream<DT, HQ_NT_G_ST>(static_cast<char*>(g.out) + (orow * g.ldo + n) * Elem<DT>::bytes, f);
     }
   }
 }

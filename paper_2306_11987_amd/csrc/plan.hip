@@ -210,7 +210,7 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
       if (w_up[t] + w_dn[t]) continue;
       char* row = static_cast<char*>(dX) + t * bytes;
       for (int64_t o = (tid & 63) * 16; o < bytes; o += 64 * 16)
-        *reinterpret_cast<uint4*>(row + o) = make_uint4(0u, 0u, 0u, 0u);
+        st_stream<HQ_NT_B_ST>(row + o, make_uint4(0u, 0u, 0u, 0u));
     }
     return;
   }
@@ -232,12 +232,12 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
       const int64_t t = kept[i];
       if (isA) {
         const int wu = w_up[t], wd = w_dn[t];
-        const uint2 up = *reinterpret_cast<const uint2*>(qup + t * (C / 2) + (col0 + q) / 2);
-        const uint2 dn = *reinterpret_cast<const uint2*>(qdn + t * (C / 2) + (col0 + q) / 2);
+        const uint2 up = ld_stream2<HQ_NT_B_LD>(qup + t * (C / 2) + (col0 + q) / 2);
+        const uint2 dn = ld_stream2<HQ_NT_B_LD>(qdn + t * (C / 2) + (col0 + q) / 2);
         weighted8(up.x, dn.x, wu, wd, v);
         weighted8(up.y, dn.y, wu, wd, v + 8);
       } else {
-        const uint2 x = *reinterpret_cast<const uint2*>(xq + t * (D / 2) + (col0 + q) / 2);
+        const uint2 x = ld_stream2<HQ_NT_B_LD>(xq + t * (D / 2) + (col0 + q) / 2);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           v[j] = sext4((x.x >> (4 * j)) & 15u);
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
     }
     if (isA && Ag) {
       const uint2 lo = interleave8(v), hi = interleave8(v + 8);
-      *reinterpret_cast<uint4*>(Ag + i * C + col0 + q) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
     }
     if (isA && !At) return;  // uniform: no transpose wanted
 #pragma unroll
@@ -261,7 +261,7 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
 #pragma unroll
       for (int j = 0; j < 16; ++j) a[j] = tile[q + j][c];
       const uint2 lo = interleave8(a), hi = interleave8(a + 8);
-      *reinterpret_cast<uint4*>(At + (col0 + c) * pitch + i0 + q) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      st_stream<HQ_NT_B_ST>(At + (col0 + c) * pitch + i0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
     } else {
       uint32_t w0 = 0, w1 = 0;
 #pragma unroll
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
         if (j < 4) w0 |= byte << (8 * j);
         else w1 |= byte << (8 * (j - 4));
       }
-      *reinterpret_cast<uint2*>(XtT + (col0 + c) * (pitch / 2) + (i0 + q) / 2) = make_uint2(w0, w1);
+      st_stream2<HQ_NT_B_ST>(XtT + (col0 + c) * (pitch / 2) + (i0 + q) / 2, make_uint2(w0, w1));
     }
   }
 }

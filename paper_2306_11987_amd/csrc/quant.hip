@@ -40,10 +40,10 @@ constexpr int kQWaves = kQThreads / kWave;
 constexpr int kVE = 16;  // elements per lane per step
 constexpr float kRne = 12582912.0f;  // 1.5 * 2^23
 
-template <int DT>
+template <int DT, bool NT>
 __device__ __forceinline__ void load16(const char* p, float v[16]) {
-  load8<DT>(p, v);
-  load8<DT>(p + 8 * Elem<DT>::bytes, v + 8);
+  load8<DT, NT>(p, v);
+  load8<DT, NT>(p + 8 * Elem<DT>::bytes, v + 8);
 }
 
 // Value of lane (lane ^ M), M in {1, 2, 4}, added to x: DPP quad permutations (folded into
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_absmax_kernel(QJob j0, QJob j1
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (s0 + u < g.steps) {
-        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        load16<DT, HQ_NT_ABS_LD>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
         if (++it == g.iters) { it = 0; ++k; }
       }
     }
@@ -234,7 +234,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (s0 + u < g.steps) {
-        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        load16<DT, HQ_NT_Q_LD>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
         if (++it == g.iters) { it = 0; ++k; }
       }
     }
@@ -249,7 +249,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
         ss = sumsq8(w1, sumsq8(w0, ss));
         const bool ok = g.valid(kp);
         const int64_t r = g.row_of(kp);
-        if (ok) reinterpret_cast<uint2*>(o.packed + r * (j.cols / 2))[(int64_t)ip * g.G + g.sub] = make_uint2(w0, w1);
+        if (ok) st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(o.packed + r * (j.cols / 2)) + (int64_t)ip * g.G + g.sub, make_uint2(w0, w1));
         if (++ip == g.iters) {  // end of the group's row
           if (o.row_sumsq) {
             ss = group_sum(ss, g.G);
@@ -326,7 +326,7 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (s0 + u < g.steps) {
-        load16<DT>(base + (g.row_of(k) * C + (int64_t)it * g.G * kVE) * EB, v[u]);
+        load16<DT, HQ_NT_BS_LD>(base + (g.row_of(k) * C + (int64_t)it * g.G * kVE) * EB, v[u]);
         if (++it == g.iters) { it = 0; ++k; }
       }
     }
@@ -359,8 +359,8 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
         sd = sumsq8(d1, sumsq8(d0, sd));
         if (ok) {
           const int64_t o8 = r * (C / 16) + (int64_t)ip * g.G + g.sub;  // uint2 index
-          reinterpret_cast<uint2*>(o.qup)[o8] = make_uint2(u0, u1);
-          reinterpret_cast<uint2*>(o.qdn)[o8] = make_uint2(d0, d1);
+          st_stream2<HQ_NT_BS_ST>(reinterpret_cast<uint2*>(o.qup) + o8, make_uint2(u0, u1));
+          st_stream2<HQ_NT_BS_ST>(reinterpret_cast<uint2*>(o.qdn) + o8, make_uint2(d0, d1));
         }
         if (++ip == g.iters) {  // end of the group's row
           su = group_sum(su, g.G);
@@ -472,7 +472,7 @@ __global__ __launch_bounds__(kQThreads) void hsize_max_kernel(QJob j0, QJob j1,
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (s0 + u < g.steps) {
-        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        load16<DT, HQ_NT_ABS_LD>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
         if (++it == g.iters) { it = 0; ++k; }
       }
     }
@@ -546,7 +546,7 @@ __global__ __launch_bounds__(kQThreads) void hsize_err_kernel(QJob j0, QJob j1,
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (s0 + u < g.steps) {
-        load16<DT>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        load16<DT, HQ_NT_ABS_LD>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
         if (++it == g.iters) { it = 0; ++k; }
       }
     }
