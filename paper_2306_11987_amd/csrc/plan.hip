@@ -34,15 +34,37 @@ namespace {
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / kWave;
 
-__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
-  v = wave_sum_u64(v);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+constexpr int kPlanRegs = 32;  // scores per thread kept in registers (2N <= 32768)
+
+// two block-wide sums with one pair of barriers (red holds 2 kPlanWaves words)
+__device__ __forceinline__ void block_sum2_u64(uint64_t& a, uint64_t& b, uint64_t* red) {
+  a = wave_sum_u64(a);
+  b = wave_sum_u64(b);
+  if ((threadIdx.x & 63) == 0) {
+    red[threadIdx.x >> 6] = a;
+    red[kPlanWaves + (threadIdx.x >> 6)] = b;
+  }
   __syncthreads();
-  uint64_t t = 0;
+  a = 0;
+  b = 0;
 #pragma unroll
-  for (int i = 0; i < kPlanWaves; ++i) t += red[i];
+  for (int i = 0; i < kPlanWaves; ++i) {
+    a += red[i];
+    b += red[kPlanWaves + i];
+  }
   __syncthreads();
-  return t;
+}
+
+// 8 consecutive words from p + t0 (n8 of them valid, the rest 0).
+__device__ __forceinline__ void load8u(const uint32_t* p, int t0, int n8, uint32_t v[8]) {
+  if (n8 == 8) {
+    const uint4 a = *reinterpret_cast<const uint4*>(p + t0), b = *reinterpret_cast<const uint4*>(p + t0 + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = j < n8 ? p[t0 + j] : 0u;
+  }
 }
 
 __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
@@ -50,7 +72,7 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     const uint4* __restrict__ parts, int nparts, int N, int64_t B, uint64_t seed,
     uint64_t offset, uint8_t* __restrict__ w_up, uint8_t* __restrict__ w_dn,
     int32_t* __restrict__ kept, int32_t* __restrict__ n_kept) {
-  __shared__ uint64_t red[kPlanWaves];
+  __shared__ uint64_t red[2 * kPlanWaves];
   __shared__ int wtot[kPlanWaves];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
 
@@ -61,53 +83,51 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     nz += p.x;
     st += ((uint64_t)p.z << 32) | p.y;
   }
-  nz = block_sum_u64(nz, red);
-  const uint64_t S_all = block_sum_u64(st, red);
+  block_sum2_u64(nz, st, red);
+  const uint64_t S_all = st;
   const bool all_nonzero_kept = (int64_t)nz <= B;
 
-  // App. A.2 clamp-and-rescale (uniform across the block)
+  // App. A.2 clamp-and-rescale (uniform across the block); each round is one pass over
+  // the scores, held in registers when they fit
   uint64_t S = S_all;
   int64_t R = B;
   if (!all_nonzero_kept) {
+    const int64_t n2 = 2 * (int64_t)N;
+    const bool in_regs = n2 <= (int64_t)kPlanRegs * kPlanThreads;
+    uint32_t cs[kPlanRegs];
+#pragma unroll
+    for (int j = 0; j < kPlanRegs; ++j) {
+      const int64_t i = tid + (int64_t)j * kPlanThreads;
+      cs[j] = (in_regs && i < n2) ? scores[i < N ? i : pitch + (i - N)] : 0u;
+    }
     int64_t k = 0;
     for (;;) {
       R = B - k;
       uint64_t cnt = 0, sum = 0;
-      for (int64_t i = tid; i < 2 * (int64_t)N; i += kPlanThreads) {
-        const uint32_t c = scores[i < N ? i : pitch + (i - N)];
-        if (c && (uint64_t)R * c >= S) { ++cnt; sum += c; }
+      if (in_regs) {
+#pragma unroll
+        for (int j = 0; j < kPlanRegs; ++j) {
+          const uint32_t c = cs[j];
+          if (c && (uint64_t)R * c >= S) { ++cnt; sum += c; }
+        }
+      } else {
+        for (int64_t i = tid; i < n2; i += kPlanThreads) {
+          const uint32_t c = scores[i < N ? i : pitch + (i - N)];
+          if (c && (uint64_t)R * c >= S) { ++cnt; sum += c; }
+        }
       }
-      cnt = block_sum_u64(cnt, red);
-      sum = block_sum_u64(sum, red);
+      block_sum2_u64(cnt, sum, red);
       if ((int64_t)cnt == k) break;  // nothing newly clamped
       k = (int64_t)cnt;
       S = S_all - sum;
     }
   }
 
-  // weights, masks and compaction, 8 consecutive tokens per thread per round
+  // weights, masks and compaction of one round: 8 consecutive tokens per thread
   int base = 0;
   const uint32_t* cdn = scores + pitch;
-  for (int r0 = 0; r0 < N; r0 += 8 * kPlanThreads) {
-    const int t0 = r0 + 8 * tid;
-    const int n8 = t0 < N ? (N - t0 < 8 ? N - t0 : 8) : 0;
-    uint32_t su[8], cd[8];
-    if (n8 == 8) {
-      const uint4 a0 = *reinterpret_cast<const uint4*>(sumsq_up + t0);
-      const uint4 a1 = *reinterpret_cast<const uint4*>(sumsq_up + t0 + 4);
-      const uint4 b0 = *reinterpret_cast<const uint4*>(cdn + t0);
-      const uint4 b1 = *reinterpret_cast<const uint4*>(cdn + t0 + 4);
-      su[0] = a0.x; su[1] = a0.y; su[2] = a0.z; su[3] = a0.w;
-      su[4] = a1.x; su[5] = a1.y; su[6] = a1.z; su[7] = a1.w;
-      cd[0] = b0.x; cd[1] = b0.y; cd[2] = b0.z; cd[3] = b0.w;
-      cd[4] = b1.x; cd[5] = b1.y; cd[6] = b1.z; cd[7] = b1.w;
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        su[j] = j < n8 ? (uint32_t)sumsq_up[t0 + j] : 0u;
-        cd[j] = j < n8 ? cdn[t0 + j] : 0u;
-      }
-    }
+  const uint32_t* sup = reinterpret_cast<const uint32_t*>(sumsq_up);
+  auto round = [&](int t0, int n8, const uint32_t su[8], const uint32_t cd[8]) {
     const U4 rnd = philox_block(seed, offset, 1u, (uint64_t)(t0 > 0 ? t0 : 0));
     uint32_t wu8[2] = {0u, 0u}, wd8[2] = {0u, 0u};
     uint32_t keepmask = 0;
@@ -162,6 +182,29 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     for (int j = 0; j < 8; ++j)
       if ((keepmask >> j) & 1) kept[pos++] = t0 + j;
     base += total;
+  };
+  if (N <= 2 * 8 * kPlanThreads) {
+    // both rounds' inputs in one round trip to memory
+    uint32_t su[2][8], cd[2][8];
+    int t0[2], n8[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      t0[r] = r * 8 * kPlanThreads + 8 * tid;
+      n8[r] = t0[r] < N ? (N - t0[r] < 8 ? N - t0[r] : 8) : 0;
+      load8u(sup, t0[r], n8[r], su[r]);
+      load8u(cdn, t0[r], n8[r], cd[r]);
+    }
+    round(t0[0], n8[0], su[0], cd[0]);
+    if (N > 8 * kPlanThreads) round(t0[1], n8[1], su[1], cd[1]);
+  } else {
+    for (int r0 = 0; r0 < N; r0 += 8 * kPlanThreads) {
+      const int t = r0 + 8 * tid;
+      const int n = t < N ? (N - t < 8 ? N - t : 8) : 0;
+      uint32_t su[8], cd[8];
+      load8u(sup, t, n, su);
+      load8u(cdn, t, n, cd);
+      round(t, n, su, cd);
+    }
   }
   if (tid == 0) *n_kept = base;
 }
