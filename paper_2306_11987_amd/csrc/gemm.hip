@@ -449,15 +449,28 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
       }
     }
     __syncthreads();
-    for (int idx = tid; idx < E_ROWS * PIECES; idx += C_::THREADS) {
+    // every LDS read (and, for dX, every destination-row lookup) of the chunk is issued
+    // before the first store, so their latencies overlap instead of adding up
+    constexpr int ITER = E_ROWS * PIECES / C_::THREADS;
+    static_assert(ITER * C_::THREADS == E_ROWS * PIECES, "whole store rounds");
+    uint4 val[ITER];
+    int orow[ITER];  // destination row (rows < 2^30), -1 past the end
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int idx = tid + it * C_::THREADS;
       const int r = idx / PIECES, pc = idx % PIECES;
       const int64_t gm = m0 + r_lo + r;
+      val[it] = *reinterpret_cast<const uint4*>(smem + r * E_PITCH + pc * 16);
+      orow[it] = gm < M ? ((EPI == kEpiDx) ? g.out_rows[gm] : (int)gm) : -1;
+    }
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int idx = tid + it * C_::THREADS;
+      const int pc = idx % PIECES;
       const int64_t gn = n0 + (int64_t)pc * (16 / ES);
-      if (gm < M && gn < g.N) {
-        const int64_t orow = (EPI == kEpiDx) ? (int64_t)g.out_rows[gm] : gm;
-        st_stream<(EPI == kEpiPartial) ? (bool)HQ_NT_P_ST : (bool)HQ_NT_G_ST>(out + (out_plane + orow * g.ldo + gn) * ES,
-                  *reinterpret_cast<const uint4*>(smem + r * E_PITCH + pc * 16));
-      }
+      if (orow[it] >= 0 && gn < g.N)
+        st_stream<(EPI == kEpiPartial) ? (bool)HQ_NT_P_ST : (bool)HQ_NT_G_ST>(
+            out + (out_plane + (int64_t)orow[it] * g.ldo + gn) * ES, val[it]);
     }
     __syncthreads();
   }
@@ -536,8 +549,9 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
 }
 
 // wave tile width: int8 x INT4 GEMMs widen only the n-side operand, so their waves take
-// 128 m x 64 n (half the widening per MFMA) unless the Hadamard block needs 128 columns
-template <bool A4, int LOG2B> constexpr int wave_n() { return (A4 || LOG2B == 7) ? 128 : 64; }
+// 128 m x 64 n (half the widening per MFMA) unless the Hadamard block spans 64 or 128
+// columns (the in-register transform then needs no lane exchange)
+template <bool A4, int LOG2B> constexpr int wave_n() { return (A4 || LOG2B >= 6) ? 128 : 64; }
 
 template <int BM, bool A4, int EPI, int DT, int LOG2B>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
