@@ -58,7 +58,8 @@ __all__ = [
     "leverage_scores", "clamp_rescale", "LSSPlan", "lss_plan", "LSSBackward",
     "lss_backward", "weighted_rows", "stochastic_round", "MAX_LOG2_BLOCK", "KEEP_NONZERO",
     "resolve_budget", "hadamard_reconstruction", "hadamard_mse", "HadamardChoice",
-    "choose_hadamard_size",
+    "choose_hadamard_size", "quantize_lsq", "LSQForward", "lsq_forward", "LSQBackward",
+    "lsq_backward", "lsq_grad_scale",
 ]
 
 
@@ -424,6 +425,18 @@ def weighted_rows(bs: BitSplit, plan: LSSPlan) -> np.ndarray:
             + plan.w_dn[:, None] * bs.q_dn.astype(np.int64))
 
 
+def _sample(G: np.ndarray, x_sumsq: np.ndarray, budget: int, seed: int, offset: int):
+    """Steps 1-4 of LSS-MM shared by both gradients (App. A.6): bit split, leverage
+    scores on the codes, the sample, and the weighted integer rows A."""
+    bs = bit_split(G, seed, offset)
+    su = np.sum(bs.q_up.astype(np.int64) ** 2, axis=1)
+    sd = np.sum(bs.q_dn.astype(np.int64) ** 2, axis=1)
+    plan = lss_plan(su, sd, x_sumsq, budget, seed, offset)
+    A = weighted_rows(bs, plan)
+    assert np.abs(A).max(initial=0) <= 126
+    return bs, plan, A
+
+
 def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: int,
                  need_dx: bool = True, need_dw: bool = True) -> LSSBackward:
     """Activation and weight gradients of HQ-MM by LSS-MM.
@@ -432,12 +445,7 @@ def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: 
     clip masks are identically 1 under absmax scales), with grad_Y replaced by
     the sampled bit-split estimate s_dn * A (Sec. 4.2, App. A.3)."""
     k = fwd.log2_block
-    bs = bit_split(G, seed, offset)
-    su = np.sum(bs.q_up.astype(np.int64) ** 2, axis=1)
-    sd = np.sum(bs.q_dn.astype(np.int64) ** 2, axis=1)
-    plan = lss_plan(su, sd, fwd.x_sumsq, budget, seed, offset)
-    A = weighted_rows(bs, plan)
-    assert np.abs(A).max(initial=0) <= 126
+    bs, plan, A = _sample(G, fwd.x_sumsq, budget, seed, offset)
     N, C = A.shape
     D = fwd.xq.shape[1]
     s_dn = float(bs.s_up) / BS_RATIO
@@ -453,3 +461,125 @@ def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: 
         acc_dw = _int_matmul(At.T, fwd.xq[plan.kept].astype(np.int64))
         dW = a_dw * fwht_rows(acc_dw, k).astype(np.float64)
     return LSSBackward(bs, plan, A, acc_dx, acc_dw, dX, dW, a_dx, a_dw)
+
+
+# --------------------------------------------------------------------------
+# Learned step size mode (Sec. 3.1 Eq. 2, Sec. 4, App. A.4)
+# --------------------------------------------------------------------------
+# Readings (listed with their reasons in the design notes):
+# * the caller's step sizes s_x, s_w belong to the unnormalised transform v = V H_u
+#   (the paper's s for the orthonormal H times 2^{k/2}), so Y = s_x s_w x^ w^^T / 2^k
+#   exactly as in the dynamic mode;
+# * v / s is taken as r = fl(v * fl(1/s)) in float32, codes clamp(rint(r), -7, 7);
+# * the clip mask of Sec. 4 is taken on r: I = [-7 <= r <= 7] (Hadamard domain);
+# * delta(s) = int_s(v) - I o (v / s) of App. A.4 is formed as q - I r (exact in float32)
+#   and kept as float16, the "FP16 version" the paper's implementation keeps for the LSQ
+#   backward (App. A.6); |delta| <= 1/2 inside the range and |delta| = 7 where clipped,
+#   so the backward reads the mask back as I = [|delta| <= 1/2];
+# * the STE gradients mask the integer accumulators in the Hadamard domain, then apply
+#   H^T (mask first: chain rule), and the step-size gradients are
+#   grad s = g(s) (s_other s_dn / 2^k) sum(acc o delta), g(s) = 1 / sqrt(Q_P numel),
+#   the chain rule through s q (App. A.4), with grad_Y replaced by the LSS estimate.
+
+
+def quantize_lsq(v: np.ndarray, s: float):
+    """int_s(v) = round(clamp(v / s, -7, 7)) with a given step s > 0 (Eq. 2).
+
+    Returns (codes int8, mask bool, delta float16): the clip mask I of Sec. 4 and
+    delta = q - I o (v / s) of App. A.4 (see the readings above)."""
+    v = np.asarray(v, dtype=np.float32)
+    s = np.float32(s)
+    assert s > 0 and np.isfinite(s)
+    inv = np.float32(1.0) / s
+    r = (v * inv).astype(np.float32)
+    inside = (r >= -QMAX) & (r <= QMAX)
+    q = np.clip(np.rint(r), -QMAX, QMAX).astype(np.int8)
+    delta = q.astype(np.float32) - np.where(inside, r, np.float32(0.0))
+    return q, inside, delta.astype(np.float16)
+
+
+def lsq_grad_scale(numel: int) -> float:
+    """g(s) = 1 / sqrt(Q_P numel), the step-size gradient scale of App. A.4."""
+    return 1.0 / math.sqrt(QMAX * int(numel))
+
+
+@dataclass
+class LSQForward:
+    log2_block: int
+    s_x: np.float32
+    s_w: np.float32
+    xq: np.ndarray  # int8 [N][D]
+    wq: np.ndarray  # int8 [C][D]
+    x_sumsq: np.ndarray  # int64 [N]
+    dx16: np.ndarray  # float16 [N][D]  delta of X (clip mask |delta| <= 1/2)
+    dw16: np.ndarray  # float16 [C][D]
+    acc: np.ndarray = field(default=None)
+    Y: np.ndarray = field(default=None)
+
+
+def lsq_forward(X: np.ndarray, W: np.ndarray, log2_block: int, s_x: float, s_w: float,
+                compute_output: bool = True) -> LSQForward:
+    """HQ-MM with learned step sizes: (1) X H and W H; (2) LSQ to INT4 (Eq. 2, Sec. 3.3
+    step 2); (3) integer product; (4) dequantise by s_X s_W (and 2^-k)."""
+    k = int(log2_block)
+    s_x, s_w = np.float32(s_x), np.float32(s_w)
+    vx = fwht_rows(np.asarray(X, dtype=np.float32), k)
+    vw = fwht_rows(np.asarray(W, dtype=np.float32), k)
+    xq, _, dx16 = quantize_lsq(vx, s_x)
+    wq, _, dw16 = quantize_lsq(vw, s_w)
+    out = LSQForward(k, s_x, s_w, xq, wq, np.sum(xq.astype(np.int64) ** 2, axis=1), dx16, dw16)
+    if compute_output:
+        out.acc = _int_matmul(xq, wq.T)
+        out.Y = float(s_x) * float(s_w) * 2.0 ** (-k) * out.acc.astype(np.float64)
+    return out
+
+
+@dataclass
+class LSQBackward:
+    bs: BitSplit
+    plan: LSSPlan
+    A: np.ndarray
+    acc_dx: np.ndarray  # int64 [T][D] unmasked
+    acc_dw: np.ndarray  # int64 [C][D] unmasked
+    dX: np.ndarray
+    dW: np.ndarray
+    ds_x: float
+    ds_w: float
+    alpha_dx: float
+    alpha_dw: float
+
+
+def lsq_backward(G: np.ndarray, fwd: LSQForward, budget: int, seed: int, offset: int,
+                 need_dx: bool = True, need_dw: bool = True,
+                 delta_x: np.ndarray = None, delta_w: np.ndarray = None) -> LSQBackward:
+    """Gradients of HQ-MM with learned step sizes by LSS-MM (Sec. 4, App. A.4).
+
+    grad_X = s_W (I_X o grad_Y W^) H^T, grad_W = s_X (grad_Y^T X^ o I_W) H^T, and the
+    step-size gradients g(s) s_other sum(grad_Y W^ o delta_X) (resp. grad_Y^T X^ o
+    delta_W), with grad_Y the sampled bit-split estimate s_dn A.  delta_x / delta_w
+    replace the stored float16 deltas (tests pass exact ones)."""
+    k = fwd.log2_block
+    bs, plan, A = _sample(G, fwd.x_sumsq, budget, seed, offset)
+    N, C = A.shape
+    D = fwd.xq.shape[1]
+    s_dn = float(bs.s_up) / BS_RATIO
+    a_dx = s_dn * float(fwd.s_w) * 2.0 ** (-k)
+    a_dw = s_dn * float(fwd.s_x) * 2.0 ** (-k)
+    dlx = np.asarray(fwd.dx16 if delta_x is None else delta_x, dtype=np.float64)
+    dlw = np.asarray(fwd.dw16 if delta_w is None else delta_w, dtype=np.float64)
+    At = A[plan.kept]
+    acc_dx = acc_dw = dX = dW = None
+    ds_x = ds_w = 0.0
+    if need_dx:
+        acc_dx = _int_matmul(At, fwd.wq.astype(np.int64))
+        d = dlx[plan.kept]
+        masked = np.where(np.abs(d) <= 0.5, acc_dx, 0)
+        dX = np.zeros((N, D), dtype=np.float64)
+        dX[plan.kept] = a_dx * fwht_rows(masked, k).astype(np.float64)
+        ds_x = lsq_grad_scale(N * D) * a_dx * float(np.sum(acc_dx.astype(np.float64) * d))
+    if need_dw:
+        acc_dw = _int_matmul(At.T, fwd.xq[plan.kept].astype(np.int64))
+        masked = np.where(np.abs(dlw) <= 0.5, acc_dw, 0)
+        dW = a_dw * fwht_rows(masked, k).astype(np.float64)
+        ds_w = lsq_grad_scale(C * D) * a_dw * float(np.sum(acc_dw.astype(np.float64) * dlw))
+    return LSQBackward(bs, plan, A, acc_dx, acc_dw, dX, dW, ds_x, ds_w, a_dx, a_dw)
