@@ -72,9 +72,10 @@ typedef enum {
   HQLSS_ERR_ARG = 9        /* any other invalid argument (e.g. budget, which)           */
 } hqlss_status;
 
-/* State written by the forward pass and read by the backward pass: the codes X^ and
- * W^ "already calculated in forward" (Sec. 4).  Caller-allocated device memory; it must
- * stay alive and unmodified from hq_linear_fwd until the backward calls have run. */
+/* State written by the forward pass and read by the backward pass: the codes X^ and W^,
+ * which the backward reuses from the forward rather than recomputing (Sec. 4).
+ * Caller-allocated device memory; it must stay alive and unmodified from hq_linear_fwd
+ * until the backward calls have run. */
 typedef struct {
   uint8_t *xq;      /* [N][D/2]  INT4 codes of X H_u                                  */
   uint8_t *wq;      /* [C][D/2]  INT4 codes of W H_u                                  */
@@ -97,12 +98,28 @@ typedef struct {
   float *amax_g;     /* [1]       a_g = max|dY|  (s_up = a_g / 7, s_dn = s_up / 14)      */
 } lss_plan_t;
 
+/* Learned-step-size (LSQ) mode (Sec. 3.1, Eq. 2; App. A.4): static step sizes given by the
+ * caller instead of the per-tensor maxima.  step holds s_X, s_W as device fp32 scalars, the
+ * steps of the transformed tensors X H_u and W H_u (unnormalised Hadamard domain, so a code
+ * q stands for s q there); each must be finite and at least 2^-126, else the codes are
+ * unspecified.  delta_x [N][D] and delta_w [C][D] are fp16 (IEEE binary16 bit patterns)
+ * written by hq_linear_fwd_lsq and read by lss_linear_bwd_lsq: delta = q - I r with
+ * r = fl(v fl(1/s)) and I = [-7 <= r <= 7], the factor of the step-size gradient; the
+ * clip indicator I is recovered from it as |delta| <= 1/2.  Caller-allocated, 16-byte
+ * aligned device memory. */
+typedef struct {
+  const float *step;   /* [2]      s_X, s_W                                                */
+  uint16_t *delta_x;   /* [N][D]   fp16 delta_X                                            */
+  uint16_t *delta_w;   /* [C][D]   fp16 delta_W                                            */
+} hqlss_lsq_t;
+
 /* budget_rows value selecting the keep-every-non-zero-row sample (see lss_grad_plan). */
 #define HQLSS_BUDGET_KEEP_NONZERO (-1)
 
 /* Workspace sizes (bytes) for the entry points below, which = HQLSS_WS_*. */
 enum { HQLSS_WS_FWD = 0, HQLSS_WS_BWD_DX = 1, HQLSS_WS_BWD_DW = 2, HQLSS_WS_BWD = 3,
-       HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5, HQLSS_WS_HSIZE = 6 };
+       HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5, HQLSS_WS_HSIZE = 6, HQLSS_WS_FWD_LSQ = 7,
+       HQLSS_WS_BWD_LSQ = 8 };
 size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C);
 
 /* HQ-MM forward (Sec. 3.3, Eq. 3; Procedure HQ-MM).
@@ -116,6 +133,21 @@ hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int
                            int64_t C, hqlss_dtype dt, int log2_block,
                            const hqlss_saved_t *saved, void *ws, size_t ws_bytes,
                            void *stream);
+
+/* HQ-MM forward with learned step sizes (Sec. 3.3 Procedure HQ-MM with step 2 done by LSQ,
+ * Eq. 2; App. A.4).
+ *   1. v_x = X H_u, v_w = W H_u in fp32, as hq_linear_fwd;
+ *   2. r = fl(v fl(1/s)), codes clamp(rint(r), -7, 7) -> saved; delta -> lsq (one pass,
+ *      no maximum);
+ *   3. acc = X^ W^^T (int32, exact);
+ *   4. Y = fl(alpha * acc), alpha = fl(fl(s_X s_W) / 2^k), cast to dt.
+ * saved: xq, wq, wqT, x_sumsq are written (amax is neither read nor written and may be
+ * NULL); lsq: step read, delta_x and delta_w written.  ws: at least
+ * hqlss_workspace_bytes(HQLSS_WS_FWD_LSQ, ...) bytes (may be NULL when that is 0). */
+hqlss_status hq_linear_fwd_lsq(const void *X, const void *W, void *Y, int64_t N, int64_t D,
+                               int64_t C, hqlss_dtype dt, int log2_block,
+                               const hqlss_saved_t *saved, const hqlss_lsq_t *lsq, void *ws,
+                               size_t ws_bytes, void *stream);
 
 /* Bit splitting and leverage-score sampling of dY (Sec. 4.2, App. A.2; Procedure LSS-MM
  * steps 1-3, shared by both gradients as in App. A.6).
@@ -166,6 +198,28 @@ hqlss_status lss_linear_bwd_dw(const void *dY, const hqlss_saved_t *saved, void 
                                int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
                                int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
                                size_t ws_bytes, void *stream);
+
+/* LSS-MM backward of the learned-step-size forward (Sec. 4, App. A.4): the sample and
+ * bit split of lss_linear_bwd, then with the unmasked integer accumulators acc_dx = A_T W^
+ * and acc_dw = A_T^T X^_T
+ *   dX[t] = fl(alpha_dx * FWHT_b(I_X[t] o acc_dx[t])), dW = fl(alpha_dw * FWHT_b(I_W o acc_dw))
+ *   (alpha as in lss_linear_bwd_from_plan with s_X, s_W the steps; I from delta);
+ *   dstep[0] = g(s_X) a_dx sum(acc_dx o delta_X[kept]),  a_dx = (s_up / 14) s_W 2^-k,
+ *   dstep[1] = g(s_W) a_dw sum(acc_dw o delta_W),         a_dw = (s_up / 14) s_X 2^-k,
+ *   g(s_X) = 1 / sqrt(7 N D), g(s_W) = 1 / sqrt(7 C D); the products and the sums are
+ *   fp64 (per-workgroup partials added in a fixed order, so results are deterministic),
+ *   rounded to fp32 at the end.
+ * dX [N][D] or NULL, dW [C][D] or NULL (at least one); dstep: device fp32[2] or NULL (no
+ * step-size gradients); dstep[0] is written only with dX, dstep[1] only with dW.  saved:
+ * xq, wq, wqT, x_sumsq from hq_linear_fwd_lsq (amax unused); lsq: the same steps and the
+ * forward's deltas (delta_x needed with dX, delta_w with dW).  budget_rows, seed and
+ * offset as for lss_linear_bwd.  ws: at least hqlss_workspace_bytes(HQLSS_WS_BWD_LSQ, ...)
+ * bytes. */
+hqlss_status lss_linear_bwd_lsq(const void *dY, const hqlss_saved_t *saved,
+                                const hqlss_lsq_t *lsq, void *dX, void *dW, float *dstep,
+                                int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                                int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
+                                size_t ws_bytes, void *stream);
 
 /* Choice of the Hadamard block size (App. A.5).  For every candidate k (0 <= k <=
  * max_log2_block <= 7, D a multiple of 2^k) the reconstructions V_bar = s int_s(V H) H^T of

@@ -9,6 +9,7 @@ from ._binding import (  # noqa: F401
     BUDGET_KEEP_NONZERO,
     DTYPE_CODES,
     HQLSSError,
+    LSQ,
     Plan,
     Saved,
     debug_copy,
@@ -16,6 +17,7 @@ from ._binding import (  # noqa: F401
     debug_set_gemm_splits,
     hq_choose_hadamard_size,
     hq_linear_fwd,
+    hq_linear_fwd_lsq,
     kernel_name,
     lib,
     lss_grad_plan,
@@ -23,6 +25,7 @@ from ._binding import (  # noqa: F401
     lss_linear_bwd_dw,
     lss_linear_bwd_dx,
     lss_linear_bwd_from_plan,
+    lss_linear_bwd_lsq,
     lss_philox_offset_advance,
     status_string,
     timing_enable,
@@ -36,4 +39,6 @@ from ._binding import (  # noqa: F401
     WS_FROM_PLAN,
     WS_PLAN,
     WS_HSIZE,
+    WS_FWD_LSQ,
+    WS_BWD_LSQ,
 )

@@ -12,6 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhqlss.so")
 
 WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN, WS_HSIZE = 0, 1, 2, 3, 4, 5, 6
+WS_FWD_LSQ, WS_BWD_LSQ = 7, 8
 BUDGET_KEEP_NONZERO = -1  # HQLSS_BUDGET_KEEP_NONZERO: keep every non-zero gradient row
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
@@ -27,6 +28,10 @@ class _PlanC(ctypes.Structure):
                 ("w_dn", _vp), ("kept", _vp), ("n_kept", _vp), ("amax_g", _vp)]
 
 
+class _LsqC(ctypes.Structure):
+    _fields_ = [("step", _vp), ("delta_x", _vp), ("delta_w", _vp)]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
@@ -36,6 +41,10 @@ def _load() -> ctypes.CDLL:
         "hqlss_workspace_bytes": (_sz, [_int, _i64, _i64, _i64]),
         "hq_linear_fwd": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
                                _vp, _sz, _vp]),
+        "hq_linear_fwd_lsq": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
+                                   ctypes.POINTER(_LsqC), _vp, _sz, _vp]),
+        "lss_linear_bwd_lsq": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_LsqC), _vp, _vp, _vp,
+                                    _i64, _i64, _i64, _int, _int, _i64, _u64, _u64, _vp, _sz, _vp]),
         "lss_grad_plan": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_PlanC), _i64, _i64, _i64,
                                _int, _i64, _u64, _u64, _vp, _sz, _vp]),
         "lss_linear_bwd_from_plan": (st, [ctypes.POINTER(_PlanC), ctypes.POINTER(_SavedC), _vp, _vp,
@@ -150,6 +159,25 @@ class Plan:
         return _PlanC(*[_ptr(getattr(self, f)) for f, _ in _PlanC._fields_])
 
 
+@dataclass
+class LSQ:
+    """Learned-step-size state (hqlss_lsq_t): the steps and the forward's fp16 deltas."""
+
+    step: torch.Tensor  # float32 [2]: s_X, s_W
+    delta_x: torch.Tensor  # float16 [N, D]
+    delta_w: torch.Tensor  # float16 [C, D]
+
+    @staticmethod
+    def empty(step: torch.Tensor, N: int, D: int, C: int) -> "LSQ":
+        if step.dtype != torch.float32 or step.numel() != 2:
+            raise ValueError("step must be a float32 tensor of two elements (s_X, s_W)")
+        f16 = dict(dtype=torch.float16, device=step.device)
+        return LSQ(step, torch.empty(N, D, **f16), torch.empty(C, D, **f16))
+
+    def c(self) -> _LsqC:
+        return _LsqC(_ptr(self.step), _ptr(self.delta_x), _ptr(self.delta_w))
+
+
 def workspace_bytes(which: int, N: int, D: int, C: int) -> int:
     return int(lib.hqlss_workspace_bytes(int(which), int(N), int(D), int(C)))
 
@@ -176,6 +204,33 @@ def hq_linear_fwd(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Save
     sv = saved.c()
     _check(lib.hq_linear_fwd(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
                              ctypes.byref(sv), p, n, _stream(X)), "hq_linear_fwd")
+
+
+def hq_linear_fwd_lsq(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Saved, lsq: LSQ,
+                      log2_block: int, ws: Optional[torch.Tensor] = None) -> None:
+    N, D = X.shape
+    C = W.shape[0]
+    if ws is None:
+        ws = workspace(WS_FWD_LSQ, N, D, C, X.device)
+    p, n = _ws(ws)
+    sv, lq = saved.c(), lsq.c()
+    _check(lib.hq_linear_fwd_lsq(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
+                                 ctypes.byref(sv), ctypes.byref(lq), p, n, _stream(X)),
+           "hq_linear_fwd_lsq")
+
+
+def lss_linear_bwd_lsq(dY: torch.Tensor, saved: Saved, lsq: LSQ, dX: Optional[torch.Tensor],
+                       dW: Optional[torch.Tensor], dstep: Optional[torch.Tensor], D: int, log2_block: int,
+                       budget: int = 0, seed: int = 0, offset: int = 0,
+                       ws: Optional[torch.Tensor] = None) -> None:
+    N, C = dY.shape
+    if ws is None:
+        ws = workspace(WS_BWD_LSQ, N, D, C, dY.device)
+    p, n = _ws(ws)
+    sv, lq = saved.c(), lsq.c()
+    _check(lib.lss_linear_bwd_lsq(_ptr(dY), ctypes.byref(sv), ctypes.byref(lq), _ptr(dX), _ptr(dW),
+                                  _ptr(dstep), N, int(D), C, _dt(dY), int(log2_block), int(budget),
+                                  int(seed), int(offset), p, n, _stream(dY)), "lss_linear_bwd_lsq")
 
 
 def hq_choose_hadamard_size(X: torch.Tensor, W: torch.Tensor, max_log2_block: int = 7,

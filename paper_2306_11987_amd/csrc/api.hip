@@ -2,6 +2,7 @@
 // HQ-MM (forward) and LSS-MM (backward) on the caller's stream.  See include/hqlss.h.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <vector>
 
 #include "../../include/hqlss.h"
@@ -59,9 +60,19 @@ hqlss_status check_bwd_overflow(int64_t N, int64_t D, int64_t C, int log2_block)
   return HQLSS_OK;
 }
 
-hqlss_status check_saved(const hqlss_saved_t* s) {
-  if (!s || !s->xq || !s->wq || !s->wqT || !s->x_sumsq || !s->amax) return HQLSS_ERR_NULL;
-  if (!a16(s->xq) || !a16(s->wq) || !a16(s->wqT) || !a16(s->x_sumsq) || !a4(s->amax))
+// need_amax: the dynamic mode's maxima (the learned-step-size mode has its steps instead)
+hqlss_status check_saved(const hqlss_saved_t* s, bool need_amax = true) {
+  if (!s || !s->xq || !s->wq || !s->wqT || !s->x_sumsq) return HQLSS_ERR_NULL;
+  if (need_amax && !s->amax) return HQLSS_ERR_NULL;
+  if (!a16(s->xq) || !a16(s->wq) || !a16(s->wqT) || !a16(s->x_sumsq) ||
+      (need_amax && !a4(s->amax)))
+    return HQLSS_ERR_ALIGN;
+  return HQLSS_OK;
+}
+// want_dx / want_dw: which deltas the call reads (the forward writes both)
+hqlss_status check_lsq(const hqlss_lsq_t* l, bool want_dx, bool want_dw) {
+  if (!l || !l->step || (want_dx && !l->delta_x) || (want_dw && !l->delta_w)) return HQLSS_ERR_NULL;
+  if (!a4(l->step) || (want_dx && !a16(l->delta_x)) || (want_dw && !a16(l->delta_w)))
     return HQLSS_ERR_ALIGN;
   return HQLSS_OK;
 }
@@ -105,6 +116,16 @@ size_t dx_bytes(int64_t N, int64_t D, int64_t C) {
 }
 size_t dw_bytes(int64_t N, int64_t D, int64_t C) {
   return al(C * rup(N, kPad)) + al(D * rup(N, kPad) / 2) + dw_gemm_partial(N, D, C);
+}
+// learned-step-size mode: per-workgroup sums of acc * delta of the dX and dW epilogues
+int64_t lsq_parts_dx(int64_t N, int64_t D, int64_t C) {
+  return gemm_epi_parts(N, D, gemm_splits(N, D, C, false, true));
+}
+int64_t lsq_parts_dw(int64_t N, int64_t D, int64_t C) {
+  return gemm_epi_parts(C, D, gemm_splits(C, D, rup(N, kPad), false, true));
+}
+size_t lsq_parts_bytes(int64_t N, int64_t D, int64_t C, bool dx, bool dw) {
+  return (dx ? al(8 * lsq_parts_dx(N, D, C)) : 0) + (dw ? al(8 * lsq_parts_dw(N, D, C)) : 0);
 }
 
 struct Carve {
@@ -171,6 +192,29 @@ hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D,
   return HQLSS_OK;
 }
 
+hqlss_status do_fwd_lsq(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
+                        int dt, int k, const hqlss_saved_t* sv, const hqlss_lsq_t* l, void* ws,
+                        hipStream_t s) {
+  QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
+  const LsqOut ox{l->step, sv->xq, sv->x_sumsq, l->delta_x};
+  const LsqOut ow{l->step + 1, sv->wq, nullptr, l->delta_w};
+  HQ_TRY(launch_fwht_lsq(s, dt, k, jx, ox, jw, ow));
+  HQ_TRY(launch_transpose_packed(s, sv->wq, C, D, sv->wqT));
+  GemmArgs g{};
+  g.A = sv->xq; g.lda = D / 2;
+  g.B = sv->wq; g.ldb = D / 2;
+  g.M = N; g.N = C; g.K = D;
+  g.out = Y; g.ldo = C;
+  g.amax1 = reinterpret_cast<const uint32_t*>(l->step);
+  g.amax2 = reinterpret_cast<const uint32_t*>(l->step + 1);
+  g.steps_mask = 3;
+  g.denom = (float)(int64_t(1) << k);
+  g.log2b = k;
+  const int sp = gemm_splits(N, C, D, true, true);
+  HQ_TRY(launch_gemm(s, kEpiFwd, dt, true, true, g, sp, static_cast<int32_t*>(ws)));
+  return HQLSS_OK;
+}
+
 hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* p, int64_t N,
                      int64_t C, int dt, int64_t budget, uint64_t seed, uint64_t offset,
                      Carve& w, hipStream_t s) {
@@ -189,10 +233,15 @@ hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* 
   return HQLSS_OK;
 }
 
+// lsq (may be null): the learned-step-size mode: masked epilogues, and the step-size
+// gradients into dstep (if not null).
 hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, void* dW,
                       int32_t* acc, int which_acc, int64_t N, int64_t D, int64_t C, int dt,
-                      int k, Carve& w, hipStream_t s) {
-  const uint32_t* amax = reinterpret_cast<const uint32_t*>(sv->amax);
+                      int k, Carve& w, hipStream_t s, const hqlss_lsq_t* lsq = nullptr,
+                      float* dstep = nullptr) {
+  const uint32_t* amax = lsq ? reinterpret_cast<const uint32_t*>(lsq->step)
+                             : reinterpret_cast<const uint32_t*>(sv->amax);
+  const int smask = lsq ? 2 : 0;  // operand 2 (s_W or s_X) is a step in the LSQ mode
   const uint32_t* ag = reinterpret_cast<const uint32_t*>(p->amax_g);
   const float denom = (float)(kBsRatio * (int64_t(1) << k));
   const bool want_dx = dX || (acc && which_acc == 1);
@@ -214,6 +263,9 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     XtT = w.take<uint8_t>(D * Kp / 2);
     part_dw = w.take<int32_t>(gemm_partial_bytes(C, D, sp_dw));
   }
+  double* px = (lsq && dX) ? w.take<double>(8 * lsq_parts_dx(N, D, C)) : nullptr;
+  double* pw = (lsq && dW) ? w.take<double>(8 * lsq_parts_dw(N, D, C)) : nullptr;
+  if (!w.ok()) return HQLSS_ERR_WORKSPACE;
   HQ_TRY(launch_build_operands(s, dt, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept, sv->xq,
                                N, C, D, Ag, At, XtT, dX));
   if (want_dx) {
@@ -223,9 +275,11 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     g.M = N; g.m_dev = p->n_kept; g.N = D; g.K = C;
     g.out_rows = p->kept;
     g.amax1 = ag; g.amax2 = amax + 1; g.denom = denom; g.log2b = k;
+    g.steps_mask = smask;
     if (dX) {
       g.out = dX; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiDx, dt, false, true, g, sp_dx, part_dx));
+      if (lsq) { g.delta = lsq->delta_x; g.ds_part = px; }
+      HQ_TRY(launch_gemm(s, lsq ? kEpiDxL : kEpiDx, dt, false, true, g, sp_dx, part_dx));
     }
     if (acc && which_acc == 1) {
       g.out = acc; g.ldo = D;
@@ -238,26 +292,37 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     g.B = XtT; g.ldb = Kp / 2;
     g.M = C; g.N = D; g.K = Kp; g.k_dev = p->n_kept;
     g.amax1 = ag; g.amax2 = amax; g.denom = denom; g.log2b = k;
+    g.steps_mask = smask;
     if (dW) {
       g.out = dW; g.ldo = D;
-      HQ_TRY(launch_gemm(s, kEpiDw, dt, false, true, g, sp_dw, part_dw));
+      if (lsq) { g.delta = lsq->delta_w; g.ds_part = pw; }
+      HQ_TRY(launch_gemm(s, lsq ? kEpiDwL : kEpiDw, dt, false, true, g, sp_dw, part_dw));
     }
     if (acc && which_acc == 2) {
       g.out = acc; g.ldo = D;
       HQ_TRY(launch_gemm(s, kEpiAcc, dt, false, true, g, sp_dw, part_dw));
     }
   }
+  if (lsq && dstep) {
+    // g(s) = 1 / sqrt(Q_P numel) with Q_P = 7 (App. A.4)
+    const double gx = 1.0 / std::sqrt(7.0 * (double)N * (double)D);
+    const double gw = 1.0 / std::sqrt(7.0 * (double)C * (double)D);
+    HQ_TRY(launch_lsq_step_grad(s, px, px ? lsq_parts_dx(N, D, C) : 0, pw,
+                                pw ? lsq_parts_dw(N, D, C) : 0, p->amax_g, lsq->step, k, gx, gw,
+                                dstep));
+  }
   return HQLSS_OK;
 }
 
 hqlss_status check_bwd_common(const void* dY, const hqlss_saved_t* saved, int64_t N, int64_t D,
-                              int64_t C, int dt, int log2_block, int64_t budget) {
+                              int64_t C, int dt, int log2_block, int64_t budget,
+                              bool need_amax = true) {
   if (!dY) return HQLSS_ERR_NULL;
   hqlss_status st;
   if ((st = check_shape(N, D, C))) return st;
   if ((st = check_block(log2_block, D))) return st;
   if ((st = check_dtype(dt))) return st;
-  if ((st = check_saved(saved))) return st;
+  if ((st = check_saved(saved, need_amax))) return st;
   if (!a16(dY)) return HQLSS_ERR_ALIGN;
   if ((st = check_bwd_overflow(N, D, C, log2_block))) return st;
   if (budget > 2 * N || budget < HQLSS_BUDGET_KEEP_NONZERO) return HQLSS_ERR_ARG;
@@ -280,7 +345,7 @@ const char* kernel_name(int id) {
                                        "bit_split", "lss_plan", "build_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
                                        "gemm_reduce", "copy", "hsize_max", "hsize_err",
-                                       "hsize_pick"};
+                                       "hsize_pick", "lsq_quant", "lsq_step_grad"};
   return (id >= 0 && id < kKCount) ? names[id] : "?";
 }
 
@@ -311,6 +376,10 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
     case HQLSS_WS_FROM_PLAN: return dx_bytes(N, D, C) + dw_bytes(N, D, C);
     case HQLSS_WS_PLAN: return plan_scratch_bytes(N);
     case HQLSS_WS_HSIZE: return hsize_bytes();
+    case HQLSS_WS_FWD_LSQ: return fwd_gemm_partial(N, D, C);
+    case HQLSS_WS_BWD_LSQ:
+      return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C) + dw_bytes(N, D, C) +
+             lsq_parts_bytes(N, D, C, true, true);
   }
   return 0;
 }
@@ -350,6 +419,26 @@ hqlss_status hq_linear_fwd(const void* X, const void* W, void* Y, int64_t N, int
   if (!ws || ws_bytes < fwd_bytes(N, D, C)) return HQLSS_ERR_WORKSPACE;
   if (!a16(ws)) return HQLSS_ERR_ALIGN;
   return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
+}
+
+hqlss_status hq_linear_fwd_lsq(const void* X, const void* W, void* Y, int64_t N, int64_t D,
+                               int64_t C, hqlss_dtype dt, int log2_block,
+                               const hqlss_saved_t* saved, const hqlss_lsq_t* lsq, void* ws,
+                               size_t ws_bytes, void* stream) {
+  if (!X || !W || !Y) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if ((st = check_block(log2_block, D))) return st;
+  if ((st = check_dtype(dt))) return st;
+  if ((st = check_saved(saved, false))) return st;
+  if ((st = check_lsq(lsq, true, true))) return st;
+  if (!a16(X) || !a16(W) || !a16(Y)) return HQLSS_ERR_ALIGN;
+  if ((st = check_fwd_overflow(D))) return st;
+  const size_t need = fwd_gemm_partial(N, D, C);
+  if (need && (!ws || ws_bytes < need)) return HQLSS_ERR_WORKSPACE;
+  if (ws && !a16(ws)) return HQLSS_ERR_ALIGN;
+  return do_fwd_lsq(X, W, Y, N, D, C, dt, log2_block, saved, lsq, ws,
+                    static_cast<hipStream_t>(stream));
 }
 
 hqlss_status hq_choose_hadamard_size(const void* X, const void* W, int64_t N, int64_t D,
@@ -455,6 +544,29 @@ hqlss_status lss_linear_bwd_dw(const void* dY, const hqlss_saved_t* saved, void*
   if (!dW) return HQLSS_ERR_NULL;
   return bwd_impl(dY, saved, nullptr, dW, N, D, C, dt, log2_block, budget_rows, seed, offset, ws,
                   ws_bytes, stream);
+}
+
+hqlss_status lss_linear_bwd_lsq(const void* dY, const hqlss_saved_t* saved,
+                                const hqlss_lsq_t* lsq, void* dX, void* dW, float* dstep,
+                                int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                                int64_t budget_rows, uint64_t seed, uint64_t offset, void* ws,
+                                size_t ws_bytes, void* stream) {
+  if (!dX && !dW) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_bwd_common(dY, saved, N, D, C, dt, log2_block, budget_rows, false))) return st;
+  if ((st = check_lsq(lsq, dX != nullptr, dW != nullptr))) return st;
+  if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws)) || (dstep && !a4(dstep)))
+    return HQLSS_ERR_ALIGN;
+  const size_t need = plan_bytes(N, C) + plan_scratch_bytes(N) + (dX ? dx_bytes(N, D, C) : 0) +
+                      (dW ? dw_bytes(N, D, C) : 0) + lsq_parts_bytes(N, D, C, dX, dW);
+  if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  lss_plan_t p;
+  plan_from_ws(w, N, C, &p);
+  const int64_t B = resolve_budget(budget_rows, N);
+  if ((st = do_plan(dY, saved, &p, N, C, dt, B, seed, offset, w, s))) return st;
+  return do_grads(&p, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w, s, lsq, dstep);
 }
 
 hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t* plan, const hqlss_saved_t* saved,

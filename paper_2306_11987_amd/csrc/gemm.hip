@@ -168,11 +168,44 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4));
 }
 
+// alpha = fl(fl(s1 s2) / denom); an operand flagged in steps_mask is a step itself,
+// otherwise a tensor maximum a with s = fl(a / 7).
+__device__ __forceinline__ float scale_of(const GemmArgs& g) {
+  const uint32_t a1 = *g.amax1, a2 = *g.amax2;
+  const float s1 = (g.steps_mask & 1) ? __uint_as_float(a1) : step_of(a1);
+  const float s2 = (g.steps_mask & 2) ? __uint_as_float(a2) : step_of(a2);
+  return (s1 * s2) / g.denom;
+}
+
+__device__ __forceinline__ double f16_bits_to_double(uint32_t h) {
+  return (double)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+// clip indicator of the learned-step-size mode from an fp16 delta: |delta| <= 1/2
+__device__ __forceinline__ bool inside_of(uint32_t h) { return (h & 0x7FFFu) <= 0x3800u; }
+
+// Sum over the workgroup of one double per thread (fixed order); thread 0 gets the total.
+template <int THREADS>
+__device__ __forceinline__ double block_sum_f64(double v, double* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double t = 0.0;
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int w = 0; w < THREADS / 64; ++w) t += red[w];
+  }
+  return t;
+}
+
 template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B>
 __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC)) void gemm_kernel(GemmArgs g) {
   using C_ = Cfg<BM, A4, WN>;
   constexpr int TI = C_::TI, TJ = C_::TJ, BN = C_::BN;
   constexpr bool RAW = (EPI == kEpiAcc || EPI == kEpiPartial);
+  constexpr bool LSQ = (EPI == kEpiDxL || EPI == kEpiDwL);
+  constexpr bool GRAD = (EPI == kEpiDx || EPI == kEpiDw || LSQ);
+  constexpr bool ROWMAP = (EPI == kEpiDx || EPI == kEpiDxL);  // rows scatter through out_rows
   constexpr int ES = (RAW || DT == kF32) ? 4 : 2;
   constexpr int E_PITCH = BN * ES + 16;
   constexpr int E_ROWS = (BM * E_PITCH <= C_::LDS_MAIN) ? BM
@@ -194,15 +227,20 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
     const int64_t md = *g.m_dev;
     M = md < M ? md : M;
   }
-  if (m0 >= M) return;  // whole workgroup: uniform exit before any barrier
+  if (m0 >= M) {  // whole workgroup: uniform exit before any barrier
+    if constexpr (LSQ) {
+      if (tid == 0) g.ds_part[blockIdx.y * gridDim.x + blockIdx.x] = 0.0;
+    }
+    return;
+  }
   // the scale is read up front so that its latency hides behind the main loop
   float alpha = 0.f;
   if constexpr (EPI == kEpiFwd) {
     // fl(alpha 2^-SHIFT * fl(acc)) == fl(alpha * fl(acc >> SHIFT)): acc is a multiple of
     // 2^SHIFT and both scalings by powers of two are exact
-    alpha = alpha_of(*g.amax1, *g.amax2, g.denom) * (1.0f / (float)(1 << C_::SHIFT));
-  } else if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
-    alpha = alpha_of(*g.amax1, *g.amax2, g.denom);
+    alpha = scale_of(g) * (1.0f / (float)(1 << C_::SHIFT));
+  } else if constexpr (GRAD) {
+    alpha = scale_of(g);
   }
   int64_t K = g.K;
   if (g.k_dev) K = ((int64_t)*g.k_dev + 127) / 128 * 128;
@@ -397,7 +435,34 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   // (WN/2) (lane / 32) + r.  They go through LDS so that every store writes whole rows.
   const int ml = lane & 31;
   const int nh = (C_::WN / 2) * (lane >> 5);
-  if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
+  double lsq_sum = 0.0;
+  if constexpr (LSQ) {
+    // sum of acc * delta over this workgroup's valid entries, then the clip mask (App. A.4):
+    // both use the integer accumulator before the transform H^T.  Rows past M hold
+    // re-read data and are skipped; N is a multiple of the block, so the mask never mixes
+    // valid and invalid columns inside one transform.
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+      const int64_t gm = m0 + wm * C_::WM + 32 * i + ml;
+      if (gm >= M) continue;
+      const int64_t drow = ROWMAP ? (int64_t)g.out_rows[gm] : gm;
+      const uint16_t* dp = g.delta + drow * g.ldo + n0 + wn * C_::WN + nh;
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) {
+        if (n0 + wn * C_::WN + 16 * j + nh >= g.N) continue;
+        const uint4 d0 = ld_stream<true>(dp + 16 * j), d1 = ld_stream<true>(dp + 16 * j + 8);
+        const uint32_t dw[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t h = (dw[r >> 1] >> (16 * (r & 1))) & 0xFFFFu;
+          const int a = acc[i][j][r];
+          lsq_sum += (double)(a >> C_::SHIFT) * f16_bits_to_double(h);
+          acc[i][j][r] = inside_of(h) ? a : 0;
+        }
+      }
+    }
+  }
+  if constexpr (GRAD) {
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
       int v[TJ * 16];
@@ -461,7 +526,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
       const int r = idx / PIECES, pc = idx % PIECES;
       const int64_t gm = m0 + r_lo + r;
       val[it] = *reinterpret_cast<const uint4*>(smem + r * E_PITCH + pc * 16);
-      orow[it] = gm < M ? ((EPI == kEpiDx) ? g.out_rows[gm] : (int)gm) : -1;
+      orow[it] = gm < M ? (ROWMAP ? g.out_rows[gm] : (int)gm) : -1;
     }
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {
@@ -473,6 +538,11 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
             out + (out_plane + (int64_t)orow[it] * g.ldo + gn) * ES, val[it]);
     }
     __syncthreads();
+  }
+  if constexpr (LSQ) {
+    __shared__ double red[C_::WAVES];
+    const double t = block_sum_f64<C_::THREADS>(lsq_sum, red);
+    if (tid == 0) g.ds_part[blockIdx.y * gridDim.x + blockIdx.x] = t;
   }
 }
 
@@ -491,8 +561,12 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
   const uint32_t chunks = (uint32_t)((g.N + 511) / 512);
   const uint32_t items = (uint32_t)M * chunks;
   const uint32_t nw = gridDim.x * 4;
+  constexpr bool LSQ = (MODE == kEpiDxL || MODE == kEpiDwL);
+  constexpr bool GRAD = (MODE == kEpiDx || MODE == kEpiDw || LSQ);
+  constexpr bool ROWMAP = (MODE == kEpiDx || MODE == kEpiDxL);
   float alpha = 0.f;
-  if constexpr (MODE != kEpiAcc) alpha = alpha_of(*g.amax1, *g.amax2, g.denom);
+  if constexpr (MODE != kEpiAcc) alpha = scale_of(g);
+  double lsq_sum = 0.0;
   const int b = 1 << g.log2b;
   const int64_t plane = g.M * g.ldo;
   for (uint32_t it = blockIdx.x * 4 + (threadIdx.x >> 6); it < items; it += nw) {
@@ -509,8 +583,19 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
         v[0] += x0.x; v[1] += x0.y; v[2] += x0.z; v[3] += x0.w;
         v[4] += x1.x; v[5] += x1.y; v[6] += x1.z; v[7] += x1.w;
       }
+      if constexpr (LSQ) {  // as in the GEMM epilogue: sum acc * delta, then the mask
+        const int64_t drow = ROWMAP ? (int64_t)g.out_rows[m] : m;
+        const uint4 d = ld_stream<true>(g.delta + drow * g.ldo + n);
+        const uint32_t dw[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t h = (dw[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+          lsq_sum += (double)v[e] * f16_bits_to_double(h);
+          v[e] = inside_of(h) ? v[e] : 0;
+        }
+      }
     }
-    if constexpr (MODE == kEpiDx || MODE == kEpiDw) {
+    if constexpr (GRAD) {
       if (b > 1) {
 #pragma unroll
         for (int e = 0; e < 8; e += 2) { const int a = v[e], c = v[e + 1]; v[e] = a + c; v[e + 1] = a - c; }
@@ -539,12 +624,40 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
       st_stream<HQ_NT_G_ST>(p, make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]));
       st_stream<HQ_NT_G_ST>(p + 4, make_uint4((uint32_t)v[4], (uint32_t)v[5], (uint32_t)v[6], (uint32_t)v[7]));
     } else {
-      const int64_t orow = (MODE == kEpiDx) ? (int64_t)g.out_rows[m] : m;
+      const int64_t orow = ROWMAP ? (int64_t)g.out_rows[m] : m;
       float f[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) f[e] = alpha * (float)v[e];
       store8_stream<DT, HQ_NT_G_ST>(static_cast<char*>(g.out) + (orow * g.ldo + n) * Elem<DT>::bytes, f);
     }
+  }
+  if constexpr (LSQ) {
+    __shared__ double red[4];
+    const double t = block_sum_f64<256>(lsq_sum, red);
+    if (threadIdx.x == 0) g.ds_part[blockIdx.x] = t;
+  }
+}
+
+// Step-size gradients (App. A.4): ds = g(s) alpha sum(acc * delta) in fp64 over the
+// per-workgroup partials, summed by one workgroup in a fixed order (deterministic).
+__global__ __launch_bounds__(256) void lsq_step_grad_kernel(const double* __restrict__ px, int64_t nx,
+                                                            const double* __restrict__ pw, int64_t nw,
+                                                            const float* __restrict__ amax_g,
+                                                            const float* __restrict__ step, int log2b,
+                                                            double gx, double gw,
+                                                            float* __restrict__ dstep) {
+  __shared__ double red[4];
+  double sx = 0.0, sw = 0.0;
+  for (int64_t i = threadIdx.x; i < nx; i += 256) sx += px[i];
+  for (int64_t i = threadIdx.x; i < nw; i += 256) sw += pw[i];
+  sx = block_sum_f64<256>(sx, red);
+  __syncthreads();
+  sw = block_sum_f64<256>(sw, red);
+  if (threadIdx.x == 0) {
+    const double s_dn = (double)step_of(__float_as_uint(*amax_g)) / (double)kBsRatio;
+    const double pk = 1.0 / (double)(1 << log2b);
+    if (nx > 0) dstep[0] = (float)(gx * (s_dn * (double)step[1] * pk) * sx);
+    if (nw > 0) dstep[1] = (float)(gw * (s_dn * (double)step[0] * pk) * sw);
   }
 }
 
@@ -552,6 +665,15 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
 // 128 m x 64 n (half the widening per MFMA) unless the Hadamard block spans 64 or 128
 // columns (the in-register transform then needs no lane exchange)
 template <bool A4, int LOG2B> constexpr int wave_n() { return (A4 || LOG2B >= 6) ? 128 : 64; }
+
+// workgroups of reduce_epilogue for an M x N output (four waves, one (row, 512-column
+// chunk) item per wave at a time)
+int64_t reduce_grid(int64_t M, int64_t N) {
+  const int64_t items = M * ((N + 511) / 512);
+  int64_t wg = (items + 3) / 4;
+  if (wg > 2048) wg = 2048;
+  return wg < 1 ? 1 : wg;
+}
 
 template <int BM, bool A4, int EPI, int DT, int LOG2B>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
@@ -567,7 +689,7 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
 // the Hadamard block is a template parameter of the gradient epilogues
 template <int BM, bool A4, int EPI, int DT>
 hipError_t gemm_b(hipStream_t s, const GemmArgs& g, int splits, int id) {
-  if constexpr (EPI == kEpiDx || EPI == kEpiDw) {
+  if constexpr (EPI == kEpiDx || EPI == kEpiDw || EPI == kEpiDxL || EPI == kEpiDwL) {
     switch (g.log2b) {
       case 0: return gemm_t<BM, A4, EPI, DT, 0>(s, g, splits, id);
       case 1: return gemm_t<BM, A4, EPI, DT, 1>(s, g, splits, id);
@@ -586,10 +708,7 @@ hipError_t gemm_b(hipStream_t s, const GemmArgs& g, int splits, int id) {
 
 template <int DT, int MODE>
 hipError_t reduce_t(hipStream_t s, const int32_t* P, int S, const GemmArgs& g) {
-  const int64_t items = g.M * ((g.N + 511) / 512);
-  int64_t wg = (items + 3) / 4;
-  if (wg > 2048) wg = 2048;
-  if (wg < 1) wg = 1;
+  const int64_t wg = reduce_grid(g.M, g.N);
   timing_begin(s);
   reduce_epilogue_kernel<DT, MODE><<<(int)wg, 256, 0, s>>>(P, S, g);
   timing_end(s, kKReduce);
@@ -650,9 +769,28 @@ hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4,
   } else {
     if (epi == kEpiDx) return run_dt<false, kEpiDx>(s, dt, g, splits, partial, kKGemmDx);
     if (epi == kEpiDw) return run_dt<false, kEpiDw>(s, dt, g, splits, partial, kKGemmDw);
+    if (epi == kEpiDxL) return run_dt<false, kEpiDxL>(s, dt, g, splits, partial, kKGemmDx);
+    if (epi == kEpiDwL) return run_dt<false, kEpiDwL>(s, dt, g, splits, partial, kKGemmDw);
     if (epi == kEpiAcc) return run<false, kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
   }
   return hipErrorInvalidValue;
+}
+
+int64_t gemm_epi_parts(int64_t M, int64_t N, int splits) {
+  if (splits <= 1) {
+    const int64_t bm = tile_m<false>();
+    return ((N + kBN - 1) / kBN) * ((M + bm - 1) / bm);
+  }
+  return reduce_grid(M, N);
+}
+
+hipError_t launch_lsq_step_grad(hipStream_t s, const double* px, int64_t nx, const double* pw,
+                                int64_t nw, const float* amax_g, const float* step, int log2b,
+                                double gx, double gw, float* dstep) {
+  timing_begin(s);
+  lsq_step_grad_kernel<<<1, 256, 0, s>>>(px, nx, pw, nw, amax_g, step, log2b, gx, gw, dstep);
+  timing_end(s, kKLsqStepGrad);
+  return hipGetLastError();
 }
 
 }  // namespace hqlss

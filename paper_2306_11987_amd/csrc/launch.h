@@ -9,7 +9,7 @@ namespace hqlss {
 enum KernelId : int {
   kKAbsmax = 0, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuild,
   kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKHsizeMax, kKHsizeErr,
-  kKHsizePick, kKCount
+  kKHsizePick, kKLsqQuant, kKLsqStepGrad, kKCount
 };
 const char* kernel_name(int id);
 
@@ -47,6 +47,17 @@ struct QOut {
 };
 hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const QJob& j0, const QOut& o0,
                              const QJob& j1, const QOut& o1);
+// Learned-step-size codes of block-FWHT(src) (one pass, no maximum): r = fl(v * fl(1/s)),
+// codes clamp(rint(r), -7, 7) packed as above, optional row sums of squares, and
+// delta = q - [|r| <= 7] r as fp16 bits [rows][cols].
+struct LsqOut {
+  const float* step;   // device scalar s > 0
+  uint8_t* packed;
+  int32_t* row_sumsq;  // may be null
+  uint16_t* delta;
+};
+hipError_t launch_fwht_lsq(hipStream_t s, int dt, int log2b, const QJob& j0, const LsqOut& o0,
+                           const QJob& j1, const LsqOut& o1);
 // packed [rows][cols/2] -> packed [cols][rows/2] (rows, cols multiples of 64).
 hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t rows, int64_t cols,
                                    uint8_t* dst);
@@ -89,7 +100,10 @@ hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, cons
                                  int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX);
 
 // Integer GEMM  acc[m][n] = sum_k A[m][k] B[n][k]  (both operands K-contiguous rows).
-enum Epi : int { kEpiFwd = 0, kEpiDx = 1, kEpiDw = 2, kEpiAcc = 3, kEpiPartial = 4 };
+// kEpiDxL / kEpiDwL: the gradient epilogues of the learned-step-size mode, which mask the
+// accumulators by the clip indicator before the transform and sum acc * delta.
+enum Epi : int { kEpiFwd = 0, kEpiDx = 1, kEpiDw = 2, kEpiAcc = 3, kEpiPartial = 4, kEpiDxL = 5,
+                 kEpiDwL = 6 };
 struct GemmArgs {
   const void* A;        // [M][lda] bytes: packed int4 (a_int4) or K-interleaved int8
   const void* B;        // [N][ldb] bytes
@@ -104,6 +118,9 @@ struct GemmArgs {
   const uint32_t* amax2;
   float denom;                 // alpha = fl(fl(s1 s2) / denom)
   int log2b;                   // FWHT block of the gradient epilogues
+  int steps_mask;              // bit i set: amax(i+1) holds a step s itself (else s = a / 7)
+  const uint16_t* delta;       // kEpiDxL / kEpiDwL: fp16 delta, indexed like out (pitch ldo)
+  double* ds_part;             // kEpiDxL / kEpiDwL: one sum of acc * delta per workgroup
 };
 // Split-K factor the launcher uses for this shape (1 = no split), and the int32 partial
 // buffer it then needs (splits x M x N words).  A non-zero override forces the factor.
@@ -112,5 +129,15 @@ size_t gemm_partial_bytes(int64_t M, int64_t N, int splits);
 void gemm_set_split_override(int splits);
 hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4, const GemmArgs& g,
                        int splits, int32_t* partial);
+// Number of ds_part entries a kEpiDxL / kEpiDwL launch of this shape writes (every entry
+// is written, 0 by workgroups without rows).
+int64_t gemm_epi_parts(int64_t M, int64_t N, int splits);
+// Step-size gradients from the partial sums (one workgroup, fixed order):
+// dstep[0] = gx * (s_up / 14) s_w 2^-k * sum(px), dstep[1] = gw * (s_up / 14) s_x 2^-k *
+// sum(pw), s_up = fl(*amax_g / 7), step = {s_x, s_w}; an entry with no partials (n = 0)
+// is left unwritten.
+hipError_t launch_lsq_step_grad(hipStream_t s, const double* px, int64_t nx, const double* pw,
+                                int64_t nw, const float* amax_g, const float* step, int log2b,
+                                double gx, double gw, float* dstep);
 
 }  // namespace hqlss

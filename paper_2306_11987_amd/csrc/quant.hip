@@ -264,6 +264,83 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
   }
 }
 
+// Learned-step-size codes (Eq. 2 at a caller-given step, after the transform of Sec. 3.3):
+// r = fl(v * fl(1/s)), q = clamp(rint(r), -7, 7) and delta = q - [-7 <= r <= 7] r, the
+// term that the step-size gradient weights (App. A.4).  One pass: no maximum is needed.
+// The clamp comes first (med3), so the magic-number rounding only sees |x| <= 7, and
+// rint(clamp(r)) = clamp(rint(r)) as the bounds are integers.  q - r is exact in fp32 (q
+// and r lie within a factor of two of each other, or q = 0), then rounded to fp16 (to
+// nearest even); |delta| <= 1/2 holds exactly for the entries inside the range and
+// |delta| > 1/2 for the clipped ones, so the gradient kernels recover the clip indicator
+// from delta alone.
+template <int DT, int LOG2B>
+__global__ __launch_bounds__(kQThreads) void fwht_lsq_kernel(QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
+  constexpr int U = 4;
+  const bool second = (int)blockIdx.x >= j0.wg;
+  const QJob& j = second ? j1 : j0;
+  const LsqOut& o = second ? o1 : o0;
+  const int wg = second ? (int)blockIdx.x - j0.wg : (int)blockIdx.x;
+  const float inv = 1.0f / *o.step;
+  const Geo g(j, wg);
+  constexpr int EB = Elem<DT>::bytes;
+  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  int64_t k = 0, kp = 0;
+  int it = 0, ip = 0;
+  int ss = 0;
+  for (int64_t s0 = 0; s0 < g.steps; s0 += U) {
+    float v[U][kVE];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        load16<DT, HQ_NT_Q_LD>(base + (g.row_of(k) * j.cols + (int64_t)it * g.G * kVE) * EB, v[u]);
+        if (++it == g.iters) { it = 0; ++k; }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (s0 + u < g.steps) {
+        fwht16<LOG2B>(v[u], g.lane);
+        uint32_t y[kVE], dh[kVE / 2];
+#pragma unroll
+        for (int e = 0; e < kVE; e += 2) {
+          uint32_t h[2];
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const float r = v[u][e + t] * inv;
+            const float rc = __builtin_amdgcn_fmed3f(r, -7.0f, 7.0f);
+            const float m = rc + kRne;
+            y[e + t] = __float_as_uint(m);
+            const float q = m - kRne;
+            const float d = (rc == r) ? q - r : q;
+            h[t] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)d);
+          }
+          dh[e / 2] = h[0] | (h[1] << 16);
+        }
+        const uint32_t w0 = pack8_bits(y), w1 = pack8_bits(y + 8);
+        ss = sumsq8(w1, sumsq8(w0, ss));
+        const bool ok = g.valid(kp);
+        const int64_t r = g.row_of(kp);
+        if (ok) {
+          const int64_t c = (int64_t)ip * g.G + g.sub;  // 16-column chunk
+          st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(o.packed + r * (j.cols / 2)) + c, make_uint2(w0, w1));
+          uint4* dp = reinterpret_cast<uint4*>(o.delta + r * j.cols) + 2 * c;
+          st_stream<HQ_NT_Q_ST>(dp, make_uint4(dh[0], dh[1], dh[2], dh[3]));
+          st_stream<HQ_NT_Q_ST>(dp + 1, make_uint4(dh[4], dh[5], dh[6], dh[7]));
+        }
+        if (++ip == g.iters) {
+          if (o.row_sumsq) {
+            ss = group_sum(ss, g.G);
+            if (ok && g.sub == 0) o.row_sumsq[r] = ss;
+          }
+          ss = 0;
+          ip = 0;
+          ++kp;
+        }
+      }
+    }
+  }
+}
+
 __device__ __forceinline__ int sext4(uint32_t n) { return (int)(n ^ 8u) - 8; }
 
 __global__ __launch_bounds__(256) void transpose_packed_kernel(const uint8_t* __restrict__ src,
@@ -710,6 +787,17 @@ template <int DT, int LOG2B> struct QuantF {
   }
 };
 
+template <int DT, int LOG2B> struct LsqF {
+  static hipError_t run(hipStream_t s, QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
+    const void* f = reinterpret_cast<const void*>(&fwht_lsq_kernel<DT, LOG2B>);
+    fit_grid(j0, j1, resident_wgs(f));
+    timing_begin(s);
+    fwht_lsq_kernel<DT, LOG2B><<<j0.wg + j1.wg, kQThreads, 0, s>>>(j0, j1, o0, o1);
+    timing_end(s, kKLsqQuant);
+    return hipGetLastError();
+  }
+};
+
 int log2_group(int64_t cols) {
   const int64_t v = cols / kVE;
   int l = 0;
@@ -751,6 +839,16 @@ hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const QJob& j0, c
     case kF32: return dispatch_block<QuantF, kF32>(log2b, s, j0, j1, o0, o1);
     case kF16: return dispatch_block<QuantF, kF16>(log2b, s, j0, j1, o0, o1);
     case kBF16: return dispatch_block<QuantF, kBF16>(log2b, s, j0, j1, o0, o1);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_fwht_lsq(hipStream_t s, int dt, int log2b, const QJob& j0, const LsqOut& o0,
+                           const QJob& j1, const LsqOut& o1) {
+  switch (dt) {
+    case kF32: return dispatch_block<LsqF, kF32>(log2b, s, j0, j1, o0, o1);
+    case kF16: return dispatch_block<LsqF, kF16>(log2b, s, j0, j1, o0, o1);
+    case kBF16: return dispatch_block<LsqF, kBF16>(log2b, s, j0, j1, o0, o1);
   }
   return hipErrorInvalidValue;
 }
