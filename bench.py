@@ -10,6 +10,11 @@ Metric: effective TOPS = sum over linears of 6 N C D / step time (the dense-equi
 work of fwd + dX + dW), also as a fraction of the int8 MFMA peak, beside the same three
 GEMMs per linear in bf16 through torch (hipBLASLt) and the CPU oracle on a token slice.
 
+--mode lsq times the learned-step-size variant instead (Eq. 2 with caller-given steps,
+App. A.4 gradients including the step-size gradients), on the same workload with steps set
+before timing to half of each tensor's dynamic step (s = max|V H| / 14, so the largest
+entries clip).
+
 Prints ONE JSON line.
 """
 from __future__ import annotations
@@ -39,6 +44,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time")
+    p.add_argument("--mode", choices=("dynamic", "lsq"), default="dynamic",
+                   help="quantiser: per-tensor maxima (default) or learned step sizes")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="before the steps, run the library's plain copy kernel once over MIB MiB "
                         "(reference for hardware traffic counters)")
@@ -105,15 +112,35 @@ def main():
     del X, W, G
     seed = 0
     offsets = [0] * len(L)
+    lsq_mode = args.mode == "lsq"
+    if lsq_mode:
+        # steps (untimed): half of the dynamic step a / 7 of each tensor, a from the library
+        for e in L:
+            lin = e["lin"]
+            H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], lin.log2_block, e["wsf"])
+            step_t = (e["saved"].amax / 14.0).contiguous()
+            e["lsq"] = H.LSQ.empty(step_t, lin.N, lin.D, lin.C)
+            e["dstep"] = torch.empty(2, dtype=torch.float32, device=dev)
+            e["ws"] = H.workspace(H.WS_BWD_LSQ, lin.N, lin.D, lin.C, dev)
+            e["wsf"] = H.workspace(H.WS_FWD_LSQ, lin.N, lin.D, lin.C, dev)
+        torch.cuda.synchronize()
 
     def step():
         for e in L:
-            H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
+            if lsq_mode:
+                H.hq_linear_fwd_lsq(e["X"], e["W"], e["Y"], e["saved"], e["lsq"], e["lin"].log2_block,
+                                    e["wsf"])
+            else:
+                H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
         for i in reversed(range(len(L))):
             e = L[i]
             lin = e["lin"]
-            H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block, lin.budget,
-                             seed, offsets[i], e["ws"])
+            if lsq_mode:
+                H.lss_linear_bwd_lsq(e["G"], e["saved"], e["lsq"], e["dX"], e["dW"], e["dstep"], lin.D,
+                                     lin.log2_block, lin.budget, seed, offsets[i], e["ws"])
+            else:
+                H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block,
+                                 lin.budget, seed, offsets[i], e["ws"])
             offsets[i] += e["adv"]
 
     if args.copy_calibration > 0:
@@ -190,7 +217,7 @@ def main():
         ach = algo / (kernels[dom]["avg_us"] * 1e-6) / 1e12
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS,
                 "unit": "TFLOP/s", "frac": round(ach / INT8_PEAK_TOPS, 4),
-                "traffic": committed_traffic(dom, "bert_base_ffn"),
+                "traffic": committed_traffic(dom, "bert_base_ffn_lsq" if lsq_mode else "bert_base_ffn"),
                 "algorithmic_ops_per_launch": algo,
                 "note": "int8 MFMA ops (multiply-adds x 2) of the kept-token GEMM"}
 
@@ -222,7 +249,7 @@ def main():
     # ---- CPU oracle on a bounded token slice of the same workload
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(lins, args.cpu_seconds)
+        cpu = cpu_baseline(lins, args.cpu_seconds, lsq_mode)
 
     out = {
         "metric": METRIC,
@@ -239,6 +266,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "N": N, "linears": [[e["lin"].D, e["lin"].C] for e in L],
                    "log2_block": lins[0].log2_block, "io_dtype": lins[0].dtype, "budget": lins[0].budget,
+                   "quantizer": "lsq (s = max|V H| / 14)" if lsq_mode else "per-tensor max",
                    "kept_tokens": [round(k, 1) for k in kept]},
         "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
         "ms_per_step_with_kernel_events": round(ms_step_events, 4),
@@ -250,7 +278,7 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(lins, target_s: float):
+def cpu_baseline(lins, target_s: float, lsq_mode: bool = False):
     """The oracle, as it stands, on the first n tokens of each linear (fwd + bwd)."""
     import numpy as np
 
@@ -271,8 +299,15 @@ def cpu_baseline(lins, target_s: float):
                                lin.x_outlier_channels, lin.x_outlier_scale, lin.grad_kind, n)
             X, W, G = synth.linear_inputs(sub, CFG_ID, li)
             t0 = time.perf_counter()
-            f = O.hq_forward(X, W, lin.log2_block)
-            O.lss_backward(G, f, n, 0, 0)
+            if lsq_mode:
+                k = lin.log2_block
+                sx = O.absmax(O.fwht_rows(X, k)) / np.float32(14.0)
+                sw = O.absmax(O.fwht_rows(W, k)) / np.float32(14.0)
+                f = O.lsq_forward(X, W, k, sx, sw)
+                O.lsq_backward(G, f, n, 0, 0)
+            else:
+                f = O.hq_forward(X, W, lin.log2_block)
+                O.lss_backward(G, f, n, 0, 0)
             t += time.perf_counter() - t0
             ops += 6.0 * n * lin.C * lin.D
         return t, ops
@@ -285,7 +320,8 @@ def cpu_baseline(lins, target_s: float):
         n = int(min(lins[0].N, max(n + 64, n * target_s / max(t, 1e-3))) // 64 * 64)
         t, ops = run(n)
     return {"value": round(ops / t / 1e12, 6), "unit": "TOPS", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {n} of {lins[0].N} tokens of each linear, fwd + bwd (budget = {n}); "
+            "sample": f"first {n} of {lins[0].N} tokens of each linear, fwd + bwd (budget = {n}"
+                      f"{', learned step sizes' if lsq_mode else ''}); "
                       f"{t:.1f} s", "seconds": round(t, 2)}
 
 
