@@ -135,19 +135,26 @@ __device__ __forceinline__ void fwht_lane(int* v, int lane) {
   }
 }
 
-// XCD-aware tile order: workgroups are dispatched round-robin over the 8 XCDs by linear id,
-// so the linear id is remapped such that each XCD walks a contiguous run of tiles, n
-// fastest: consecutive tiles on one XCD share their A rows in that XCD's L2.
-__device__ __forceinline__ void tile_of(int& tm, int& tn) {
-  const int tiles_n = gridDim.x, T = gridDim.x * gridDim.y;
-  const int L = blockIdx.x + blockIdx.y * gridDim.x;
-  int Lp = L;
+// XCD-aware tile order.  The hardware dispatches workgroups to the 8 XCDs round-robin by
+// linear id, so workgroup b runs on XCD b % 8.  The T tiles (row-major, n fastest) are cut
+// into 8 contiguous chunks, one per XCD, and the j-th workgroup of XCD x takes position j
+// of chunk x: tiles in flight on one XCD then share their operand rows in its L2.  T counts
+// only the tiles with rows below M (the device-side row count of dX), so that the tiles
+// past it do not all fall on the last XCDs; workgroups beyond their chunk get no tile.
+// Returns false for those.  Split-K grids and small grids keep the plain order.
+__device__ __forceinline__ bool tile_of(int T, int tiles_n, int& tm, int& tn) {
+  const int b = blockIdx.x;
+  int L = b;
   if (gridDim.z == 1 && T >= 16) {
-    const int x = L % 8, loc = L / 8, q = T / 8, r = T % 8;
-    Lp = (x < r) ? x * (q + 1) + loc : r * (q + 1) + (x - r) * q + loc;
+    const int x = b & 7, j = b >> 3, q = T >> 3, r = T & 7;
+    if (j >= q + (x < r ? 1 : 0)) return false;
+    L = x * q + min(x, r) + j;
+  } else if (b >= T) {
+    return false;
   }
-  tm = Lp / tiles_n;
-  tn = Lp % tiles_n;
+  tm = L / tiles_n;
+  tn = L % tiles_n;
+  return true;
 }
 
 // 16-byte LDS-DMA load (global_load_lds_dwordx4): each lane's 16 bytes at g land at
@@ -219,20 +226,21 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / C_::WGN, wn = wid % C_::WGN;
 
-  int tm, tn;
-  tile_of(tm, tn);
-  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   int64_t M = g.M;
   if (g.m_dev) {
     const int64_t md = *g.m_dev;
     M = md < M ? md : M;
   }
-  if (m0 >= M) {  // whole workgroup: uniform exit before any barrier
+  const int tiles_n = (int)((g.N + BN - 1) / BN);
+  const int t_valid = tiles_n * (int)((M + BM - 1) / BM);  // tiles with rows below M
+  int tm, tn;
+  if (!tile_of(t_valid, tiles_n, tm, tn)) {  // whole workgroup: uniform exit before any barrier
     if constexpr (LSQ) {
-      if (tid == 0) g.ds_part[blockIdx.y * gridDim.x + blockIdx.x] = 0.0;
+      if (tid == 0) g.ds_part[blockIdx.x] = 0.0;
     }
     return;
   }
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   // the scale is read up front so that its latency hides behind the main loop
   float alpha = 0.f;
   if constexpr (EPI == kEpiFwd) {
@@ -542,7 +550,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   if constexpr (LSQ) {
     __shared__ double red[C_::WAVES];
     const double t = block_sum_f64<C_::THREADS>(lsq_sum, red);
-    if (tid == 0) g.ds_part[blockIdx.y * gridDim.x + blockIdx.x] = t;
+    if (tid == 0) g.ds_part[blockIdx.x] = t;
   }
 }
 
@@ -679,7 +687,8 @@ template <int BM, bool A4, int EPI, int DT, int LOG2B>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   constexpr int WN = wave_n<A4, LOG2B>();
   using C_ = Cfg<BM, A4, WN>;
-  dim3 grid((unsigned)((g.N + kBN - 1) / kBN), (unsigned)((g.M + BM - 1) / BM), (unsigned)splits);
+  // one workgroup per tile of the M x N output (M the host-side bound; see tile_of)
+  dim3 grid((unsigned)(((g.N + kBN - 1) / kBN) * ((g.M + BM - 1) / BM)), 1u, (unsigned)splits);
   timing_begin(s);
   gemm_kernel<BM, A4, WN, EPI, DT, LOG2B><<<grid, C_::THREADS, 0, s>>>(g);
   timing_end(s, id);

@@ -129,8 +129,9 @@ size_t gemm_partial_bytes(int64_t M, int64_t N, int splits);
 void gemm_set_split_override(int splits);
 hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4, const GemmArgs& g,
                        int splits, int32_t* partial);
-// Number of ds_part entries a kEpiDxL / kEpiDwL launch of this shape writes (every entry
-// is written, 0 by workgroups without rows).
+// Number of ds_part entries a kEpiDxL / kEpiDwL launch of this shape writes (one per
+// workgroup: of the GEMM, or of the reduction after split-K; every entry is written, 0 by
+// workgroups without rows).
 int64_t gemm_epi_parts(int64_t M, int64_t N, int splits);
 // Step-size gradients from the partial sums (one workgroup, fixed order):
 // dstep[0] = gx * (s_up / 14) s_w 2^-k * sum(px), dstep[1] = gw * (s_up / 14) s_x 2^-k *
