@@ -43,7 +43,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-from .philox_ref import uniforms16
+from .philox_ref import philox_blocks, uniforms16
 
 QMAX = 7  # Q_N = Q_P = 7 (Sec. 3.1)
 BS_RATIO = 14  # s_up / s_dn (bit-split reading)
@@ -59,7 +59,8 @@ __all__ = [
     "lss_backward", "weighted_rows", "stochastic_round", "MAX_LOG2_BLOCK", "KEEP_NONZERO",
     "resolve_budget", "hadamard_reconstruction", "hadamard_mse", "HadamardChoice",
     "choose_hadamard_size", "quantize_lsq", "LSQForward", "lsq_forward", "LSQBackward",
-    "lsq_backward", "lsq_grad_scale",
+    "lsq_backward", "lsq_grad_scale", "bmm_counter_stride", "bmm_lsq_forward",
+    "bmm_lsq_backward", "STREAM_SR", "STREAM_MASK",
 ]
 
 
@@ -473,8 +474,9 @@ def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: 
 # * v / s is taken as r = fl(v * fl(1/s)) in float32, codes clamp(rint(r), -7, 7);
 # * the clip mask of Sec. 4 is taken on r: I = [-7 <= r <= 7] (Hadamard domain);
 # * delta(s) = int_s(v) - I o (v / s) of App. A.4 is formed as q - I r (exact in float32)
-#   and kept as float16, the "FP16 version" the paper's implementation keeps for the LSQ
-#   backward (App. A.6); |delta| <= 1/2 inside the range and |delta| = 7 where clipped,
+#   and kept as float16, in place of the fp16 copy of the input that the paper's
+#   implementation keeps for the LSQ backward (App. A.6); |delta| <= 1/2 inside the range
+#   and |delta| = 7 where clipped,
 #   so the backward reads the mask back as I = [|delta| <= 1/2];
 # * the STE gradients mask the integer accumulators in the Hadamard domain, then apply
 #   H^T (mask first: chain rule), and the step-size gradients are
@@ -583,3 +585,46 @@ def lsq_backward(G: np.ndarray, fwd: LSQForward, budget: int, seed: int, offset:
         dW = a_dw * fwht_rows(masked, k).astype(np.float64)
         ds_w = lsq_grad_scale(C * D) * a_dw * float(np.sum(acc_dw.astype(np.float64) * dlw))
     return LSQBackward(bs, plan, A, acc_dx, acc_dw, dX, dW, ds_x, ds_w, a_dx, a_dw)
+
+
+# --------------------------------------------------------------------------
+# Attention BMM, T = BMM(Q, K^T) (App. A.1)
+# --------------------------------------------------------------------------
+# Readings:
+# * the batch is B independent instances of the learned-step-size linear operator above,
+#   X = Q_b [N][M], W = K_b [P][M], Y = T_b [N][P], with the per-batch steps s_Q[b],
+#   s_K[b] of App. A.1 and one Hadamard block size for all batches (H^ repeats H);
+# * the backward bit-splits and samples every batch on its own (per-batch scales s_up,b
+#   and leverage scores c_{b,i}, as for the linear operator), one shared sample per
+#   batch for grad Q and grad K;
+# * the random numbers of batch b are those of a single-instance backward at counter
+#   offset + b * bmm_counter_stride(N, P): disjoint Philox ranges for every batch;
+# * grad s_Q[b] and grad s_K[b] scale by g = 1 / sqrt(Q_P N_s) with N_s the elements
+#   quantised with that step (N M and P M).
+
+
+def bmm_counter_stride(N: int, P: int) -> int:
+    """Counter blocks between consecutive batches: those one backward over an N x P
+    gradient draws on its stochastic-rounding stream (8 uniforms per block)."""
+    return philox_blocks(int(N) * int(P))
+
+
+def bmm_lsq_forward(Q: np.ndarray, K: np.ndarray, log2_block: int, s_q, s_k,
+                    compute_output: bool = True):
+    """HQ-MM of every batch (App. A.1): Q [B][N][M], K [B][P][M], steps s_q, s_k [B]."""
+    Q = np.asarray(Q, dtype=np.float32)
+    K = np.asarray(K, dtype=np.float32)
+    assert Q.ndim == 3 and K.ndim == 3 and Q.shape[0] == K.shape[0] and Q.shape[2] == K.shape[2]
+    return [lsq_forward(Q[b], K[b], log2_block, np.float32(s_q[b]), np.float32(s_k[b]),
+                        compute_output) for b in range(Q.shape[0])]
+
+
+def bmm_lsq_backward(G: np.ndarray, fwds, budget: int, seed: int, offset: int,
+                     need_dq: bool = True, need_dk: bool = True):
+    """LSS-MM of every batch (App. A.1): G = grad T [B][N][P]; batch b draws its random
+    numbers at counter offset + b * bmm_counter_stride(N, P)."""
+    G = np.asarray(G, dtype=np.float32)
+    B, N, P = G.shape
+    adv = bmm_counter_stride(N, P)
+    return [lsq_backward(G[b], fwds[b], budget, seed, offset + b * adv, need_dq, need_dk)
+            for b in range(B)]
