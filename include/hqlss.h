@@ -113,6 +113,20 @@ typedef struct {
   uint16_t *delta_w;   /* [C][D]   fp16 delta_W                                            */
 } hqlss_lsq_t;
 
+/* Attention BMM T = BMM(Q, K^T) with per-batch learned steps (App. A.1): B independent
+ * problems with Q_b [N][M], K_b [P][M], T_b [N][P] (in the terms of the linear operator
+ * X = Q_b, W = K_b, D = M, C = P).  step_q and step_k hold one step per batch (device fp32,
+ * as for hqlss_lsq_t); delta_q [B][N][M] and delta_k [B][P][M] are the forward's fp16
+ * deltas.  The saved state of a batched call is the linear operator's per batch, stored
+ * batch after batch: xq [B][N][M/2], wq [B][P][M/2], wqT [B][M][P/2], x_sumsq [B][N];
+ * amax is not used. */
+typedef struct {
+  const float *step_q;  /* [B]        */
+  const float *step_k;  /* [B]        */
+  uint16_t *delta_q;    /* [B][N][M]  */
+  uint16_t *delta_k;    /* [B][P][M]  */
+} hqlss_bmm_lsq_t;
+
 /* budget_rows value selecting the keep-every-non-zero-row sample (see lss_grad_plan). */
 #define HQLSS_BUDGET_KEEP_NONZERO (-1)
 
@@ -120,6 +134,9 @@ typedef struct {
 enum { HQLSS_WS_FWD = 0, HQLSS_WS_BWD_DX = 1, HQLSS_WS_BWD_DW = 2, HQLSS_WS_BWD = 3,
        HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5, HQLSS_WS_HSIZE = 6, HQLSS_WS_FWD_LSQ = 7,
        HQLSS_WS_BWD_LSQ = 8 };
+/* Workspace sizes of the batched entry points (B problems of the given shape). */
+enum { HQLSS_WS_BMM_FWD = 0, HQLSS_WS_BMM_BWD = 1 };
+size_t hqlss_bmm_workspace_bytes(int which, int64_t B, int64_t N, int64_t M, int64_t P);
 size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C);
 
 /* HQ-MM forward (Sec. 3.3, Eq. 3; Procedure HQ-MM).
@@ -148,6 +165,19 @@ hqlss_status hq_linear_fwd_lsq(const void *X, const void *W, void *Y, int64_t N,
                                int64_t C, hqlss_dtype dt, int log2_block,
                                const hqlss_saved_t *saved, const hqlss_lsq_t *lsq, void *ws,
                                size_t ws_bytes, void *stream);
+
+/* Forward of the attention BMM (App. A.1): for every batch b, hq_linear_fwd_lsq with
+ * X = Q_b, W = K_b, steps step_q[b], step_k[b]:
+ *   codes and deltas of Q_b H_u and K_b H_u (one pass), T_b = fl(alpha_b acc_b) with
+ *   alpha_b = fl(fl(step_q[b] step_k[b]) / 2^k), cast to dt.
+ * Q [B][N][M], K [B][P][M] inputs; T [B][N][P] output; M and P positive multiples of 64
+ * (and M % 2^k == 0), 1 <= B <= 65535, B N and B P at most 2^30.  Every batch runs in the
+ * same launches (batch strides, no per-batch host work).  ws: at least
+ * hqlss_bmm_workspace_bytes(HQLSS_WS_BMM_FWD, ...) bytes (may be NULL when that is 0). */
+hqlss_status hq_bmm_fwd_lsq(const void *Q, const void *K, void *T, int64_t B, int64_t N,
+                            int64_t M, int64_t P, hqlss_dtype dt, int log2_block,
+                            const hqlss_saved_t *saved, const hqlss_bmm_lsq_t *lsq, void *ws,
+                            size_t ws_bytes, void *stream);
 
 /* Bit splitting and leverage-score sampling of dY (Sec. 4.2, App. A.2; Procedure LSS-MM
  * steps 1-3, shared by both gradients as in App. A.6).

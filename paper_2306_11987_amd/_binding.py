@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(_HERE, "libhqlss.so")
 
 WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN, WS_HSIZE = 0, 1, 2, 3, 4, 5, 6
 WS_FWD_LSQ, WS_BWD_LSQ = 7, 8
+WS_BMM_FWD, WS_BMM_BWD = 0, 1
 BUDGET_KEEP_NONZERO = -1  # HQLSS_BUDGET_KEEP_NONZERO: keep every non-zero gradient row
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
@@ -32,6 +33,10 @@ class _LsqC(ctypes.Structure):
     _fields_ = [("step", _vp), ("delta_x", _vp), ("delta_w", _vp)]
 
 
+class _BmmLsqC(ctypes.Structure):
+    _fields_ = [("step_q", _vp), ("step_k", _vp), ("delta_q", _vp), ("delta_k", _vp)]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
@@ -45,6 +50,9 @@ def _load() -> ctypes.CDLL:
                                    ctypes.POINTER(_LsqC), _vp, _sz, _vp]),
         "lss_linear_bwd_lsq": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_LsqC), _vp, _vp, _vp,
                                     _i64, _i64, _i64, _int, _int, _i64, _u64, _u64, _vp, _sz, _vp]),
+        "hq_bmm_fwd_lsq": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
+                                ctypes.POINTER(_BmmLsqC), _vp, _sz, _vp]),
+        "hqlss_bmm_workspace_bytes": (_sz, [_int, _i64, _i64, _i64, _i64]),
         "lss_grad_plan": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_PlanC), _i64, _i64, _i64,
                                _int, _i64, _u64, _u64, _vp, _sz, _vp]),
         "lss_linear_bwd_from_plan": (st, [ctypes.POINTER(_PlanC), ctypes.POINTER(_SavedC), _vp, _vp,
@@ -176,6 +184,53 @@ class LSQ:
 
     def c(self) -> _LsqC:
         return _LsqC(_ptr(self.step), _ptr(self.delta_x), _ptr(self.delta_w))
+
+
+@dataclass
+class BmmLSQ:
+    """Per-batch steps and fp16 deltas of the attention BMM (hqlss_bmm_lsq_t)."""
+
+    step_q: torch.Tensor  # float32 [B]
+    step_k: torch.Tensor  # float32 [B]
+    delta_q: torch.Tensor  # float16 [B, N, M]
+    delta_k: torch.Tensor  # float16 [B, P, M]
+
+    @staticmethod
+    def empty(step_q: torch.Tensor, step_k: torch.Tensor, N: int, M: int, P: int) -> "BmmLSQ":
+        B = step_q.numel()
+        if step_q.dtype != torch.float32 or step_k.dtype != torch.float32 or step_k.numel() != B:
+            raise ValueError("step_q and step_k must be float32 tensors of B elements")
+        f16 = dict(dtype=torch.float16, device=step_q.device)
+        return BmmLSQ(step_q, step_k, torch.empty(B, N, M, **f16), torch.empty(B, P, M, **f16))
+
+    def c(self) -> _BmmLsqC:
+        return _BmmLsqC(_ptr(self.step_q), _ptr(self.step_k), _ptr(self.delta_q), _ptr(self.delta_k))
+
+
+def bmm_saved_empty(B: int, N: int, M: int, P: int, device="cuda") -> "Saved":
+    """Saved state of a batched call: the linear operator's, batch after batch."""
+    u8 = dict(dtype=torch.uint8, device=device)
+    return Saved(torch.empty(B, N, M // 2, **u8), torch.empty(B, P, M // 2, **u8),
+                 torch.empty(B, M, P // 2, **u8), torch.empty(B, N, dtype=torch.int32, device=device),
+                 torch.empty(2, dtype=torch.float32, device=device))
+
+
+def bmm_workspace_bytes(which: int, B: int, N: int, M: int, P: int) -> int:
+    return int(lib.hqlss_bmm_workspace_bytes(int(which), int(B), int(N), int(M), int(P)))
+
+
+def bmm_workspace(which: int, B: int, N: int, M: int, P: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(bmm_workspace_bytes(which, B, N, M, P), 256), dtype=torch.uint8, device=device)
+
+
+def hq_bmm_fwd_lsq(Q: torch.Tensor, K: torch.Tensor, T: torch.Tensor, saved: "Saved", lsq: BmmLSQ,
+                   log2_block: int, ws: Optional[torch.Tensor] = None) -> None:
+    B, N, M = Q.shape
+    P = K.shape[1]
+    p, n = _ws(ws)
+    sv, lq = saved.c(), lsq.c()
+    _check(lib.hq_bmm_fwd_lsq(_ptr(Q), _ptr(K), _ptr(T), B, N, M, P, _dt(Q), int(log2_block),
+                              ctypes.byref(sv), ctypes.byref(lq), p, n, _stream(Q)), "hq_bmm_fwd_lsq")
 
 
 def workspace_bytes(which: int, N: int, D: int, C: int) -> int:

@@ -215,6 +215,48 @@ hqlss_status do_fwd_lsq(const void* X, const void* W, void* Y, int64_t N, int64_
   return HQLSS_OK;
 }
 
+// ---------------------------------------------------------------- attention BMM (App. A.1)
+hqlss_status check_bmm(int64_t B, int64_t N, int64_t M, int64_t P, int dt, int k) {
+  hqlss_status st;
+  if ((st = check_shape(N, M, P))) return st;
+  if (B < 1 || B > 65535 || B * N > (int64_t(1) << 30) || B * P > (int64_t(1) << 30))
+    return HQLSS_ERR_SHAPE;
+  if ((st = check_block(k, M))) return st;
+  return check_dtype(dt);
+}
+hqlss_status check_bmm_lsq(const hqlss_bmm_lsq_t* l) {
+  if (!l || !l->step_q || !l->step_k || !l->delta_q || !l->delta_k) return HQLSS_ERR_NULL;
+  if (!a4(l->step_q) || !a4(l->step_k) || !a16(l->delta_q) || !a16(l->delta_k))
+    return HQLSS_ERR_ALIGN;
+  return HQLSS_OK;
+}
+
+hqlss_status do_bmm_fwd(const void* Q, const void* K, void* T, int64_t B, int64_t N, int64_t M,
+                        int64_t P, int dt, int k, const hqlss_saved_t* sv,
+                        const hqlss_bmm_lsq_t* l, hipStream_t s) {
+  QJob jq = make_job_batched(Q, B, N, M), jk = make_job_batched(K, B, P, M);
+  const LsqOut oq{l->step_q, sv->xq, sv->x_sumsq, l->delta_q};
+  const LsqOut ok{l->step_k, sv->wq, nullptr, l->delta_k};
+  HQ_TRY(launch_fwht_lsq(s, dt, k, jq, oq, jk, ok));
+  HQ_TRY(launch_transpose_packed(s, sv->wq, P, M, sv->wqT, B));
+  GemmArgs g{};
+  g.A = sv->xq; g.lda = M / 2;
+  g.B = sv->wq; g.ldb = M / 2;
+  g.M = N; g.N = P; g.K = M;
+  g.out = T; g.ldo = P;
+  g.amax1 = reinterpret_cast<const uint32_t*>(l->step_q);
+  g.amax2 = reinterpret_cast<const uint32_t*>(l->step_k);
+  g.steps_mask = 3;
+  g.denom = (float)(int64_t(1) << k);
+  g.log2b = k;
+  g.batch = (int)B;
+  g.bs_a = N * M / 2;
+  g.bs_b = P * M / 2;
+  g.bs_out = N * P;
+  HQ_TRY(launch_gemm(s, kEpiFwd, dt, true, true, g, 1, nullptr));
+  return HQLSS_OK;
+}
+
 hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* p, int64_t N,
                      int64_t C, int dt, int64_t budget, uint64_t seed, uint64_t offset,
                      Carve& w, hipStream_t s) {
@@ -382,6 +424,31 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
              lsq_parts_bytes(N, D, C, true, true);
   }
   return 0;
+}
+
+size_t hqlss_bmm_workspace_bytes(int which, int64_t B, int64_t N, int64_t M, int64_t P) {
+  if (B < 1 || N < 1 || M < 1 || P < 1) return 0;
+  switch (which) {
+    case HQLSS_WS_BMM_FWD: return 0;
+  }
+  return 0;
+}
+
+hqlss_status hq_bmm_fwd_lsq(const void* Q, const void* K, void* T, int64_t B, int64_t N,
+                            int64_t M, int64_t P, hqlss_dtype dt, int log2_block,
+                            const hqlss_saved_t* saved, const hqlss_bmm_lsq_t* lsq, void* ws,
+                            size_t ws_bytes, void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!Q || !K || !T) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_bmm(B, N, M, P, dt, log2_block))) return st;
+  if ((st = check_saved(saved, false))) return st;
+  if ((st = check_bmm_lsq(lsq))) return st;
+  if (!a16(Q) || !a16(K) || !a16(T)) return HQLSS_ERR_ALIGN;
+  if ((st = check_fwd_overflow(M))) return st;
+  return do_bmm_fwd(Q, K, T, B, N, M, P, dt, log2_block, saved, lsq,
+                    static_cast<hipStream_t>(stream));
 }
 
 uint64_t lss_philox_offset_advance(int64_t N, int64_t C) {

@@ -142,10 +142,10 @@ __device__ __forceinline__ void fwht_lane(int* v, int lane) {
 // only the tiles with rows below M (the device-side row count of dX), so that the tiles
 // past it do not all fall on the last XCDs; workgroups beyond their chunk get no tile.
 // Returns false for those.  Split-K grids and small grids keep the plain order.
-__device__ __forceinline__ bool tile_of(int T, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ bool tile_of(int T, int tiles_n, bool split, int& tm, int& tn) {
   const int b = blockIdx.x;
   int L = b;
-  if (gridDim.z == 1 && T >= 16) {
+  if (!split && T >= 16) {
     const int x = b & 7, j = b >> 3, q = T >> 3, r = T & 7;
     if (j >= q + (x < r ? 1 : 0)) return false;
     L = x * q + min(x, r) + j;
@@ -225,6 +225,22 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   // wave index as a scalar: the LDS-DMA destinations (M0) then need no lane-to-scalar moves
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / C_::WGN, wn = wid % C_::WGN;
+  // grid z: the batch of a batched launch, else the split-K index
+  const int nsplit = g.batch > 0 ? 1 : (int)gridDim.z;
+  const int zsplit = g.batch > 0 ? 0 : (int)blockIdx.z;
+  if (g.batch > 0) {
+    const int64_t b = blockIdx.z;
+    g.A = static_cast<const uint8_t*>(g.A) + b * g.bs_a;
+    g.B = static_cast<const uint8_t*>(g.B) + b * g.bs_b;
+    g.out = static_cast<char*>(g.out) + b * g.bs_out * ES;
+    if (g.out_rows) g.out_rows += b * g.bs_rows;
+    if (g.m_dev) g.m_dev += b;
+    if (g.k_dev) g.k_dev += b;
+    if (g.amax1) g.amax1 += b;
+    if (g.amax2) g.amax2 += b;
+    if (g.delta) g.delta += b * g.bs_delta;
+    if (g.ds_part) g.ds_part += b * gridDim.x;
+  }
 
   int64_t M = g.M;
   if (g.m_dev) {
@@ -234,7 +250,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   const int tiles_n = (int)((g.N + BN - 1) / BN);
   const int t_valid = tiles_n * (int)((M + BM - 1) / BM);  // tiles with rows below M
   int tm, tn;
-  if (!tile_of(t_valid, tiles_n, tm, tn)) {  // whole workgroup: uniform exit before any barrier
+  if (!tile_of(t_valid, tiles_n, nsplit > 1, tm, tn)) {  // whole workgroup: uniform exit before any barrier
     if constexpr (LSQ) {
       if (tid == 0) g.ds_part[blockIdx.x] = 0.0;
     }
@@ -254,8 +270,8 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   if (g.k_dev) K = ((int64_t)*g.k_dev + 127) / 128 * 128;
   // split-K range of this workgroup (whole stages)
   const int nst_all = (int)((K + kKS - 1) / kKS);
-  const int per = (nst_all + (int)gridDim.z - 1) / (int)gridDim.z;
-  const int st0 = (int)blockIdx.z * per;
+  const int per = (nst_all + nsplit - 1) / nsplit;
+  const int st0 = zsplit * per;
   const int nst = max(0, min(nst_all, st0 + per) - st0);
   const int64_t Ka = A4 ? K / 2 : K, Kb = K / 2;  // row extents in bytes
 
@@ -487,7 +503,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC))
   }
   constexpr int PIECES = BN * ES / 16;  // 16-byte pieces per output row
   char* const out = static_cast<char*>(g.out);
-  const int64_t out_plane = (EPI == kEpiPartial) ? (int64_t)blockIdx.z * g.M * g.ldo : 0;
+  const int64_t out_plane = (EPI == kEpiPartial) ? (int64_t)zsplit * g.M * g.ldo : 0;
 #pragma unroll
   for (int chunk = 0; chunk < BM / E_ROWS; ++chunk) {
     const int r_lo = chunk * E_ROWS;
@@ -688,7 +704,8 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   constexpr int WN = wave_n<A4, LOG2B>();
   using C_ = Cfg<BM, A4, WN>;
   // one workgroup per tile of the M x N output (M the host-side bound; see tile_of)
-  dim3 grid((unsigned)(((g.N + kBN - 1) / kBN) * ((g.M + BM - 1) / BM)), 1u, (unsigned)splits);
+  dim3 grid((unsigned)(((g.N + kBN - 1) / kBN) * ((g.M + BM - 1) / BM)), 1u,
+            (unsigned)(g.batch > 0 ? g.batch : splits));
   timing_begin(s);
   gemm_kernel<BM, A4, WN, EPI, DT, LOG2B><<<grid, C_::THREADS, 0, s>>>(g);
   timing_end(s, id);

@@ -22,15 +22,20 @@ hipError_t launch_copy(hipStream_t s, const void* src, void* dst, int64_t bytes)
 
 // One tensor for the row-group quantisers: rows x cols (cols a multiple of 64), processed
 // by `wg` workgroups of 512 threads with 2^log2g lanes per row.  Launchers choose `wg`
-// (a grid that is resident at once) and store it back into the job.
-constexpr int kQMaxWg = 1024;  // workgroups (= partial results) of one job at most
+// (a grid that is resident at once) and store it back into the job.  A batched job holds
+// `batch` such tensors, `bstride` elements apart; `wg` is then per batch, and every
+// per-tensor output (codes, row sums, maxima, partials, ...) is one block per batch.
+constexpr int kQMaxWg = 1024;  // workgroups (= partial results) of one unbatched job at most
 struct QJob {
   const void* src;
   int64_t rows, cols;
   int log2g;
   int wg;
+  int batch;
+  int64_t bstride;
 };
 QJob make_job(const void* src, int64_t rows, int64_t cols);  // rows = 0: an empty job; wg unset
+QJob make_job_batched(const void* src, int64_t batch, int64_t rows, int64_t cols);
 
 // Per-workgroup maxima of |block-FWHT(src)| of up to two tensors in one launch:
 // part0[0, j0.wg) and part1[0, j1.wg), plain stores (no initialisation needed).
@@ -51,16 +56,17 @@ hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const QJob& j0, c
 // codes clamp(rint(r), -7, 7) packed as above, optional row sums of squares, and
 // delta = q - [|r| <= 7] r as fp16 bits [rows][cols].
 struct LsqOut {
-  const float* step;   // device scalar s > 0
+  const float* step;   // device scalar s > 0 (batched: step[b], one per batch)
   uint8_t* packed;
   int32_t* row_sumsq;  // may be null
   uint16_t* delta;
 };
 hipError_t launch_fwht_lsq(hipStream_t s, int dt, int log2b, const QJob& j0, const LsqOut& o0,
                            const QJob& j1, const LsqOut& o1);
-// packed [rows][cols/2] -> packed [cols][rows/2] (rows, cols multiples of 64).
+// packed [rows][cols/2] -> packed [cols][rows/2] (rows, cols multiples of 64), for each
+// of `batch` matrices stored one after the other.
 hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t rows, int64_t cols,
-                                   uint8_t* dst);
+                                   uint8_t* dst, int64_t batch = 1);
 // Bit split of dY [N][C] into two packed code planes, their row sums of squares, the
 // integer leverage scores scores[t] (upper row) and scores[score_pitch + t] (lower row),
 // and per-workgroup {count of non-zero scores, sum lo, sum hi, 0} in parts[0, j.wg).
@@ -74,6 +80,7 @@ struct BsOut {
   uint32_t* scores;
   int64_t score_pitch;
   uint4* parts;
+  uint64_t offset_stride;  // batched: Philox counter offset between batches
 };
 hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, int nparts,
                             const BsOut& o, uint64_t seed, uint64_t offset);
@@ -121,6 +128,12 @@ struct GemmArgs {
   int steps_mask;              // bit i set: amax(i+1) holds a step s itself (else s = a / 7)
   const uint16_t* delta;       // kEpiDxL / kEpiDwL: fp16 delta, indexed like out (pitch ldo)
   double* ds_part;             // kEpiDxL / kEpiDwL: one sum of acc * delta per workgroup
+  // Batched launch (batch > 0): blockIdx.z is the batch b (no split-K), and problem b uses
+  // A + b bs_a, B + b bs_b (bytes), out + b bs_out, delta + b bs_delta (elements),
+  // out_rows + b bs_rows, one m_dev / k_dev / amax1 / amax2 entry per batch and one block
+  // of ds_part entries per batch.
+  int batch;
+  int64_t bs_a, bs_b, bs_out, bs_rows, bs_delta;
 };
 // Split-K factor the launcher uses for this shape (1 = no split), and the int32 partial
 // buffer it then needs (splits x M x N words).  A non-zero override forces the factor.

@@ -154,6 +154,20 @@ __device__ __forceinline__ float reduce_parts(const float* __restrict__ part, in
   return m;
 }
 
+// Position of this workgroup in a launch over two (possibly batched) jobs: which job, the
+// batch b inside it, and the workgroup index within that batch.
+struct QPos {
+  bool second;
+  int b, wg;
+};
+__device__ __forceinline__ QPos qpos(const QJob& j0, const QJob& j1) {
+  const int n0 = j0.wg * j0.batch;
+  const bool second = (int)blockIdx.x >= n0;
+  const int idx = second ? (int)blockIdx.x - n0 : (int)blockIdx.x;
+  const int per = second ? j1.wg : j0.wg;
+  return {second, idx / per, idx % per};
+}
+
 // Plain 16-byte copy: the reference kernel against which hardware traffic counters are
 // calibrated (its bytes read and written are known exactly).
 __global__ __launch_bounds__(256) void copy_kernel(const uint4* __restrict__ src,
@@ -171,13 +185,13 @@ __global__ __launch_bounds__(kQThreads) void fwht_absmax_kernel(QJob j0, QJob j1
                                                                 float* __restrict__ part1) {
   constexpr int U = 4;  // steps in flight
   __shared__ float red[kQWaves];
-  const bool second = (int)blockIdx.x >= j0.wg;
-  const QJob& j = second ? j1 : j0;
-  const int wg = second ? (int)blockIdx.x - j0.wg : (int)blockIdx.x;
+  const QPos q = qpos(j0, j1);
+  const QJob& j = q.second ? j1 : j0;
+  const int wg = q.wg;
   const Geo g(j, wg);
   constexpr int EB = Elem<DT>::bytes;
   float m = 0.f;
-  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  const char* base = static_cast<const char*>(j.src) + ((int64_t)q.b * j.bstride + (int64_t)g.sub * kVE) * EB;
   int64_t k = 0;
   int it = 0;
   for (int64_t s0 = 0; s0 < g.steps; s0 += U) {
@@ -205,7 +219,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_absmax_kernel(QJob j0, QJob j1
 #pragma unroll
     for (int i = 1; i < kQWaves; ++i) m = fmaxf(m, red[i]);
     m = fmaxf(m, red[0]);
-    (second ? part1 : part0)[wg] = m;
+    (q.second ? part1 : part0)[q.b * j.wg + wg] = m;
   }
 }
 
@@ -276,14 +290,18 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_lsq_kernel(QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
   constexpr int U = 4;
-  const bool second = (int)blockIdx.x >= j0.wg;
-  const QJob& j = second ? j1 : j0;
-  const LsqOut& o = second ? o1 : o0;
-  const int wg = second ? (int)blockIdx.x - j0.wg : (int)blockIdx.x;
-  const float inv = 1.0f / *o.step;
+  const QPos qp = qpos(j0, j1);
+  const QJob& j = qp.second ? j1 : j0;
+  const LsqOut& o = qp.second ? o1 : o0;
+  const int wg = qp.wg;
+  const float inv = 1.0f / o.step[qp.b];
   const Geo g(j, wg);
   constexpr int EB = Elem<DT>::bytes;
-  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  const char* base = static_cast<const char*>(j.src) + ((int64_t)qp.b * j.bstride + (int64_t)g.sub * kVE) * EB;
+  // this batch's outputs
+  uint8_t* const packed = o.packed + (int64_t)qp.b * j.rows * (j.cols / 2);
+  uint16_t* const delta = o.delta + (int64_t)qp.b * j.rows * j.cols;
+  int32_t* const row_sumsq = o.row_sumsq ? o.row_sumsq + (int64_t)qp.b * j.rows : nullptr;
   int64_t k = 0, kp = 0;
   int it = 0, ip = 0;
   int ss = 0;
@@ -322,15 +340,15 @@ __global__ __launch_bounds__(kQThreads) void fwht_lsq_kernel(QJob j0, QJob j1, L
         const int64_t r = g.row_of(kp);
         if (ok) {
           const int64_t c = (int64_t)ip * g.G + g.sub;  // 16-column chunk
-          st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(o.packed + r * (j.cols / 2)) + c, make_uint2(w0, w1));
-          uint4* dp = reinterpret_cast<uint4*>(o.delta + r * j.cols) + 2 * c;
+          st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(packed + r * (j.cols / 2)) + c, make_uint2(w0, w1));
+          uint4* dp = reinterpret_cast<uint4*>(delta + r * j.cols) + 2 * c;
           st_stream<HQ_NT_Q_ST>(dp, make_uint4(dh[0], dh[1], dh[2], dh[3]));
           st_stream<HQ_NT_Q_ST>(dp + 1, make_uint4(dh[4], dh[5], dh[6], dh[7]));
         }
         if (++ip == g.iters) {
-          if (o.row_sumsq) {
+          if (row_sumsq) {
             ss = group_sum(ss, g.G);
-            if (ok && g.sub == 0) o.row_sumsq[r] = ss;
+            if (ok && g.sub == 0) row_sumsq[r] = ss;
           }
           ss = 0;
           ip = 0;
@@ -348,6 +366,8 @@ __global__ __launch_bounds__(256) void transpose_packed_kernel(const uint8_t* __
                                                                uint8_t* __restrict__ dst) {
   __shared__ int8_t t[64][65];  // codes [row_local][col_local]
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  src += (int64_t)blockIdx.z * rows * (cols / 2);  // matrix of this batch
+  dst += (int64_t)blockIdx.z * rows * (cols / 2);
   const int tid = threadIdx.x;
   const int r = tid >> 2, q = (tid & 3) * 8;  // 64 rows x 4 groups of 8 bytes
   {
@@ -385,16 +405,22 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
   constexpr int U = 2;
   __shared__ uint64_t red_s[kQWaves];
   __shared__ uint32_t red_n[kQWaves];
-  const int wg = blockIdx.x;
-  const float a = reduce_parts(part, nparts);
-  if (wg == 0 && threadIdx.x == 0) *o.amax_out = a;
+  // batch b of a batched job: its own maximum, outputs and Philox counter range
+  const int b = (int)blockIdx.x / j.wg, wg = (int)blockIdx.x % j.wg;
+  const float a = reduce_parts(part + (int64_t)b * nparts, nparts);
+  if (wg == 0 && threadIdx.x == 0) o.amax_out[b] = a;
   const float inv = a > 0.f ? 7.0f / a : 0.f;
   const Geo g(j, wg);
   const int64_t C = j.cols;
   constexpr int EB = Elem<DT>::bytes;
   uint32_t nnz = 0;
   uint64_t ssum = 0;
-  const char* base = static_cast<const char*>(j.src) + (int64_t)g.sub * kVE * EB;
+  const char* base = static_cast<const char*>(j.src) + ((int64_t)b * j.bstride + (int64_t)g.sub * kVE) * EB;
+  offset += (uint64_t)b * o.offset_stride;
+  const int64_t rb = (int64_t)b * j.rows;  // first row of this batch in the row-indexed outputs
+  uint8_t* const qup = o.qup + rb * (C / 2);
+  uint8_t* const qdn = o.qdn + rb * (C / 2);
+  uint32_t* const scores = o.scores + (int64_t)b * 2 * o.score_pitch;
   int64_t k = 0, kp = 0;
   int it = 0, ip = 0;
   int su = 0, sd = 0;
@@ -436,20 +462,20 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
         sd = sumsq8(d1, sumsq8(d0, sd));
         if (ok) {
           const int64_t o8 = r * (C / 16) + (int64_t)ip * g.G + g.sub;  // uint2 index
-          st_stream2<HQ_NT_BS_ST>(reinterpret_cast<uint2*>(o.qup) + o8, make_uint2(u0, u1));
-          st_stream2<HQ_NT_BS_ST>(reinterpret_cast<uint2*>(o.qdn) + o8, make_uint2(d0, d1));
+          st_stream2<HQ_NT_BS_ST>(reinterpret_cast<uint2*>(qup) + o8, make_uint2(u0, u1));
+          st_stream2<HQ_NT_BS_ST>(reinterpret_cast<uint2*>(qdn) + o8, make_uint2(d0, d1));
         }
         if (++ip == g.iters) {  // end of the group's row
           su = group_sum(su, g.G);
           sd = group_sum(sd, g.G);
           if (ok && g.sub == 0) {
-            o.sumsq_up[r] = su;
-            o.sumsq_dn[r] = sd;
-            const uint64_t sx = (uint32_t)o.x_sumsq[r];
+            o.sumsq_up[rb + r] = su;
+            o.sumsq_dn[rb + r] = sd;
+            const uint64_t sx = (uint32_t)o.x_sumsq[rb + r];
             const uint32_t cu = isqrt64(((uint64_t)(kBsRatio * kBsRatio) * (uint32_t)su * sx) << 16);
             const uint32_t cd = isqrt64(((uint64_t)(uint32_t)sd * sx) << 16);
-            o.scores[r] = cu;
-            o.scores[o.score_pitch + r] = cd;
+            scores[r] = cu;
+            scores[o.score_pitch + r] = cd;
             nnz += (cu > 0) + (cd > 0);
             ssum += (uint64_t)cu + cd;
           }
@@ -475,7 +501,7 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
       n += red_n[i];
       t += red_s[i];
     }
-    o.parts[wg] = make_uint4(n, (uint32_t)t, (uint32_t)(t >> 32), 0u);
+    o.parts[(int64_t)b * j.wg + wg] = make_uint4(n, (uint32_t)t, (uint32_t)(t >> 32), 0u);
   }
 }
 
@@ -749,10 +775,22 @@ int64_t wgs_needed(const QJob& j) {
 // Share one resident grid between two jobs: all they need if it fits, else in proportion
 // to their sizes (each at least one workgroup).
 void fit_grid(QJob& a, QJob& b, int cap) {
-  const int64_t na = wgs_needed(a), nb = wgs_needed(b);
-  if (na + nb <= cap) {
+  const int64_t na = wgs_needed(a), nb = wgs_needed(b);  // per batch
+  if (na * a.batch + nb * b.batch <= cap) {
     a.wg = (int)na;
     b.wg = (int)nb;
+    return;
+  }
+  if (a.batch > 1 || b.batch > 1) {  // batched: share the grid by size, then per batch
+    const double sa = (double)a.rows * a.cols * a.batch, sb = (double)b.rows * b.cols * b.batch;
+    const int64_t ca = nb ? (int64_t)(cap * sa / (sa + sb)) : cap, cb = cap - ca;
+    auto per = [](int64_t c, int64_t n, int64_t batch) {
+      int64_t w = c / batch;
+      if (w > n) w = n;
+      return (int)(w < 1 ? 1 : w);
+    };
+    a.wg = na ? per(ca, na, a.batch) : 0;
+    b.wg = nb ? per(cb, nb, b.batch) : 0;
     return;
   }
   const double ba = (double)a.rows * a.cols, bb = (double)b.rows * b.cols;
@@ -771,7 +809,7 @@ template <int DT, int LOG2B> struct AbsmaxF {
     const void* f = reinterpret_cast<const void*>(&fwht_absmax_kernel<DT, LOG2B>);
     fit_grid(j0, j1, resident_wgs(f));
     timing_begin(s);
-    fwht_absmax_kernel<DT, LOG2B><<<j0.wg + j1.wg, kQThreads, 0, s>>>(j0, j1, p0, p1);
+    fwht_absmax_kernel<DT, LOG2B><<<j0.wg * j0.batch + j1.wg * j1.batch, kQThreads, 0, s>>>(j0, j1, p0, p1);
     timing_end(s, kKAbsmax);
     return hipGetLastError();
   }
@@ -792,7 +830,7 @@ template <int DT, int LOG2B> struct LsqF {
     const void* f = reinterpret_cast<const void*>(&fwht_lsq_kernel<DT, LOG2B>);
     fit_grid(j0, j1, resident_wgs(f));
     timing_begin(s);
-    fwht_lsq_kernel<DT, LOG2B><<<j0.wg + j1.wg, kQThreads, 0, s>>>(j0, j1, o0, o1);
+    fwht_lsq_kernel<DT, LOG2B><<<j0.wg * j0.batch + j1.wg * j1.batch, kQThreads, 0, s>>>(j0, j1, o0, o1);
     timing_end(s, kKLsqQuant);
     return hipGetLastError();
   }
@@ -808,7 +846,13 @@ int log2_group(int64_t cols) {
 }  // namespace
 
 QJob make_job(const void* src, int64_t rows, int64_t cols) {
-  QJob j{src, rows > 0 ? rows : 0, cols, log2_group(cols), 0};
+  QJob j{src, rows > 0 ? rows : 0, cols, log2_group(cols), 0, 1, (rows > 0 ? rows : 0) * cols};
+  return j;
+}
+
+QJob make_job_batched(const void* src, int64_t batch, int64_t rows, int64_t cols) {
+  QJob j = make_job(src, rows, cols);
+  j.batch = (int)batch;
   return j;
 }
 
@@ -854,8 +898,8 @@ hipError_t launch_fwht_lsq(hipStream_t s, int dt, int log2b, const QJob& j0, con
 }
 
 hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t rows, int64_t cols,
-                                   uint8_t* dst) {
-  dim3 grid((unsigned)(cols / 64), (unsigned)(rows / 64));
+                                   uint8_t* dst, int64_t batch) {
+  dim3 grid((unsigned)(cols / 64), (unsigned)(rows / 64), (unsigned)batch);
   timing_begin(s);
   transpose_packed_kernel<<<grid, 256, 0, s>>>(src, rows, cols, dst);
   timing_end(s, kKTranspose);
@@ -872,13 +916,13 @@ hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, i
   timing_begin(s);
   switch (dt) {
     case kF32:
-      bit_split_kernel<kF32><<<j.wg, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
+      bit_split_kernel<kF32><<<j.wg * j.batch, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
       break;
     case kF16:
-      bit_split_kernel<kF16><<<j.wg, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
+      bit_split_kernel<kF16><<<j.wg * j.batch, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
       break;
     case kBF16:
-      bit_split_kernel<kBF16><<<j.wg, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
+      bit_split_kernel<kBF16><<<j.wg * j.batch, kQThreads, 0, s>>>(j, part, nparts, o, seed, offset);
       break;
     default:
       return hipErrorInvalidValue;
