@@ -179,6 +179,24 @@ hqlss_status hq_bmm_fwd_lsq(const void *Q, const void *K, void *T, int64_t B, in
                             const hqlss_saved_t *saved, const hqlss_bmm_lsq_t *lsq, void *ws,
                             size_t ws_bytes, void *stream);
 
+/* Backward of the attention BMM (App. A.1): for every batch b, lss_linear_bwd_lsq with
+ * dY = dT_b, X = Q_b, W = K_b and the steps of batch b: its own bit split (scale s_up,b),
+ * leverage scores c_{b,i} and sample, drawing its random numbers at counter offset
+ * offset + b * lss_philox_offset_advance(N, P); then
+ *   dQ_b = fl(alpha * FWHT_b(I_Q o acc_dx)), dK_b = fl(alpha * FWHT_b(I_K o acc_dw)),
+ *   dstep_q[b], dstep_k[b] as dstep[0], dstep[1] of lss_linear_bwd_lsq (g = 1/sqrt(7 N M)
+ *   and 1/sqrt(7 P M)).
+ * dT [B][N][P] input; dQ [B][N][M] or NULL, dK [B][P][M] or NULL (at least one);
+ * dstep_q, dstep_k: device fp32 [B] or NULL (dstep_q is written only with dQ, dstep_k only
+ * with dK).  saved and lsq as written by hq_bmm_fwd_lsq.  budget_rows per batch as for
+ * lss_linear_bwd.  Shapes as for hq_bmm_fwd_lsq, and N <= 65536.  ws: at least
+ * hqlss_bmm_workspace_bytes(HQLSS_WS_BMM_BWD, ...) bytes (less suffices with dQ or dK NULL). */
+hqlss_status lss_bmm_bwd_lsq(const void *dT, const hqlss_saved_t *saved,
+                             const hqlss_bmm_lsq_t *lsq, void *dQ, void *dK, float *dstep_q,
+                             float *dstep_k, int64_t B, int64_t N, int64_t M, int64_t P,
+                             hqlss_dtype dt, int log2_block, int64_t budget_rows, uint64_t seed,
+                             uint64_t offset, void *ws, size_t ws_bytes, void *stream);
+
 /* Bit splitting and leverage-score sampling of dY (Sec. 4.2, App. A.2; Procedure LSS-MM
  * steps 1-3, shared by both gradients as in App. A.6).
  *   q_up = rint(dY * fl(7/a_g)); r = that product - q_up; q_dn = SR(fl(14 r)) (stream 0);

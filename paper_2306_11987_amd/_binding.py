@@ -53,6 +53,8 @@ def _load() -> ctypes.CDLL:
         "hq_bmm_fwd_lsq": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
                                 ctypes.POINTER(_BmmLsqC), _vp, _sz, _vp]),
         "hqlss_bmm_workspace_bytes": (_sz, [_int, _i64, _i64, _i64, _i64]),
+        "lss_bmm_bwd_lsq": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_BmmLsqC), _vp, _vp, _vp, _vp,
+                                 _i64, _i64, _i64, _i64, _int, _int, _i64, _u64, _u64, _vp, _sz, _vp]),
         "lss_grad_plan": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_PlanC), _i64, _i64, _i64,
                                _int, _i64, _u64, _u64, _vp, _sz, _vp]),
         "lss_linear_bwd_from_plan": (st, [ctypes.POINTER(_PlanC), ctypes.POINTER(_SavedC), _vp, _vp,
@@ -231,6 +233,20 @@ def hq_bmm_fwd_lsq(Q: torch.Tensor, K: torch.Tensor, T: torch.Tensor, saved: "Sa
     sv, lq = saved.c(), lsq.c()
     _check(lib.hq_bmm_fwd_lsq(_ptr(Q), _ptr(K), _ptr(T), B, N, M, P, _dt(Q), int(log2_block),
                               ctypes.byref(sv), ctypes.byref(lq), p, n, _stream(Q)), "hq_bmm_fwd_lsq")
+
+
+def lss_bmm_bwd_lsq(dT: torch.Tensor, saved: "Saved", lsq: BmmLSQ, dQ: Optional[torch.Tensor],
+                    dK: Optional[torch.Tensor], dstep_q: Optional[torch.Tensor],
+                    dstep_k: Optional[torch.Tensor], M: int, log2_block: int, budget: int = 0,
+                    seed: int = 0, offset: int = 0, ws: Optional[torch.Tensor] = None) -> None:
+    B, N, P = dT.shape
+    if ws is None:
+        ws = bmm_workspace(WS_BMM_BWD, B, N, M, P, dT.device)
+    p, n = _ws(ws)
+    sv, lq = saved.c(), lsq.c()
+    _check(lib.lss_bmm_bwd_lsq(_ptr(dT), ctypes.byref(sv), ctypes.byref(lq), _ptr(dQ), _ptr(dK),
+                               _ptr(dstep_q), _ptr(dstep_k), B, N, int(M), P, _dt(dT), int(log2_block),
+                               int(budget), int(seed), int(offset), p, n, _stream(dT)), "lss_bmm_bwd_lsq")
 
 
 def workspace_bytes(which: int, N: int, D: int, C: int) -> int:

@@ -257,6 +257,102 @@ hqlss_status do_bmm_fwd(const void* Q, const void* K, void* T, int64_t B, int64_
   return HQLSS_OK;
 }
 
+// batched backward workspace: plan arrays, scratch, GEMM operands and step-gradient
+// partials of all batches (every batch is in flight at once)
+struct BmmWs {
+  int64_t parts;  // absmax / bit-split partials of all batches (upper bound)
+  int64_t kp;     // padded kept-token count per batch
+  int64_t tiles_dx, tiles_dw;
+};
+BmmWs bmm_ws_dims(int64_t B, int64_t N, int64_t M, int64_t P) {
+  return {B > kQMaxWg ? B : kQMaxWg, rup(N, kPad), gemm_epi_parts(N, M, 1), gemm_epi_parts(P, M, 1)};
+}
+size_t bmm_bwd_bytes(int64_t B, int64_t N, int64_t M, int64_t P, bool dq, bool dk) {
+  const BmmWs d = bmm_ws_dims(B, N, M, P);
+  size_t t = 2 * al(B * N * P / 2) + 2 * al(4 * B * N) + 2 * al(B * N) + al(4 * B * N) +
+             al(4 * B) * 2;
+  t += al(4 * d.parts) + al(4 * B * 2 * score_pitch(N)) + al(16 * d.parts);
+  if (dq) t += al(B * d.kp * P) + al(8 * B * d.tiles_dx);
+  if (dk) t += al(B * P * d.kp) + al(B * M * d.kp / 2) + al(8 * B * d.tiles_dw);
+  return t;
+}
+
+hqlss_status do_bmm_bwd(const void* dT, const hqlss_saved_t* sv, const hqlss_bmm_lsq_t* l,
+                        void* dQ, void* dK, float* dstep_q, float* dstep_k, int64_t B, int64_t N,
+                        int64_t M, int64_t P, int dt, int k, int64_t budget, uint64_t seed,
+                        uint64_t offset, Carve& w, hipStream_t s) {
+  const BmmWs d = bmm_ws_dims(B, N, M, P);
+  const int64_t pitch = score_pitch(N);
+  const uint64_t ostride = (uint64_t)((N * P + 7) / 8);  // counter blocks per batch (8 per block)
+  uint8_t* qup = w.take<uint8_t>(B * N * P / 2);
+  uint8_t* qdn = w.take<uint8_t>(B * N * P / 2);
+  int32_t* su = w.take<int32_t>(4 * B * N);
+  int32_t* sd = w.take<int32_t>(4 * B * N);
+  uint8_t* wu = w.take<uint8_t>(B * N);
+  uint8_t* wd = w.take<uint8_t>(B * N);
+  int32_t* kept = w.take<int32_t>(4 * B * N);
+  int32_t* nk = w.take<int32_t>(4 * B);
+  float* ag = w.take<float>(4 * B);
+  float* pg = w.take<float>(4 * d.parts);
+  uint32_t* scores = w.take<uint32_t>(4 * B * 2 * pitch);
+  uint4* bparts = w.take<uint4>(16 * d.parts);
+  int8_t* Ag = dQ ? w.take<int8_t>(B * d.kp * P) : nullptr;
+  double* px = dQ ? w.take<double>(8 * B * d.tiles_dx) : nullptr;
+  int8_t* At = dK ? w.take<int8_t>(B * P * d.kp) : nullptr;
+  uint8_t* XtT = dK ? w.take<uint8_t>(B * M * d.kp / 2) : nullptr;
+  double* pw = dK ? w.take<double>(8 * B * d.tiles_dw) : nullptr;
+  if (!w.ok()) return HQLSS_ERR_WORKSPACE;
+
+  // per-batch bit split and sample (App. A.1: every batch as a linear operator)
+  QJob jg = make_job_batched(dT, B, N, P), none = make_job(nullptr, 0, P);
+  HQ_TRY(launch_fwht_absmax(s, dt, 0, jg, pg, none, nullptr));
+  const int nparts = jg.wg;
+  const BsOut o{ag, qup, qdn, su, sd, sv->x_sumsq, scores, pitch, bparts, ostride};
+  HQ_TRY(launch_bit_split(s, dt, jg, pg, nparts, o, seed, offset));
+  HQ_TRY(launch_lss_plan(s, su, scores, pitch, bparts, jg.wg, N, budget, seed, offset, wu, wd,
+                         kept, nk, B, ostride));
+  HQ_TRY(launch_build_operands(s, dt, qup, qdn, wu, wd, kept, nk, sv->xq, N, P, M, Ag, At, XtT,
+                               dQ, B));
+  const uint32_t* agb = reinterpret_cast<const uint32_t*>(ag);
+  const float denom = (float)(kBsRatio * (int64_t(1) << k));
+  if (dQ) {  // grad Q_b = s_K[b] (I_Q o grad T_b K^_b) H^T on the kept rows
+    GemmArgs g{};
+    g.A = Ag; g.lda = P;
+    g.B = sv->wqT; g.ldb = P / 2;
+    g.M = N; g.m_dev = nk; g.N = M; g.K = P;
+    g.out_rows = kept;
+    g.amax1 = agb; g.amax2 = reinterpret_cast<const uint32_t*>(l->step_k);
+    g.steps_mask = 2; g.denom = denom; g.log2b = k;
+    g.out = dQ; g.ldo = M;
+    g.delta = l->delta_q; g.ds_part = px;
+    g.batch = (int)B;
+    g.bs_a = d.kp * P; g.bs_b = M * P / 2; g.bs_out = N * M; g.bs_rows = N; g.bs_delta = N * M;
+    HQ_TRY(launch_gemm(s, kEpiDxL, dt, false, true, g, 1, nullptr));
+  }
+  if (dK) {  // grad K_b = s_Q[b] (I_K o grad T_b^T Q^_b) H^T over the kept tokens
+    GemmArgs g{};
+    g.A = At; g.lda = d.kp;
+    g.B = XtT; g.ldb = d.kp / 2;
+    g.M = P; g.N = M; g.K = d.kp; g.k_dev = nk;
+    g.amax1 = agb; g.amax2 = reinterpret_cast<const uint32_t*>(l->step_q);
+    g.steps_mask = 2; g.denom = denom; g.log2b = k;
+    g.out = dK; g.ldo = M;
+    g.delta = l->delta_k; g.ds_part = pw;
+    g.batch = (int)B;
+    g.bs_a = P * d.kp; g.bs_b = M * d.kp / 2; g.bs_out = P * M; g.bs_delta = P * M;
+    HQ_TRY(launch_gemm(s, kEpiDwL, dt, false, true, g, 1, nullptr));
+  }
+  const bool sq = dQ && dstep_q, sk = dK && dstep_k;
+  if (sq || sk) {  // g(s) = 1 / sqrt(Q_P numel) per batch (App. A.4)
+    const double gq = 1.0 / std::sqrt(7.0 * (double)N * (double)M);
+    const double gk = 1.0 / std::sqrt(7.0 * (double)P * (double)M);
+    HQ_TRY(launch_lsq_step_grad(s, px, sq ? d.tiles_dx : 0, pw, sk ? d.tiles_dw : 0, ag,
+                                l->step_q, l->step_k, k, gq, gk, sq ? dstep_q : nullptr,
+                                sk ? dstep_k : nullptr, B));
+  }
+  return HQLSS_OK;
+}
+
 hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* p, int64_t N,
                      int64_t C, int dt, int64_t budget, uint64_t seed, uint64_t offset,
                      Carve& w, hipStream_t s) {
@@ -350,8 +446,8 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     const double gx = 1.0 / std::sqrt(7.0 * (double)N * (double)D);
     const double gw = 1.0 / std::sqrt(7.0 * (double)C * (double)D);
     HQ_TRY(launch_lsq_step_grad(s, px, px ? lsq_parts_dx(N, D, C) : 0, pw,
-                                pw ? lsq_parts_dw(N, D, C) : 0, p->amax_g, lsq->step, k, gx, gw,
-                                dstep));
+                                pw ? lsq_parts_dw(N, D, C) : 0, p->amax_g, lsq->step,
+                                lsq->step + 1, k, gx, gw, dstep, dstep + 1));
   }
   return HQLSS_OK;
 }
@@ -430,8 +526,33 @@ size_t hqlss_bmm_workspace_bytes(int which, int64_t B, int64_t N, int64_t M, int
   if (B < 1 || N < 1 || M < 1 || P < 1) return 0;
   switch (which) {
     case HQLSS_WS_BMM_FWD: return 0;
+    case HQLSS_WS_BMM_BWD: return bmm_bwd_bytes(B, N, M, P, true, true);
   }
   return 0;
+}
+
+hqlss_status lss_bmm_bwd_lsq(const void* dT, const hqlss_saved_t* saved,
+                             const hqlss_bmm_lsq_t* lsq, void* dQ, void* dK, float* dstep_q,
+                             float* dstep_k, int64_t B, int64_t N, int64_t M, int64_t P,
+                             hqlss_dtype dt, int log2_block, int64_t budget_rows, uint64_t seed,
+                             uint64_t offset, void* ws, size_t ws_bytes, void* stream) {
+  if (!dT) return HQLSS_ERR_NULL;
+  if (!dQ && !dK) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_bmm(B, N, M, P, dt, log2_block))) return st;
+  if ((st = check_saved(saved, false))) return st;
+  if ((st = check_bmm_lsq(lsq))) return st;
+  if (!a16(dT) || (dQ && !a16(dQ)) || (dK && !a16(dK)) || (ws && !a16(ws)) ||
+      (dstep_q && !a4(dstep_q)) || (dstep_k && !a4(dstep_k)))
+    return HQLSS_ERR_ALIGN;
+  if ((st = check_bwd_overflow(N, M, P, log2_block))) return st;
+  if (budget_rows > 2 * N || budget_rows < HQLSS_BUDGET_KEEP_NONZERO) return HQLSS_ERR_ARG;
+  if (!ws || ws_bytes < bmm_bwd_bytes(B, N, M, P, dQ != nullptr, dK != nullptr))
+    return HQLSS_ERR_WORKSPACE;
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  return do_bmm_bwd(dT, saved, lsq, dQ, dK, dstep_q, dstep_k, B, N, M, P, dt, log2_block,
+                    resolve_budget(budget_rows, N), seed, offset, w,
+                    static_cast<hipStream_t>(stream));
 }
 
 hqlss_status hq_bmm_fwd_lsq(const void* Q, const void* K, void* T, int64_t B, int64_t N,

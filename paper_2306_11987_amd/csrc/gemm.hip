@@ -667,10 +667,22 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
 __global__ __launch_bounds__(256) void lsq_step_grad_kernel(const double* __restrict__ px, int64_t nx,
                                                             const double* __restrict__ pw, int64_t nw,
                                                             const float* __restrict__ amax_g,
-                                                            const float* __restrict__ step, int log2b,
+                                                            const float* __restrict__ step_x,
+                                                            const float* __restrict__ step_w, int log2b,
                                                             double gx, double gw,
-                                                            float* __restrict__ dstep) {
+                                                            float* __restrict__ dstep_x,
+                                                            float* __restrict__ dstep_w) {
   __shared__ double red[4];
+  {  // block b: batch b of a batched call
+    const int64_t bt = blockIdx.x;
+    px += bt * nx;
+    pw += bt * nw;
+    amax_g += bt;
+    step_x += bt;
+    step_w += bt;
+    dstep_x += bt;
+    dstep_w += bt;
+  }
   double sx = 0.0, sw = 0.0;
   for (int64_t i = threadIdx.x; i < nx; i += 256) sx += px[i];
   for (int64_t i = threadIdx.x; i < nw; i += 256) sw += pw[i];
@@ -680,8 +692,8 @@ __global__ __launch_bounds__(256) void lsq_step_grad_kernel(const double* __rest
   if (threadIdx.x == 0) {
     const double s_dn = (double)step_of(__float_as_uint(*amax_g)) / (double)kBsRatio;
     const double pk = 1.0 / (double)(1 << log2b);
-    if (nx > 0) dstep[0] = (float)(gx * (s_dn * (double)step[1] * pk) * sx);
-    if (nw > 0) dstep[1] = (float)(gw * (s_dn * (double)step[0] * pk) * sw);
+    if (nx > 0) *dstep_x = (float)(gx * (s_dn * (double)*step_w * pk) * sx);
+    if (nw > 0) *dstep_w = (float)(gw * (s_dn * (double)*step_x * pk) * sw);
   }
 }
 
@@ -811,10 +823,12 @@ int64_t gemm_epi_parts(int64_t M, int64_t N, int splits) {
 }
 
 hipError_t launch_lsq_step_grad(hipStream_t s, const double* px, int64_t nx, const double* pw,
-                                int64_t nw, const float* amax_g, const float* step, int log2b,
-                                double gx, double gw, float* dstep) {
+                                int64_t nw, const float* amax_g, const float* step_x,
+                                const float* step_w, int log2b, double gx, double gw,
+                                float* dstep_x, float* dstep_w, int64_t batch) {
   timing_begin(s);
-  lsq_step_grad_kernel<<<1, 256, 0, s>>>(px, nx, pw, nw, amax_g, step, log2b, gx, gw, dstep);
+  lsq_step_grad_kernel<<<(unsigned)batch, 256, 0, s>>>(px, nx, pw, nw, amax_g, step_x, step_w, log2b,
+                                                       gx, gw, dstep_x, dstep_w);
   timing_end(s, kKLsqStepGrad);
   return hipGetLastError();
 }

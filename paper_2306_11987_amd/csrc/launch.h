@@ -91,11 +91,14 @@ hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, i
 hipError_t launch_hsize_search(hipStream_t s, int dt, QJob& j0, QJob& j1, float* mx0, float* mx1,
                                double* err0, double* err1, int kmax, int32_t* k_out,
                                double* mse_out);
-// leverage scores, clamp-rescale, masks, compaction (one workgroup).
+// leverage scores, clamp-rescale, masks, compaction (one workgroup per batch; batch b reads
+// and writes its own blocks: N rows, 2 score_pitch scores, nparts partials, one n_kept, and
+// draws at counter offset + b offset_stride).
 hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_t* scores,
                            int64_t score_pitch, const uint4* parts, int nparts, int64_t N,
                            int64_t budget, uint64_t seed, uint64_t offset, uint8_t* w_up,
-                           uint8_t* w_dn, int32_t* kept, int32_t* n_kept);
+                           uint8_t* w_dn, int32_t* kept, int32_t* n_kept, int64_t batch = 1,
+                           uint64_t offset_stride = 0);
 // GEMM operands of the kept tokens in one pass (any of Ag, At, XtT, dX may be null):
 // Ag [round_up(N,128)][C] weighted rows (int8, K-interleaved; rows < round_up(n_kept,128)
 // written), At [C][Kp] the same transposed and XtT [D][Kp/2] the gathered X^ rows
@@ -104,7 +107,8 @@ hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_
 hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
                                  const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
                                  const int32_t* n_kept, const uint8_t* xq, int64_t N, int64_t C,
-                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX);
+                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX,
+                                 int64_t batch = 1);
 
 // Integer GEMM  acc[m][n] = sum_k A[m][k] B[n][k]  (both operands K-contiguous rows).
 // kEpiDxL / kEpiDwL: the gradient epilogues of the learned-step-size mode, which mask the
@@ -147,11 +151,14 @@ hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4,
 // workgroups without rows).
 int64_t gemm_epi_parts(int64_t M, int64_t N, int splits);
 // Step-size gradients from the partial sums (one workgroup, fixed order):
-// dstep[0] = gx * (s_up / 14) s_w 2^-k * sum(px), dstep[1] = gw * (s_up / 14) s_x 2^-k *
-// sum(pw), s_up = fl(*amax_g / 7), step = {s_x, s_w}; an entry with no partials (n = 0)
-// is left unwritten.
+// dstep_x = gx * (s_up / 14) s_w 2^-k * sum(px), dstep_w = gw * (s_up / 14) s_x 2^-k *
+// sum(pw), s_up = fl(*amax_g / 7), s_x = *step_x, s_w = *step_w; an entry with no partials
+// (n = 0) is left unwritten.
+// Batched (batch > 1): block b uses px + b nx, pw + b nw and entry b of amax_g, step_x,
+// step_w, dstep_x, dstep_w; the linear operator passes step_x = step, step_w = step + 1.
 hipError_t launch_lsq_step_grad(hipStream_t s, const double* px, int64_t nx, const double* pw,
-                                int64_t nw, const float* amax_g, const float* step, int log2b,
-                                double gx, double gw, float* dstep);
+                                int64_t nw, const float* amax_g, const float* step_x,
+                                const float* step_w, int log2b, double gx, double gw,
+                                float* dstep_x, float* dstep_w, int64_t batch = 1);
 
 }  // namespace hqlss

@@ -71,10 +71,21 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     const int32_t* __restrict__ sumsq_up, const uint32_t* __restrict__ scores, int64_t pitch,
     const uint4* __restrict__ parts, int nparts, int N, int64_t B, uint64_t seed,
     uint64_t offset, uint8_t* __restrict__ w_up, uint8_t* __restrict__ w_dn,
-    int32_t* __restrict__ kept, int32_t* __restrict__ n_kept) {
+    int32_t* __restrict__ kept, int32_t* __restrict__ n_kept, uint64_t offset_stride) {
   __shared__ uint64_t red[2 * kPlanWaves];
   __shared__ int wtot[kPlanWaves];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  {  // workgroup b samples batch b of a batched call (its own inputs, outputs and counters)
+    const int64_t bt = blockIdx.x;
+    sumsq_up += bt * N;
+    scores += bt * 2 * pitch;
+    parts += bt * nparts;
+    w_up += bt * N;
+    w_dn += bt * N;
+    kept += bt * N;
+    n_kept += bt;
+    offset += (uint64_t)bt * offset_stride;
+  }
 
   // totals of the bit-split workgroups: non-zero rows and the score sum
   uint64_t nz = 0, st = 0;
@@ -245,6 +256,20 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
   __shared__ int8_t tile[64][65];  // [kept index][column]
   const int tid = threadIdx.x;
   const int64_t cb = C / 64, db = D / 64;
+  {  // grid z: batch b of a batched call, every operand one block per batch
+    const int64_t bt = blockIdx.z, kpad = (N + 127) / 128 * 128;
+    qup += bt * N * (C / 2);
+    qdn += bt * N * (C / 2);
+    w_up += bt * N;
+    w_dn += bt * N;
+    kept += bt * N;
+    n_kept += bt;
+    xq += bt * N * (D / 2);
+    if (Ag) Ag += bt * kpad * C;
+    if (At) At += bt * C * kpad;
+    if (XtT) XtT += bt * D * (kpad / 2);
+    if (dX) dX = static_cast<char*>(dX) + bt * N * D * Elem<DT>::bytes;
+  }
   if ((int64_t)blockIdx.y == cb + db) {  // zero the dX rows of dropped tokens
     if (!dX) return;
     const int64_t bytes = D * Elem<DT>::bytes;
@@ -324,10 +349,12 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
 hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_t* scores,
                            int64_t score_pitch, const uint4* parts, int nparts, int64_t N,
                            int64_t budget, uint64_t seed, uint64_t offset, uint8_t* w_up,
-                           uint8_t* w_dn, int32_t* kept, int32_t* n_kept) {
+                           uint8_t* w_dn, int32_t* kept, int32_t* n_kept, int64_t batch,
+                           uint64_t offset_stride) {
   timing_begin(s);
-  lss_plan_kernel<<<1, kPlanThreads, 0, s>>>(sumsq_up, scores, score_pitch, parts, nparts, (int)N,
-                                             budget, seed, offset, w_up, w_dn, kept, n_kept);
+  lss_plan_kernel<<<(unsigned)batch, kPlanThreads, 0, s>>>(sumsq_up, scores, score_pitch, parts,
+                                                           nparts, (int)N, budget, seed, offset,
+                                                           w_up, w_dn, kept, n_kept, offset_stride);
   timing_end(s, kKPlan);
   return hipGetLastError();
 }
@@ -335,9 +362,10 @@ hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_
 hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
                                  const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
                                  const int32_t* n_kept, const uint8_t* xq, int64_t N, int64_t C,
-                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX) {
+                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX,
+                                 int64_t batch) {
   const int64_t pitch = (N + 127) / 128 * 128;
-  dim3 grid((unsigned)(pitch / 64), (unsigned)(C / 64 + D / 64 + 1));
+  dim3 grid((unsigned)(pitch / 64), (unsigned)(C / 64 + D / 64 + 1), (unsigned)batch);
   timing_begin(s);
   switch (dt) {
     case kF32:
