@@ -10,6 +10,12 @@ Metric: effective TOPS = sum over linears of 6 N C D / step time (the dense-equi
 work of fwd + dX + dW), also as a fraction of the int8 MFMA peak, beside the same three
 GEMMs per linear in bf16 through torch (hipBLASLt) and the CPU oracle on a token slice.
 
+--mode bmm times the attention BMM T = BMM(Q, K^T) of App. A.1 instead (per-batch learned
+steps, per-batch sampling): BERT-base attention scores, 32 sequences x 12 heads = 384
+batches of 512 x 512 x 64, fp16, Hadamard block 32, steps half of each batch's dynamic
+step; effective TOPS = 6 B N P M / step time, beside the same three products per step as
+bf16 torch.bmm.
+
 --mode lsq times the learned-step-size variant instead (Eq. 2 with caller-given steps,
 App. A.4 gradients including the step-size gradients), on the same workload with steps set
 before timing to half of each tensor's dynamic step (s = max|V H| / 14, so the largest
@@ -44,7 +50,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time")
-    p.add_argument("--mode", choices=("dynamic", "lsq"), default="dynamic",
+    p.add_argument("--mode", choices=("dynamic", "lsq", "bmm"), default="dynamic",
                    help="quantiser: per-tensor maxima (default) or learned step sizes")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="before the steps, run the library's plain copy kernel once over MIB MiB "
@@ -89,6 +95,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if args.mode == "bmm":
+        return main_bmm(args, np, torch, H, synth, dev)
     wl = synth.workload(CFG_ID)
     lins = wl.linears
     N = lins[0].N
@@ -276,6 +284,153 @@ def main():
         "kernels": {k: {kk: round(vv, 3) for kk, vv in v.items()} for k, v in sorted(kernels.items())},
     }
     print(json.dumps(out), flush=True)
+
+
+BMM_B, BMM_N, BMM_P, BMM_M, BMM_K = 384, 512, 512, 64, 5
+BMM_METRIC = "INT4 attention BMM fwd+bwd effective TOPS (fraction of int8-MFMA peak) vs bf16"
+
+
+def bmm_inputs(np, synth, b, n_rows=BMM_N):
+    """Q_b, K_b, dT_b of batch b: the linear workload generators at attention shapes."""
+    lin = synth.Linear(f"attn{b}", n_rows, BMM_M, BMM_P, BMM_K, "f16", 2, 20.0, "lognormal", n_rows)
+    return synth.linear_inputs(lin, 5000 + b)
+
+
+def main_bmm(args, np, torch, H, synth, dev):
+    B, N, P, M, k = BMM_B, BMM_N, BMM_P, BMM_M, BMM_K
+    tdt = torch.float16
+    Qh, Kh, Gh = (np.stack(a) for a in zip(*[bmm_inputs(np, synth, b) for b in range(B)]))
+    Q = torch.from_numpy(Qh).to(dev, tdt)
+    K = torch.from_numpy(Kh).to(dev, tdt)
+    G = torch.from_numpy(Gh).to(dev, tdt)
+    del Qh, Kh, Gh
+    # per-batch steps (untimed): half of each batch's dynamic step, from the library's forward
+    s_q = torch.empty(B, dtype=torch.float32, device=dev)
+    s_k = torch.empty(B, dtype=torch.float32, device=dev)
+    sv1 = H.Saved.empty(N, M, P, dev)
+    Y1 = torch.empty(N, P, device=dev, dtype=tdt)
+    ws1 = H.workspace(H.WS_FWD, N, M, P, dev)
+    for b in range(B):
+        H.hq_linear_fwd(Q[b], K[b], Y1, sv1, k, ws1)
+        s_q[b:b + 1].copy_(sv1.amax[0:1] / 14.0)
+        s_k[b:b + 1].copy_(sv1.amax[1:2] / 14.0)
+    del sv1, Y1, ws1
+    T = torch.empty(B, N, P, device=dev, dtype=tdt)
+    dQ = torch.empty(B, N, M, device=dev, dtype=tdt)
+    dK = torch.empty(B, P, M, device=dev, dtype=tdt)
+    ds_q = torch.empty(B, dtype=torch.float32, device=dev)
+    ds_k = torch.empty(B, dtype=torch.float32, device=dev)
+    saved = H.bmm_saved_empty(B, N, M, P, dev)
+    lsq = H.BmmLSQ.empty(s_q, s_k, N, M, P)
+    ws = H.bmm_workspace(H.WS_BMM_BWD, B, N, M, P, dev)
+    adv = B * H.lss_philox_offset_advance(N, P)
+    off = [0]
+
+    def step():
+        H.hq_bmm_fwd_lsq(Q, K, T, saved, lsq, k)
+        H.lss_bmm_bwd_lsq(G, saved, lsq, dQ, dK, ds_q, ds_k, M, k, N, 0, off[0], ws)
+        off[0] += adv
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    H.timing_enable(True)
+    H.timing_read()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    log = H.timing_read(1 << 16)
+    H.timing_enable(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    ops_step = 6.0 * B * N * P * M
+    tops = ops_step / (ms_step * 1e-3) / 1e12
+    per = {}
+    for kid, ms in log:
+        c = per.setdefault(H.kernel_name(kid), [0, 0.0])
+        c[0] += 1
+        c[1] += ms
+    kernels = {nm: {"launches_per_step": c[0] / args.steps, "avg_us": 1e3 * c[1] / c[0],
+                    "us_per_step": 1e3 * c[1] / args.steps} for nm, c in per.items()}
+    dom = max(kernels, key=lambda x: kernels[x]["us_per_step"])
+    roof = None
+    if dom == "gemm_fwd":
+        algo = 2.0 * B * N * P * M
+        ach = algo / (kernels[dom]["avg_us"] * 1e-6) / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS,
+                "unit": "TFLOP/s", "frac": round(ach / INT8_PEAK_TOPS, 4), "traffic": None,
+                "algorithmic_ops_per_launch": algo}
+    bf16 = None
+    if not args.no_bf16:
+        Qb, Kb, Gb = (t.to(torch.bfloat16) for t in (Q, K, G))
+        KbT = Kb.transpose(1, 2).contiguous()
+        GbT = Gb.transpose(1, 2).contiguous()
+
+        def bstep():
+            torch.bmm(Qb, KbT)
+            torch.bmm(Gb, Kb)
+            torch.bmm(GbT, Qb)
+
+        for _ in range(args.warmup):
+            bstep()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            bstep()
+        torch.cuda.synchronize()
+        bms = (time.perf_counter() - t0) * 1e3 / args.steps
+        bf16 = {"ms_per_step": round(bms, 4), "tops": round(ops_step / (bms * 1e-3) / 1e12, 2),
+                "speedup_int4_over_bf16": round(bms / ms_step, 3)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline_bmm(np, synth, args.cpu_seconds)
+    out = {
+        "metric": BMM_METRIC, "value": round(tops, 2), "unit": "TOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "i8",
+        "data": "synthetic",
+        "config": {"workload": "BERT-base attention scores BMM (App. A.1)", "B": B, "N": N, "P": P,
+                   "M": M, "log2_block": k, "io_dtype": "f16", "budget": N,
+                   "quantizer": "lsq, per-batch steps (s = max|V H| / 14)"},
+        "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
+        "roofline": roof, "cpu_baseline": cpu, "bf16": bf16,
+        "kernels": {x: {kk: round(vv, 3) for kk, vv in v.items()} for x, v in sorted(kernels.items())},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_bmm(np, synth, target_s: float):
+    """The oracle, as it stands, on the first nb batches of the attention BMM (fwd + bwd)."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+
+    def run(nb):
+        Qh, Kh, Gh = (np.stack(a) for a in zip(*[bmm_inputs(np, synth, b) for b in range(nb)]))
+        t0 = time.perf_counter()
+        sq = np.array([O.absmax(O.fwht_rows(Qh[b], BMM_K)) / np.float32(14.0) for b in range(nb)])
+        sk = np.array([O.absmax(O.fwht_rows(Kh[b], BMM_K)) / np.float32(14.0) for b in range(nb)])
+        fw = O.bmm_lsq_forward(Qh, Kh, BMM_K, sq, sk)
+        O.bmm_lsq_backward(Gh, fw, BMM_N, 0, 0)
+        return time.perf_counter() - t0, 6.0 * nb * BMM_N * BMM_P * BMM_M
+
+    nb = 2
+    t, ops = run(nb)
+    for _ in range(3):
+        if t >= 0.7 * target_s or nb >= BMM_B:
+            break
+        nb = int(min(BMM_B, max(nb + 1, nb * target_s / max(t, 1e-3))))
+        t, ops = run(nb)
+    return {"value": round(ops / t / 1e12, 6), "unit": "TOPS", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {nb} of {BMM_B} batches, fwd + bwd (budget = {BMM_N}); {t:.1f} s",
+            "seconds": round(t, 2)}
 
 
 def cpu_baseline(lins, target_s: float, lsq_mode: bool = False):

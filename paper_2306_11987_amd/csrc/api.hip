@@ -265,7 +265,7 @@ struct BmmWs {
   int64_t tiles_dx, tiles_dw;
 };
 BmmWs bmm_ws_dims(int64_t B, int64_t N, int64_t M, int64_t P) {
-  return {B > kQMaxWg ? B : kQMaxWg, rup(N, kPad), gemm_epi_parts(N, M, 1), gemm_epi_parts(P, M, 1)};
+  return {B + kBatchWgSlack, rup(N, kPad), gemm_epi_parts(N, M, 1), gemm_epi_parts(P, M, 1)};
 }
 size_t bmm_bwd_bytes(int64_t B, int64_t N, int64_t M, int64_t P, bool dq, bool dk) {
   const BmmWs d = bmm_ws_dims(B, N, M, P);

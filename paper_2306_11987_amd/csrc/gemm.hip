@@ -49,6 +49,7 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kBN = 256;  // workgroup tile width (n)
+constexpr int kNarrowBN = 64;  // tile width of the gradient GEMMs for outputs <= 64 wide
 constexpr int kKS = 128;  // K elements per stage
 #ifndef HQLSS_GEMM_FWD_BM
 #define HQLSS_GEMM_FWD_BM 128
@@ -58,9 +59,9 @@ constexpr int kKS = 128;  // K elements per stage
 #endif
 template <bool A4> constexpr int tile_m() { return A4 ? HQLSS_GEMM_FWD_BM : HQLSS_GEMM_GRAD_BM; }
 
-template <int BM, bool A4, int WN_ = 128>
+template <int BM, bool A4, int WN_ = 128, int BN_ = kBN>
 struct Cfg {
-  static constexpr int BN = kBN;
+  static constexpr int BN = BN_;
   static constexpr int WAVES = BM / 32, THREADS = 64 * WAVES;
   static constexpr int WN = WN_, WGN = BN / WN, WGM = WAVES / WGN;
   static constexpr int WM = BM / WGM, TI = WM / 32, TJ = WN / 32;
@@ -205,9 +206,9 @@ __device__ __forceinline__ double block_sum_f64(double v, double* red) {
   return t;
 }
 
-template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B>
-__global__ __launch_bounds__((Cfg<BM, A4, WN>::THREADS), (Cfg<BM, A4, WN>::OCC)) void gemm_kernel(GemmArgs g) {
-  using C_ = Cfg<BM, A4, WN>;
+template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B, int BN_>
+__global__ __launch_bounds__((Cfg<BM, A4, WN, BN_>::THREADS), (Cfg<BM, A4, WN, BN_>::OCC)) void gemm_kernel(GemmArgs g) {
+  using C_ = Cfg<BM, A4, WN, BN_>;
   constexpr int TI = C_::TI, TJ = C_::TJ, BN = C_::BN;
   constexpr bool RAW = (EPI == kEpiAcc || EPI == kEpiPartial);
   constexpr bool LSQ = (EPI == kEpiDxL || EPI == kEpiDwL);
@@ -711,15 +712,17 @@ int64_t reduce_grid(int64_t M, int64_t N) {
   return wg < 1 ? 1 : wg;
 }
 
-template <int BM, bool A4, int EPI, int DT, int LOG2B>
+// BN_: workgroup tile width; kNarrowBN for outputs at most that wide (attention head
+// dimensions), which would otherwise leave most of a 256-wide tile idle
+template <int BM, bool A4, int EPI, int DT, int LOG2B, int BN_ = kBN>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
-  constexpr int WN = wave_n<A4, LOG2B>();
-  using C_ = Cfg<BM, A4, WN>;
+  constexpr int WN = wave_n<A4, LOG2B>() < BN_ ? wave_n<A4, LOG2B>() : BN_;
+  using C_ = Cfg<BM, A4, WN, BN_>;
   // one workgroup per tile of the M x N output (M the host-side bound; see tile_of)
-  dim3 grid((unsigned)(((g.N + kBN - 1) / kBN) * ((g.M + BM - 1) / BM)), 1u,
+  dim3 grid((unsigned)(((g.N + BN_ - 1) / BN_) * ((g.M + BM - 1) / BM)), 1u,
             (unsigned)(g.batch > 0 ? g.batch : splits));
   timing_begin(s);
-  gemm_kernel<BM, A4, WN, EPI, DT, LOG2B><<<grid, C_::THREADS, 0, s>>>(g);
+  gemm_kernel<BM, A4, WN, EPI, DT, LOG2B, BN_><<<grid, C_::THREADS, 0, s>>>(g);
   timing_end(s, id);
   return hipGetLastError();
 }
@@ -728,6 +731,18 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
 template <int BM, bool A4, int EPI, int DT>
 hipError_t gemm_b(hipStream_t s, const GemmArgs& g, int splits, int id) {
   if constexpr (EPI == kEpiDx || EPI == kEpiDw || EPI == kEpiDxL || EPI == kEpiDwL) {
+    if (splits <= 1 && g.N <= kNarrowBN) {  // narrow output: blocks of at most 64 columns
+      switch (g.log2b) {
+        case 0: return gemm_t<BM, A4, EPI, DT, 0, kNarrowBN>(s, g, splits, id);
+        case 1: return gemm_t<BM, A4, EPI, DT, 1, kNarrowBN>(s, g, splits, id);
+        case 2: return gemm_t<BM, A4, EPI, DT, 2, kNarrowBN>(s, g, splits, id);
+        case 3: return gemm_t<BM, A4, EPI, DT, 3, kNarrowBN>(s, g, splits, id);
+        case 4: return gemm_t<BM, A4, EPI, DT, 4, kNarrowBN>(s, g, splits, id);
+        case 5: return gemm_t<BM, A4, EPI, DT, 5, kNarrowBN>(s, g, splits, id);
+        case 6: return gemm_t<BM, A4, EPI, DT, 6, kNarrowBN>(s, g, splits, id);
+      }
+      return hipErrorInvalidValue;
+    }
     switch (g.log2b) {
       case 0: return gemm_t<BM, A4, EPI, DT, 0>(s, g, splits, id);
       case 1: return gemm_t<BM, A4, EPI, DT, 1>(s, g, splits, id);
@@ -817,7 +832,8 @@ hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4,
 int64_t gemm_epi_parts(int64_t M, int64_t N, int splits) {
   if (splits <= 1) {
     const int64_t bm = tile_m<false>();
-    return ((N + kBN - 1) / kBN) * ((M + bm - 1) / bm);
+    const int64_t bn = N <= kNarrowBN ? kNarrowBN : kBN;  // as gemm_b chooses
+    return ((N + bn - 1) / bn) * ((M + bm - 1) / bm);
   }
   return reduce_grid(M, N);
 }

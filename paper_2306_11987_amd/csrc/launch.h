@@ -26,6 +26,8 @@ hipError_t launch_copy(hipStream_t s, const void* src, void* dst, int64_t bytes)
 // `batch` such tensors, `bstride` elements apart; `wg` is then per batch, and every
 // per-tensor output (codes, row sums, maxima, partials, ...) is one block per batch.
 constexpr int kQMaxWg = 1024;  // workgroups (= partial results) of one unbatched job at most
+// a batched job has at most kBatchWgSlack + batch workgroups in all (ceil(2 kQMaxWg / B) per batch)
+constexpr int kBatchWgSlack = 2 * kQMaxWg;
 struct QJob {
   const void* src;
   int64_t rows, cols;

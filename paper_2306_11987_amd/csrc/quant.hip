@@ -781,11 +781,15 @@ void fit_grid(QJob& a, QJob& b, int cap) {
     b.wg = (int)nb;
     return;
   }
-  if (a.batch > 1 || b.batch > 1) {  // batched: share the grid by size, then per batch
+  if (a.batch > 1 || b.batch > 1) {
+    // batched: about two resident rounds shared by size, then per batch (many small
+    // batches would otherwise get one workgroup each and leave the CUs half occupied);
+    // at most kBatchWgSlack + batch workgroups per job in all (the partials bound)
     const double sa = (double)a.rows * a.cols * a.batch, sb = (double)b.rows * b.cols * b.batch;
-    const int64_t ca = nb ? (int64_t)(cap * sa / (sa + sb)) : cap, cb = cap - ca;
+    const int64_t c2 = 2 * (int64_t)cap;
+    const int64_t ca = nb ? (int64_t)(c2 * sa / (sa + sb)) : c2, cb = c2 - ca;
     auto per = [](int64_t c, int64_t n, int64_t batch) {
-      int64_t w = c / batch;
+      int64_t w = (c + batch - 1) / batch;
       if (w > n) w = n;
       return (int)(w < 1 ? 1 : w);
     };
