@@ -229,6 +229,30 @@ def main():
                 "algorithmic_ops_per_launch": algo,
                 "note": "int8 MFMA ops (multiply-adds x 2) of the kept-token GEMM"}
 
+    # ---- memory-bound kernels against the HBM peak: algorithmic bytes of one step (every
+    # tensor read once and every result written once) over the kernel's time per step
+    ab = {}
+    eb = {"f16": 2, "bf16": 2, "f32": 4}[lins[0].dtype]
+    for e, kt in zip(L, kept):
+        N_, D_, C_ = e["lin"].N, e["lin"].D, e["lin"].C
+        if lsq_mode:  # one read, codes + fp16 deltas written, row sums of X
+            ab["lsq_quant"] = ab.get("lsq_quant", 0.0) + (eb + 2.5) * (N_ + C_) * D_ + 4 * N_
+        else:  # the maximum pass reads X and W; the quantiser reads them again, writes codes
+            ab["fwht_absmax"] = ab.get("fwht_absmax", 0.0) + eb * (N_ + C_) * D_
+            ab["fwht_quant"] = ab.get("fwht_quant", 0.0) + (eb + 0.5) * (N_ + C_) * D_ + 4 * N_
+        ab["fwht_absmax"] = ab.get("fwht_absmax", 0.0) + eb * N_ * C_  # maximum of dY
+        ab["transpose_packed"] = ab.get("transpose_packed", 0.0) + 1.0 * C_ * D_
+        # dY read; two INT4 code planes written; row sums and the two scores per token
+        ab["bit_split"] = ab.get("bit_split", 0.0) + (eb + 1.0) * N_ * C_ + 20 * N_
+        # codes of the kept rows read, A and A^T written; gathered X codes read and written
+        ab["build_operands"] = ab.get("build_operands", 0.0) + 3.0 * kt * C_ + 1.0 * kt * D_
+    hbm = {}
+    for nm, b in ab.items():
+        if nm in kernels:
+            gbs = b / (kernels[nm]["us_per_step"] * 1e-6) / 1e9
+            hbm[nm] = {"algorithmic_MB_per_step": round(b / 1e6, 2), "achieved_GBps": round(gbs, 1),
+                       "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
     # ---- bf16 reference: the same three GEMMs per linear through torch (hipBLASLt)
     bf16 = None
     if not args.no_bf16:
@@ -280,6 +304,7 @@ def main():
         "ms_per_step_with_kernel_events": round(ms_step_events, 4),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "hbm_kernels": hbm,
         "bf16": bf16,
         "kernels": {k: {kk: round(vv, 3) for kk, vv in v.items()} for k, v in sorted(kernels.items())},
     }
