@@ -1,8 +1,9 @@
 // Leverage-score sampling of the bit-split gradient rows and the GEMM operands it
 // selects (gfx950).
 //
-// lss_plan (one workgroup of 1024 threads).  Its inputs are the integer leverage scores
-// of the 2N stacked rows, formed by the bit-split kernel (Sec. 4.2: with the common factor
+// lss_plan (one workgroup per problem: 1024 threads, 256 for N <= 4096).  Its inputs are
+// the integer leverage scores of the 2N stacked rows, formed by the bit-split kernel
+// (Sec. 4.2: with the common factor
 // s_dn s_x dropped, c^2 = w^2 sum q^2 x_sumsq, w = 14 for the upper row of a token and 1
 // for the lower one, c = isqrt(c^2 2^16)), and that kernel's per-workgroup totals:
 //   1. inclusion probabilities by the clamp-and-rescale loop of App. A.2 with sum p = B,
@@ -31,26 +32,30 @@ namespace hqlss {
 
 namespace {
 
+// Workgroup sizes of the sampler: 1024 threads, or 256 for short sequences (N <= 4096),
+// where four samplers then share a CU (a batched call runs one per batch).  The result
+// does not depend on the size: counters are per 8 tokens and every sum is exact.
 constexpr int kPlanThreads = 1024;
-constexpr int kPlanWaves = kPlanThreads / kWave;
+constexpr int kPlanThreadsSmall = 256;
 
-constexpr int kPlanRegs = 32;  // scores per thread kept in registers (2N <= 32768)
+constexpr int kPlanRegs = 32;  // scores per thread kept in registers (2N <= 32 x threads)
 
-// two block-wide sums with one pair of barriers (red holds 2 kPlanWaves words)
+// two block-wide sums with one pair of barriers (red holds 2 WAVES words)
+template <int WAVES>
 __device__ __forceinline__ void block_sum2_u64(uint64_t& a, uint64_t& b, uint64_t* red) {
   a = wave_sum_u64(a);
   b = wave_sum_u64(b);
   if ((threadIdx.x & 63) == 0) {
     red[threadIdx.x >> 6] = a;
-    red[kPlanWaves + (threadIdx.x >> 6)] = b;
+    red[WAVES + (threadIdx.x >> 6)] = b;
   }
   __syncthreads();
   a = 0;
   b = 0;
 #pragma unroll
-  for (int i = 0; i < kPlanWaves; ++i) {
+  for (int i = 0; i < WAVES; ++i) {
     a += red[i];
-    b += red[kPlanWaves + i];
+    b += red[WAVES + i];
   }
   __syncthreads();
 }
@@ -67,11 +72,13 @@ __device__ __forceinline__ void load8u(const uint32_t* p, int t0, int n8, uint32
   }
 }
 
+template <int kPlanThreads>
 __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     const int32_t* __restrict__ sumsq_up, const uint32_t* __restrict__ scores, int64_t pitch,
     const uint4* __restrict__ parts, int nparts, int N, int64_t B, uint64_t seed,
     uint64_t offset, uint8_t* __restrict__ w_up, uint8_t* __restrict__ w_dn,
     int32_t* __restrict__ kept, int32_t* __restrict__ n_kept, uint64_t offset_stride) {
+  constexpr int kPlanWaves = kPlanThreads / kWave;
   __shared__ uint64_t red[2 * kPlanWaves];
   __shared__ int wtot[kPlanWaves];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -94,7 +101,7 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     nz += p.x;
     st += ((uint64_t)p.z << 32) | p.y;
   }
-  block_sum2_u64(nz, st, red);
+  block_sum2_u64<kPlanWaves>(nz, st, red);
   const uint64_t S_all = st;
   const bool all_nonzero_kept = (int64_t)nz <= B;
 
@@ -127,7 +134,7 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
           if (c && (uint64_t)R * c >= S) { ++cnt; sum += c; }
         }
       }
-      block_sum2_u64(cnt, sum, red);
+      block_sum2_u64<kPlanWaves>(cnt, sum, red);
       if ((int64_t)cnt == k) break;  // nothing newly clamped
       k = (int64_t)cnt;
       S = S_all - sum;
@@ -352,9 +359,14 @@ hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_
                            uint8_t* w_dn, int32_t* kept, int32_t* n_kept, int64_t batch,
                            uint64_t offset_stride) {
   timing_begin(s);
-  lss_plan_kernel<<<(unsigned)batch, kPlanThreads, 0, s>>>(sumsq_up, scores, score_pitch, parts,
-                                                           nparts, (int)N, budget, seed, offset,
-                                                           w_up, w_dn, kept, n_kept, offset_stride);
+  if (N <= 16 * kPlanThreadsSmall)
+    lss_plan_kernel<kPlanThreadsSmall><<<(unsigned)batch, kPlanThreadsSmall, 0, s>>>(
+        sumsq_up, scores, score_pitch, parts, nparts, (int)N, budget, seed, offset, w_up, w_dn,
+        kept, n_kept, offset_stride);
+  else
+    lss_plan_kernel<kPlanThreads><<<(unsigned)batch, kPlanThreads, 0, s>>>(
+        sumsq_up, scores, score_pitch, parts, nparts, (int)N, budget, seed, offset, w_up, w_dn,
+        kept, n_kept, offset_stride);
   timing_end(s, kKPlan);
   return hipGetLastError();
 }
