@@ -401,6 +401,33 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_>::THREADS), (Cfg<BM, A4, WN, B
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // up to 1 LDS read
     }
   };
+#ifndef HQLSS_LSQ_PREFETCH
+#define HQLSS_LSQ_PREFETCH 1
+#endif
+  // Learned-step epilogues read this tile's deltas (2 B per output) after the main loop.
+  // The deltas are fetched into the caches during the main loop by LDS-DMA loads into a
+  // 1 KB sink (no registers held): each lane touches one 128-byte line of one row.
+  constexpr bool PREFETCH = LSQ && HQLSS_LSQ_PREFETCH;
+  // with two stage buffers every stage wait drains all loads, the prefetch included
+  static_assert(!PREFETCH || C_::NBUF == 2, "partial stage waits would not count the prefetch");
+  __shared__ __attribute__((aligned(1024))) uint8_t pf_sink[PREFETCH ? 1024 : 16];
+  int pf_row[2] = {0, 0};
+  if constexpr (PREFETCH) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      int64_t gm = m0 + (wid * 2 + x) * 16 + (lane >> 2);
+      gm = gm < M ? gm : M - 1;
+      pf_row[x] = ROWMAP ? g.out_rows[gm] : (int)gm;
+    }
+  }
+  auto prefetch_delta = [&]() {
+    if constexpr (PREFETCH) {
+      int64_t col = n0 + (int64_t)(lane & 3) * 64;  // one 128-byte line of fp16
+      col = col < g.N ? col : n0;
+#pragma unroll
+      for (int x = 0; x < 2; ++x) dma16(g.delta + (int64_t)pf_row[x] * g.ldo + col, pf_sink);
+    }
+  };
   auto stage_ready = [&](int st) {  // this wave's loads of stage st landed, then all waves'
     // loads of later stages may stay in flight: min(NBUF - 2, nst - 1 - st) of them
     const int later = nst - 1 - st;
@@ -409,6 +436,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_>::THREADS), (Cfg<BM, A4, WN, B
     else wait_vm_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
     if (st + C_::NBUF - 1 < nst) issue(st + C_::NBUF - 1);
+    if (st == 0) prefetch_delta();
   };
 #pragma unroll
   for (int p = 0; p < C_::NBUF - 1; ++p)
