@@ -166,3 +166,70 @@ def test_binding_rejects_cpu_tensors():
     sv = H.Saved(*(torch.zeros(2) for _ in range(5)))
     with pytest.raises(ValueError):
         H.hq_linear_fwd(X, X, X, sv, 5)
+
+
+_Lsq = H._binding._LsqC
+_BmmLsq = H._binding._BmmLsqC
+
+
+def fwd_lsq(N=128, D=256, C=256, k=5, lsq=None, saved=None, X=FAKE):
+    s = saved if saved is not None else _saved(amax=None)  # amax is not used by this mode
+    lq = lsq if lsq is not None else _Lsq(FAKE, FAKE, FAKE)
+    return lib.hq_linear_fwd_lsq(X, FAKE, FAKE, N, D, C, 0, k, ctypes.byref(s), ctypes.byref(lq),
+                                 FAKE, 1 << 40, None)
+
+
+def bwd_lsq(dX=FAKE, dW=FAKE, lsq=None, budget=0, nbytes=1 << 40, N=128):
+    lq = lsq if lsq is not None else _Lsq(FAKE, FAKE, FAKE)
+    return lib.lss_linear_bwd_lsq(FAKE, ctypes.byref(_saved(amax=None)), ctypes.byref(lq), dX, dW, FAKE,
+                                  N, 256, 256, 0, 5, budget, 0, 0, FAKE, nbytes, None)
+
+
+def test_lsq_argument_errors():
+    assert fwd_lsq(X=None) == NULL
+    assert fwd_lsq(lsq=_Lsq(None, FAKE, FAKE)) == NULL
+    assert fwd_lsq(lsq=_Lsq(FAKE, FAKE, None)) == NULL
+    assert fwd_lsq(lsq=_Lsq(FAKE + 2, FAKE, FAKE)) == ALIGN  # steps need 4-byte alignment
+    assert fwd_lsq(lsq=_Lsq(FAKE, FAKE + 8, FAKE)) == ALIGN
+    assert fwd_lsq(saved=_saved(amax=None, xq=None)) == NULL
+    assert fwd_lsq(N=0) == SHAPE
+    assert fwd_lsq(k=8) == BLOCK
+    assert bwd_lsq(dX=None, dW=None) == NULL
+    assert bwd_lsq(dW=None, lsq=_Lsq(FAKE, None, FAKE)) == NULL  # dX reads delta_x
+    assert bwd_lsq(budget=1000) == ARG
+    assert bwd_lsq(nbytes=64) == WS
+    assert bwd_lsq(N=70000) == SHAPE
+
+
+def bmm_fwd(B=2, N=128, M=64, P=128, k=5, lsq=None, Q=FAKE):
+    lq = lsq if lsq is not None else _BmmLsq(FAKE, FAKE, FAKE, FAKE)
+    return lib.hq_bmm_fwd_lsq(Q, FAKE, FAKE, B, N, M, P, 0, k, ctypes.byref(_saved(amax=None)),
+                              ctypes.byref(lq), None, 0, None)
+
+
+def bmm_bwd(B=2, N=128, M=64, P=128, k=5, dQ=FAKE, dK=FAKE, nbytes=1 << 40, budget=0):
+    lq = _BmmLsq(FAKE, FAKE, FAKE, FAKE)
+    return lib.lss_bmm_bwd_lsq(FAKE, ctypes.byref(_saved(amax=None)), ctypes.byref(lq), dQ, dK, FAKE, FAKE,
+                               B, N, M, P, 0, k, budget, 0, 0, FAKE, nbytes, None)
+
+
+def test_bmm_argument_errors():
+    assert bmm_fwd(Q=None) == NULL
+    assert bmm_fwd(lsq=_BmmLsq(FAKE, None, FAKE, FAKE)) == NULL
+    assert bmm_fwd(B=0) == SHAPE
+    assert bmm_fwd(B=70000) == SHAPE  # grid z limit
+    assert bmm_fwd(B=1 << 14, N=1 << 17) == SHAPE  # B N > 2^30
+    assert bmm_fwd(M=96) == SHAPE
+    assert bmm_fwd(k=7) == BLOCK  # M = 64 < 128
+    assert bmm_bwd(dQ=None, dK=None) == NULL
+    assert bmm_bwd(nbytes=1024) == WS
+    assert bmm_bwd(budget=257) == ARG  # budget > 2N
+    assert bmm_bwd(N=70000, B=2) == SHAPE
+
+
+def test_bmm_workspace_sizes():
+    a = H.bmm_workspace_bytes(H.WS_BMM_BWD, 2, 128, 64, 128)
+    b = H.bmm_workspace_bytes(H.WS_BMM_BWD, 384, 512, 64, 512)
+    assert 0 < a < b
+    assert H.bmm_workspace_bytes(H.WS_BMM_FWD, 384, 512, 64, 512) == 0
+    assert H.bmm_workspace_bytes(H.WS_BMM_BWD, 0, 512, 64, 512) == 0
