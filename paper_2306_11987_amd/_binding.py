@@ -351,6 +351,8 @@ def lss_linear_bwd(dY: torch.Tensor, saved: Saved, dX: Optional[torch.Tensor], d
                    D: int, log2_block: int, budget: int = 0, seed: int = 0, offset: int = 0,
                    ws: Optional[torch.Tensor] = None) -> None:
     N, C = dY.shape
+    if ws is None:
+        ws = workspace(WS_BWD, N, D, C, dY.device)
     p, n = _ws(ws)
     sv = saved.c()
     _check(lib.lss_linear_bwd(_ptr(dY), ctypes.byref(sv), _ptr(dX), _ptr(dW), N, int(D), C, _dt(dY),
@@ -362,6 +364,8 @@ def lss_linear_bwd_dx(dY: torch.Tensor, saved: Saved, dX: torch.Tensor, log2_blo
                       seed: int = 0, offset: int = 0, ws: Optional[torch.Tensor] = None) -> None:
     N, C = dY.shape
     D = dX.shape[1]
+    if ws is None:
+        ws = workspace(WS_BWD_DX, N, D, C, dY.device)
     p, n = _ws(ws)
     sv = saved.c()
     _check(lib.lss_linear_bwd_dx(_ptr(dY), ctypes.byref(sv), _ptr(dX), N, D, C, _dt(dY), int(log2_block),
@@ -372,6 +376,8 @@ def lss_linear_bwd_dw(dY: torch.Tensor, saved: Saved, dW: torch.Tensor, log2_blo
                       seed: int = 0, offset: int = 0, ws: Optional[torch.Tensor] = None) -> None:
     N, C = dY.shape
     D = dW.shape[1]
+    if ws is None:
+        ws = workspace(WS_BWD_DW, N, D, C, dY.device)
     p, n = _ws(ws)
     sv = saved.c()
     _check(lib.lss_linear_bwd_dw(_ptr(dY), ctypes.byref(sv), _ptr(dW), N, D, C, _dt(dY), int(log2_block),
