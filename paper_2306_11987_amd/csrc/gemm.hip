@@ -17,16 +17,18 @@
 // and as the reduction over k is order-free the product is exact.  The factor 16 per INT4
 // operand is a power of two, removed by an arithmetic shift (or folded into the scale).
 //
-// Tiling.  Workgroup tile BM x 256 with waves of 64 x 128 (2 x 4 MFMA tiles of 32 x 32,
-// 128 accumulators in AGPRs): BM = 256 runs 8 waves and one workgroup per CU, BM = 128
-// runs 4 waves and two workgroups per CU.  Either way every SIMD holds two waves, so one
-// wave's LDS reads, INT4 widening and epilogue overlap the other's MFMAs.  The MFMA "A"
-// operand carries the n rows and the "B" operand the m rows, so that a lane's accumulators
-// run along n: lane l, MFMA tile (i, j), register r holds m = 32 i + (l % 32) and
-// n = 16 j + r + 64 (l / 32) of the wave tile.  This is arranged by the order in which the
-// B rows are placed in LDS.  Each lane then owns 16 consecutive n per (i, j), and the
-// gradient epilogue's Hadamard transform along n runs in registers for blocks up to 64
-// and pairs lanes l and l ^ 32 for the stride 64.
+// Tiling.  Workgroup tile BM x 256 (BM = 128: 4 waves, two workgroups per CU, so every
+// SIMD holds two waves and one wave's LDS reads, INT4 widening and epilogue overlap the
+// other's MFMAs).  The forward (INT4 x INT4) uses wave tiles of 64 x 128; the gradient
+// GEMMs (int8 x INT4) use 128 x 64, as only their n-side operand is widened, or 64 x 128
+// for Hadamard blocks of 64 and 128; outputs at most 64 columns wide (attention head
+// dimensions) use 64-wide workgroup tiles.  128 int32 accumulators per lane.  The MFMA
+// "A" operand carries the n rows and the "B" operand the m rows, so that a lane's
+// accumulators run along n: lane l, MFMA tile (i, j), register r holds m = 32 i + (l % 32)
+// and n = 16 j + r + (WN / 2) (l / 32) of the wave tile.  This is arranged by the order in
+// which the B rows are placed in LDS.  Each lane then owns 16 consecutive n per (i, j),
+// and the gradient epilogue's Hadamard transform along n runs in registers, pairing lanes
+// l and l ^ 32 for the widest stride.
 //
 // Main loop.  K advances in stages of 128; operands move from HBM/L2 straight into LDS
 // with 16-byte LDS-DMA loads (no register staging), NBUF stages deep, so each stage's
@@ -35,8 +37,11 @@
 // (32 rows x one chunk per instruction) hit distinct banks.  A stage boundary is one
 // wait on this wave's own loads plus one barrier.
 // Epilogue: results are staged through LDS in row chunks so that each store instruction
-// writes contiguous 16-byte pieces of whole output rows.  Split-K (gridDim.z > 1) writes
-// int32 partial tiles the same way, and reduce_epilogue sums them.
+// writes contiguous 16-byte pieces of whole output rows.  The learned-step gradient
+// epilogues first sum acc * delta (fp64) and zero the clipped accumulators (App. A.4).
+// Grid z is either the split-K index (int32 partial tiles, summed by reduce_epilogue) or
+// the batch of a batched launch (per-batch operand and output strides).  Workgroups take
+// tiles in an XCD-aware order over the tiles with rows below the device-side row count.
 #include "common.h"
 #include "launch.h"
 

@@ -5,6 +5,8 @@
 //    fp32), then per-tensor absmax and INT4 codes clamp(rint(v * fl(7/a)), -7, 7)
 //    (Sec. 3.1, Eq. 2), packed two per byte (App. A.6) with per-row sums of squares
 //    (the ||X_i|| factor of the leverage score, Sec. 4.2).  One launch serves X and W.
+//  * fwht_lsq: the same transform quantised at a caller-given (learned) step in one pass,
+//    with the fp16 deltas q - I r that the learned-step backward needs (Eq. 2, App. A.4).
 //  * bit_split: bit splitting of the output gradient (Sec. 4.2, Eq. 4): upper codes by
 //    round-to-nearest at s_up = a/7, lower codes by stochastic rounding of 14 x the exact
 //    residual (s_dn = s_up / 14), Philox stream 0.  It also forms the integer leverage
@@ -19,6 +21,8 @@
 // every admitted shape), so strides 1..8 run in registers and strides 16..64 are lane
 // exchanges folded into the butterfly add (DPP) or a swizzle.  Per-tensor maxima leave
 // each workgroup as one plain store of a partial; consumers reduce the partials.
+// A batched job (the attention BMM) holds many equal tensors; its workgroups are split
+// evenly over the batches and every per-tensor output is one block per batch.
 //
 // These kernels are bound by vector-ALU issue as much as by HBM, so the per-element work
 // is kept to a handful of instructions: codes come from the magic-number form of
