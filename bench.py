@@ -199,6 +199,19 @@ def main():
     kernels = {nm: {"launches_per_step": c[0] / args.steps, "avg_us": 1e3 * c[1] / c[0],
                     "us_per_step": 1e3 * c[1] / args.steps} for nm, c in per.items()}
 
+    # forward and backward time per step: the log is in launch order, and each step
+    # launches the forwards of all linears (4 kernels each) before the backwards
+    per_step = len(log) // args.steps
+    n_fwd = 4 * len(L)
+    fwd_us = bwd_us = 0.0
+    if per_step * args.steps == len(log) and per_step > n_fwd:
+        for st in range(args.steps):
+            chunk = log[st * per_step:(st + 1) * per_step]
+            fwd_us += 1e3 * sum(ms for _, ms in chunk[:n_fwd])
+            bwd_us += 1e3 * sum(ms for _, ms in chunk[n_fwd:])
+        fwd_us /= args.steps
+        bwd_us /= args.steps
+
     # kept tokens of the timed steps (replayed plans; needed for algorithmic GEMM ops)
     kept = []
     for i, e in enumerate(L):
@@ -302,6 +315,7 @@ def main():
                    "kept_tokens": [round(k, 1) for k in kept]},
         "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
         "ms_per_step_with_kernel_events": round(ms_step_events, 4),
+        "us_per_step_fwd_bwd": [round(fwd_us, 1), round(bwd_us, 1)],
         "roofline": roof,
         "cpu_baseline": cpu,
         "hbm_kernels": hbm,
