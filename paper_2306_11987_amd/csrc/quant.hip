@@ -414,6 +414,8 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
   const float a = reduce_parts(part + (int64_t)b * nparts, nparts);
   if (wg == 0 && threadIdx.x == 0) o.amax_out[b] = a;
   const float inv = a > 0.f ? 7.0f / a : 0.f;
+  // -0.0f, from an argument so that the fma below is not folded into a multiply
+  const float nzero = __uint_as_float(0x80000000u | (uint32_t)((uint64_t)j.cols >> 63));
   const Geo g(j, wg);
   const int64_t C = j.cols;
   constexpr int EB = Elem<DT>::bytes;
@@ -449,10 +451,14 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
           const U4 rnd = philox_block(seed, offset, 0u, (uint64_t)(r * C + col + 8 * h));
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float x = v[u][8 * h + e] * inv;
+            // fl(v inv): one rounding, so the fma with a -0 addend equals the product
+            // (an fp16 operand widens inside the instruction)
+            const float x = __builtin_fmaf(v[u][8 * h + e], inv, nzero);
             const uint32_t bu = rne_bits(x);                  // |x| <= 7 (1 + 2^-23)
-            const float up = __uint_as_float(bu) - kRne;      // rint(x), exact
-            const float w = 14.0f * (x - up);                 // residual exact; |w| <= 7
+            // -14 rint(x) exactly from the bits 1.5 * 2^23 + rint(x); then
+            // fl(14 x - 14 rint(x)) = fl(14 (x - rint(x))), the residual being exact
+            const float m14 = __builtin_fmaf(__uint_as_float(bu), -14.0f, 14.0f * kRne);
+            const float w = __builtin_fmaf(x, 14.0f, m14);   // |w| <= 7
             const float fl = floorf(w);
             const float thr = (w - fl) * 65536.0f;
             const uint32_t bd = __float_as_uint(fl + kRne);   // floor(w) in the low bits
