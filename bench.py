@@ -21,6 +21,10 @@ App. A.4 gradients including the step-size gradients), on the same workload with
 before timing to half of each tensor's dynamic step (s = max|V H| / 14, so the largest
 entries clip).
 
+--workload 2, 3 or 4 runs the same step on the other linear-layer workloads instead
+(GPT-2-medium linears N = 8192; the GEMM sweep N = 16384 up to 11008 wide, bf16; the
+BERT-large encoder block linears).
+
 Prints ONE JSON line.
 """
 from __future__ import annotations
@@ -39,7 +43,8 @@ sys.path.insert(0, ROOT)
 INT8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
 HBM_PEAK_GBS = 8000.0
 METRIC = "INT4 linear fwd+bwd effective TOPS (fraction of int8-MFMA peak) vs bf16"
-CFG_ID = 1  # BERT-base FFN pair
+# workloads: id -> key of the committed counter summaries under profiles/
+WORKLOAD_KEYS = {1: "bert_base_ffn", 2: "gpt2_medium", 3: "gemm_sweep", 4: "bert_large_block"}
 
 
 def parse():
@@ -52,6 +57,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time")
     p.add_argument("--mode", choices=("dynamic", "lsq", "bmm"), default="dynamic",
                    help="quantiser: per-tensor maxima (default) or learned step sizes")
+    p.add_argument("--workload", type=int, choices=sorted(WORKLOAD_KEYS), default=1,
+                   help="1: BERT-base FFN pair (default); 2: GPT-2-medium linears; "
+                        "3: GEMM sweep N=16384 (4096..11008, bf16); 4: BERT-large encoder block linears")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="before the steps, run the library's plain copy kernel once over MIB MiB "
                         "(reference for hardware traffic counters)")
@@ -97,7 +105,8 @@ def main():
     dev = torch.device("cuda:0")
     if args.mode == "bmm":
         return main_bmm(args, np, torch, H, synth, dev)
-    wl = synth.workload(CFG_ID)
+    cfg_id = args.workload
+    wl = synth.workload(cfg_id)
     lins = wl.linears
     N = lins[0].N
     tdt = {"f16": torch.float16, "bf16": torch.bfloat16, "f32": torch.float32}[lins[0].dtype]
@@ -105,7 +114,7 @@ def main():
     # ---- inputs resident in HBM, state and workspaces preallocated
     L = []
     for li, lin in enumerate(lins):
-        X, W, G = synth.linear_inputs(lin, CFG_ID, li)
+        X, W, G = synth.linear_inputs(lin, cfg_id, li)
         e = dict(lin=lin,
                  X=torch.from_numpy(X).to(dev, tdt), W=torch.from_numpy(W).to(dev, tdt),
                  G=torch.from_numpy(G).to(dev, tdt),
@@ -133,13 +142,15 @@ def main():
             e["wsf"] = H.workspace(H.WS_FWD_LSQ, lin.N, lin.D, lin.C, dev)
         torch.cuda.synchronize()
 
-    def step():
+    def fwd():
         for e in L:
             if lsq_mode:
                 H.hq_linear_fwd_lsq(e["X"], e["W"], e["Y"], e["saved"], e["lsq"], e["lin"].log2_block,
                                     e["wsf"])
             else:
                 H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
+
+    def bwd():
         for i in reversed(range(len(L))):
             e = L[i]
             lin = e["lin"]
@@ -150,6 +161,10 @@ def main():
                 H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block,
                                  lin.budget, seed, offsets[i], e["ws"])
             offsets[i] += e["adv"]
+
+    def step():
+        fwd()
+        bwd()
 
     if args.copy_calibration > 0:
         nb = args.copy_calibration << 20
@@ -163,6 +178,13 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # launches of the forwards of one step (splits the per-launch log into fwd and bwd)
+    H.timing_enable(True)
+    H.timing_read()  # clear
+    fwd()
+    torch.cuda.synchronize()
+    n_fwd = len(H.timing_read(1 << 16))
+    H.timing_enable(False)
     step_offsets = list(offsets)
     H.timing_enable(True)
     H.timing_read()  # clear
@@ -200,9 +222,8 @@ def main():
                     "us_per_step": 1e3 * c[1] / args.steps} for nm, c in per.items()}
 
     # forward and backward time per step: the log is in launch order, and each step
-    # launches the forwards of all linears (4 kernels each) before the backwards
+    # launches the forwards of all linears (n_fwd kernels) before the backwards
     per_step = len(log) // args.steps
-    n_fwd = 4 * len(L)
     fwd_us = bwd_us = 0.0
     if per_step * args.steps == len(log) and per_step > n_fwd:
         for st in range(args.steps):
@@ -238,7 +259,7 @@ def main():
         ach = algo / (kernels[dom]["avg_us"] * 1e-6) / 1e12
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS,
                 "unit": "TFLOP/s", "frac": round(ach / INT8_PEAK_TOPS, 4),
-                "traffic": committed_traffic(dom, "bert_base_ffn_lsq" if lsq_mode else "bert_base_ffn"),
+                "traffic": committed_traffic(dom, WORKLOAD_KEYS[cfg_id] + ("_lsq" if lsq_mode else "")),
                 "algorithmic_ops_per_launch": algo,
                 "note": "int8 MFMA ops (multiply-adds x 2) of the kept-token GEMM"}
 
@@ -294,7 +315,7 @@ def main():
     # ---- CPU oracle on a bounded token slice of the same workload
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(lins, args.cpu_seconds, lsq_mode)
+        cpu = cpu_baseline(lins, cfg_id, args.cpu_seconds, lsq_mode)
 
     out = {
         "metric": METRIC,
@@ -472,7 +493,7 @@ def cpu_baseline_bmm(np, synth, target_s: float):
             "seconds": round(t, 2)}
 
 
-def cpu_baseline(lins, target_s: float, lsq_mode: bool = False):
+def cpu_baseline(lins, cfg_id: int, target_s: float, lsq_mode: bool = False):
     """The oracle, as it stands, on the first n tokens of each linear (fwd + bwd)."""
     import numpy as np
 
@@ -491,7 +512,7 @@ def cpu_baseline(lins, target_s: float, lsq_mode: bool = False):
         for li, lin in enumerate(lins):
             sub = synth.Linear(lin.name, n, lin.D, lin.C, lin.log2_block, lin.dtype,
                                lin.x_outlier_channels, lin.x_outlier_scale, lin.grad_kind, n)
-            X, W, G = synth.linear_inputs(sub, CFG_ID, li)
+            X, W, G = synth.linear_inputs(sub, cfg_id, li)
             t0 = time.perf_counter()
             if lsq_mode:
                 k = lin.log2_block
