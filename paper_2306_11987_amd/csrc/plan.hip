@@ -146,7 +146,9 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
   const uint32_t* cdn = scores + pitch;
   const uint32_t* sup = reinterpret_cast<const uint32_t*>(sumsq_up);
   auto round = [&](int t0, int n8, const uint32_t su[8], const uint32_t cd[8]) {
-    const U4 rnd = philox_block(seed, offset, 1u, (uint64_t)(t0 > 0 ? t0 : 0));
+    // Bernoulli draws only when some row has p < 1 (uniform over the workgroup)
+    const U4 rnd = all_nonzero_kept ? U4{0u, 0u, 0u, 0u}
+                                    : philox_block(seed, offset, 1u, (uint64_t)(t0 > 0 ? t0 : 0));
     uint32_t wu8[2] = {0u, 0u}, wd8[2] = {0u, 0u};
     uint32_t keepmask = 0;
 #pragma unroll
