@@ -55,6 +55,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kBN = 256;  // workgroup tile width (n)
 constexpr int kNarrowBN = 64;  // tile width of the gradient GEMMs for outputs <= 64 wide
+constexpr int kMidBN = 128;    // tile width of gradient GEMMs with few 256-wide tiles
+#ifndef HQLSS_GEMM_MID_TILES
+#define HQLSS_GEMM_MID_TILES 1
+#endif
 constexpr int kKS = 128;  // K elements per stage
 #ifndef HQLSS_GEMM_FWD_BM
 #define HQLSS_GEMM_FWD_BM 128
@@ -760,11 +764,40 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   return hipGetLastError();
 }
 
+int g_grad_bn_override = 0;  // test hook: 128 or 256 forces that width (0: the rule below)
+
+// Workgroup tile width of a gradient GEMM: 64 for outputs at most 64 wide; 128 when the
+// 256-wide tiles would fill at most three quarters of one round of two workgroups per CU
+// (most CUs would then hold a single workgroup, whose MFMA issue is about half as dense);
+// else 256.
+int grad_bn(int64_t M, int64_t N, int splits) {
+  if (splits > 1) return kBN;
+  if (N <= kNarrowBN) return kNarrowBN;
+  if (g_grad_bn_override) return g_grad_bn_override;
+  const int64_t bm = tile_m<false>();
+  const int64_t t256 = ((M + bm - 1) / bm) * ((N + kBN - 1) / kBN);
+  return (HQLSS_GEMM_MID_TILES && 4 * t256 <= 3 * 512) ? kMidBN : kBN;  // 256 CUs
+}
+
 // the Hadamard block is a template parameter of the gradient epilogues
 template <int BM, bool A4, int EPI, int DT>
 hipError_t gemm_b(hipStream_t s, const GemmArgs& g, int splits, int id) {
   if constexpr (EPI == kEpiDx || EPI == kEpiDw || EPI == kEpiDxL || EPI == kEpiDwL) {
-    if (splits <= 1 && g.N <= kNarrowBN) {  // narrow output: blocks of at most 64 columns
+    const int bn = grad_bn(g.M, g.N, splits);
+    if (bn == kMidBN) {
+      switch (g.log2b) {
+        case 0: return gemm_t<BM, A4, EPI, DT, 0, kMidBN>(s, g, splits, id);
+        case 1: return gemm_t<BM, A4, EPI, DT, 1, kMidBN>(s, g, splits, id);
+        case 2: return gemm_t<BM, A4, EPI, DT, 2, kMidBN>(s, g, splits, id);
+        case 3: return gemm_t<BM, A4, EPI, DT, 3, kMidBN>(s, g, splits, id);
+        case 4: return gemm_t<BM, A4, EPI, DT, 4, kMidBN>(s, g, splits, id);
+        case 5: return gemm_t<BM, A4, EPI, DT, 5, kMidBN>(s, g, splits, id);
+        case 6: return gemm_t<BM, A4, EPI, DT, 6, kMidBN>(s, g, splits, id);
+        case 7: return gemm_t<BM, A4, EPI, DT, 7, kMidBN>(s, g, splits, id);
+      }
+      return hipErrorInvalidValue;
+    }
+    if (bn == kNarrowBN) {  // narrow output: blocks of at most 64 columns
       switch (g.log2b) {
         case 0: return gemm_t<BM, A4, EPI, DT, 0, kNarrowBN>(s, g, splits, id);
         case 1: return gemm_t<BM, A4, EPI, DT, 1, kNarrowBN>(s, g, splits, id);
@@ -827,6 +860,7 @@ hipError_t run_dt(hipStream_t s, int dt, const GemmArgs& g, int splits, int32_t*
 
 static int g_split_override = 0;
 void gemm_set_split_override(int splits) { g_split_override = splits < 0 ? 0 : splits; }
+void gemm_set_grad_tile_override(int bn) { g_grad_bn_override = (bn == kMidBN || bn == kBN) ? bn : 0; }
 
 int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4) {
   (void)b_int4;
@@ -865,7 +899,7 @@ hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4,
 int64_t gemm_epi_parts(int64_t M, int64_t N, int splits) {
   if (splits <= 1) {
     const int64_t bm = tile_m<false>();
-    const int64_t bn = N <= kNarrowBN ? kNarrowBN : kBN;  // as gemm_b chooses
+    const int64_t bn = grad_bn(M, N, splits);  // as gemm_b chooses
     return ((N + bn - 1) / bn) * ((M + bm - 1) / bm);
   }
   return reduce_grid(M, N);

@@ -224,3 +224,25 @@ def test_forced_split_k_parity(splits):
         check_float_output("dW", dW, b.dW, dt)
     finally:
         H.debug_set_gemm_splits(0)
+
+
+@pytest.mark.parametrize("bn", [128, 256])
+def test_forced_grad_tile_width(bn):
+    """Gradient GEMMs with 128- or 256-wide workgroup tiles on a shape that fills neither
+    width (D = 448 and C = 320 output columns and rows, 600 tokens): bit-exact against the
+    oracle under both widths."""
+    H = need_gpu()
+    lin, X, W, G = _case((600, 448, 320, 5, "f16", "lognormal"), seed=8)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    say(f"forced gradient tile width {bn}")
+    H.debug_set_grad_tile_n(bn)
+    try:
+        saved, _ = run_forward(H, X, W, k, dt)
+        f = O.hq_forward(X, W, k, compute_output=False)
+        b = O.lss_backward(G, f, N // 2, 6, 0)
+        _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N // 2, 6, 0)
+        check_plan(plan, b)
+        check_float_output("dX", dX, b.dX, dt)
+        check_float_output("dW", dW, b.dW, dt)
+    finally:
+        H.debug_set_grad_tile_n(0)
