@@ -271,11 +271,12 @@ def main():
         N_, D_, C_ = e["lin"].N, e["lin"].D, e["lin"].C
         if lsq_mode:  # one read, codes + fp16 deltas written, row sums of X
             ab["lsq_quant"] = ab.get("lsq_quant", 0.0) + (eb + 2.5) * (N_ + C_) * D_ + 4 * N_
-        else:  # the maximum pass reads X and W; the quantiser reads them again, writes codes
+            ab["transpose_packed"] = ab.get("transpose_packed", 0.0) + 1.0 * C_ * D_
+        else:  # the maximum pass reads X and W; the quantiser reads them again, writes the
+            # codes of X, W and W^T
             ab["fwht_absmax"] = ab.get("fwht_absmax", 0.0) + eb * (N_ + C_) * D_
-            ab["fwht_quant"] = ab.get("fwht_quant", 0.0) + (eb + 0.5) * (N_ + C_) * D_ + 4 * N_
+            ab["fwht_quant"] = ab.get("fwht_quant", 0.0) + (eb + 0.5) * (N_ + C_) * D_ + 0.5 * C_ * D_ + 4 * N_
         ab["fwht_absmax"] = ab.get("fwht_absmax", 0.0) + eb * N_ * C_  # maximum of dY
-        ab["transpose_packed"] = ab.get("transpose_packed", 0.0) + 1.0 * C_ * D_
         # dY read; two INT4 code planes written; row sums and the two scores per token
         ab["bit_split"] = ab.get("bit_split", 0.0) + (eb + 1.0) * N_ * C_ + 20 * N_
         # codes of the kept rows read, A and A^T written; gathered X codes read and written

@@ -173,9 +173,8 @@ hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D,
   QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
   HQ_TRY(launch_fwht_absmax(s, dt, k, jx, px, jw, pw));
   const QOut ox{px, jx.wg, sv->amax, sv->xq, sv->x_sumsq};
-  const QOut ow{pw, jw.wg, sv->amax + 1, sv->wq, nullptr};
+  const QOut ow{pw, jw.wg, sv->amax + 1, sv->wq, nullptr, sv->wqT};  // W^ and W^^T
   HQ_TRY(launch_fwht_quant(s, dt, k, jx, ox, jw, ow));
-  HQ_TRY(launch_transpose_packed(s, sv->wq, C, D, sv->wqT));
   if (Y) {
     GemmArgs g{};
     g.A = sv->xq; g.lda = D / 2;

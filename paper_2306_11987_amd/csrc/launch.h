@@ -44,13 +44,16 @@ QJob make_job_batched(const void* src, int64_t batch, int64_t rows, int64_t cols
 hipError_t launch_fwht_absmax(hipStream_t s, int dt, int log2b, QJob& j0, float* part0,
                               QJob& j1, float* part1);
 // Codes of block-FWHT(src) at the maximum of the partials, packed [rows][cols/2]; optional
-// per-row sums of squares; the maximum itself is stored to *amax_out.
+// per-row sums of squares; the maximum itself is stored to *amax_out.  For the second job
+// the same codes can also be written transposed, packed [cols][rows/2] (rows a multiple of
+// 16), by extra workgroups of the same launch.
 struct QOut {
   const float* part;
   int nparts;
   float* amax_out;
   uint8_t* packed;
   int32_t* row_sumsq;  // may be null
+  uint8_t* packed_t;   // may be null; honoured for the second job only
 };
 hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const QJob& j0, const QOut& o0,
                              const QJob& j1, const QOut& o1);

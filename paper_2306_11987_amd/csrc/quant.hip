@@ -227,13 +227,64 @@ __global__ __launch_bounds__(kQThreads) void fwht_absmax_kernel(QJob j0, QJob j1
   }
 }
 
+// Transposed codes of one tile of a job: TW columns (whole Hadamard blocks) x R rows,
+// 16 elements per lane as in the row kernels, so the transform and the rounding are the
+// same operations on the same values.  The codes pass through LDS and leave as rows of
+// the transposed matrix: thread (d, q) packs rows 16 q .. 16 q + 15 of column d.  Rows
+// past the end are loaded from the last row and not stored.
+template <int LOG2B> struct TileT {
+  static constexpr int TW = (1 << LOG2B) > 64 ? 128 : 64;
+  static constexpr int LPR = TW / kVE;         // lanes per row
+  static constexpr int R = kQThreads / LPR;    // rows per tile
+  static int64_t tiles(int64_t rows, int64_t cols) { return (rows + R - 1) / R * (cols / TW); }
+};
+
+template <int DT, int LOG2B>
+__device__ void quant_tile_t(const QJob& j, uint8_t* __restrict__ dst, float inv, int t) {
+  using T = TileT<LOG2B>;
+  constexpr int TW = T::TW, LPR = T::LPR, R = T::R, PITCH = TW + 4;
+  __shared__ uint8_t tile[R * PITCH];
+  constexpr int EB = Elem<DT>::bytes;
+  const int64_t rows = j.rows, cols = j.cols, ntc = cols / TW;
+  const int64_t r0 = (int64_t)(t / ntc) * R, c0 = (int64_t)(t % ntc) * TW;
+  const int tid = threadIdx.x, rr = tid / LPR, sub = tid % LPR;
+  {
+    const int64_t r = r0 + rr < rows ? r0 + rr : rows - 1;
+    float v[kVE];
+    load16<DT, HQ_NT_Q_LD>(static_cast<const char*>(j.src) + (r * cols + c0 + sub * kVE) * EB, v);
+    fwht16<LOG2B>(v, tid & 63);
+    uint32_t* row = reinterpret_cast<uint32_t*>(tile + rr * PITCH + sub * kVE);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      uint32_t b = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) b |= (rne_bits(v[4 * w + e] * inv) & 15u) << (8 * e);
+      row[w] = b;
+    }
+  }
+  __syncthreads();
+  const int d = tid / (R / 16), q = tid % (R / 16);
+  if (r0 + 16 * q < rows) {
+    uint32_t w2[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) w2[i >> 3] |= (uint32_t)tile[(16 * q + i) * PITCH + d] << (4 * (i & 7));
+    *reinterpret_cast<uint2*>(dst + (c0 + d) * (rows / 2) + r0 / 2 + 8 * q) = make_uint2(w2[0], w2[1]);
+  }
+}
+
 // Codes of FWHT(rows) at the reduced maximum a; the first workgroup of each job also
-// stores a.  Row sums of squares are plain stores by the group's first lane.  The clamp
+// stores a.  Workgroups past the two jobs' row workgroups write job 1's transposed codes
+// (one tile each) when o1.packed_t is set.  Row sums of squares are plain stores by the group's first lane.  The clamp
 // to +-7 of the definition never engages here: |v| <= a gives |v * fl(7/a)| <= 7 (1 + 2^-24),
 // which rounds to at most 7.
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1, QOut o0, QOut o1) {
   constexpr int U = 4;
+  if ((int)blockIdx.x >= j0.wg + j1.wg) {  // uniform per workgroup
+    const float a = reduce_parts(o1.part, o1.nparts);
+    quant_tile_t<DT, LOG2B>(j1, o1.packed_t, a > 0.f ? 7.0f / a : 0.f, (int)blockIdx.x - j0.wg - j1.wg);
+    return;
+  }
   const bool second = (int)blockIdx.x >= j0.wg;
   const QJob& j = second ? j1 : j0;
   const QOut& o = second ? o1 : o0;
@@ -832,8 +883,9 @@ template <int DT, int LOG2B> struct QuantF {
   static hipError_t run(hipStream_t s, QJob j0, QJob j1, QOut o0, QOut o1) {
     const void* f = reinterpret_cast<const void*>(&fwht_quant_kernel<DT, LOG2B>);
     fit_grid(j0, j1, resident_wgs(f));
+    const int64_t nt = o1.packed_t ? TileT<LOG2B>::tiles(j1.rows, j1.cols) : 0;
     timing_begin(s);
-    fwht_quant_kernel<DT, LOG2B><<<j0.wg + j1.wg, kQThreads, 0, s>>>(j0, j1, o0, o1);
+    fwht_quant_kernel<DT, LOG2B><<<(unsigned)(j0.wg + j1.wg + nt), kQThreads, 0, s>>>(j0, j1, o0, o1);
     timing_end(s, kKQuant);
     return hipGetLastError();
   }

@@ -156,6 +156,7 @@ def test_full_size_sampled(case):
     assert to_np(saved.amax)[0] == f.amax_x and to_np(saved.amax)[1] == f.amax_w
     assert np.array_equal(to_np(saved.xq), O.pack_int4(f.xq))
     assert np.array_equal(to_np(saved.wq), O.pack_int4(f.wq))
+    assert np.array_equal(to_np(saved.wqT), O.pack_int4(f.wq.T.copy()))
     assert np.array_equal(to_np(saved.x_sumsq), f.x_sumsq.astype(np.int32))
     rng = np.random.default_rng(cid * 10 + li)
     rows = rng.choice(N, 64, replace=False)
