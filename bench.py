@@ -42,6 +42,14 @@ sys.path.insert(0, ROOT)
 
 INT8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
 HBM_PEAK_GBS = 8000.0
+# vector ALU: 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz (the fp32 vector peak of
+# 157.3 TFLOP/s counts a packed FMA, 4 flops, per slot)
+VALU_PEAK_TSLOTS = 256 * 4 * 16 * 2.4e9 / 1e12
+# bit split, per gradient element: one Philox4x32-10 block per 8 elements (10 rounds of two
+# 32x32->64 multiplies, 4 slots each, and two 3-input xors) = 12.5, plus 11 full-rate
+# operations (widen and scale, round, residual x 14, floor, fraction, x 2^16, uniform to
+# float, compare, add, pack, sum of squares)
+BS_VALU_SLOTS_PER_ELEM = 23.5
 METRIC = "INT4 linear fwd+bwd effective TOPS (fraction of int8-MFMA peak) vs bf16"
 # workloads: id -> key of the committed counter summaries under profiles/
 WORKLOAD_KEYS = {1: "bert_base_ffn", 2: "gpt2_medium", 3: "gemm_sweep", 4: "bert_large_block"}
@@ -270,8 +278,7 @@ def main():
     for e, kt in zip(L, kept):
         N_, D_, C_ = e["lin"].N, e["lin"].D, e["lin"].C
         if lsq_mode:  # one read, codes + fp16 deltas written, row sums of X
-            ab["lsq_quant"] = ab.get("lsq_quant", 0.0) + (eb + 2.5) * (N_ + C_) * D_ + 4 * N_
-            ab["transpose_packed"] = ab.get("transpose_packed", 0.0) + 1.0 * C_ * D_
+            ab["lsq_quant"] = ab.get("lsq_quant", 0.0) + (eb + 2.5) * (N_ + C_) * D_ + 0.5 * C_ * D_ + 4 * N_
         else:  # the maximum pass reads X and W; the quantiser reads them again, writes the
             # codes of X, W and W^T
             ab["fwht_absmax"] = ab.get("fwht_absmax", 0.0) + eb * (N_ + C_) * D_
@@ -425,6 +432,14 @@ def main_bmm(args, np, torch, H, synth, dev):
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS,
                 "unit": "TFLOP/s", "frac": round(ach / INT8_PEAK_TOPS, 4), "traffic": None,
                 "algorithmic_ops_per_launch": algo}
+    elif dom == "bit_split":  # bound by vector-ALU issue (Philox and the rounding)
+        algo = BS_VALU_SLOTS_PER_ELEM * B * N * P
+        ach = algo / (kernels[dom]["avg_us"] * 1e-6) / 1e12
+        roof = {"kernel": dom, "bound": "alu", "achieved": round(ach, 2), "peak": VALU_PEAK_TSLOTS,
+                "unit": "T VALU lane-slots/s", "frac": round(ach / VALU_PEAK_TSLOTS, 4), "traffic": None,
+                "algorithmic_ops_per_launch": algo,
+                "note": f"{BS_VALU_SLOTS_PER_ELEM} lane-slots per element of dT (Philox4x32-10 share "
+                        "with 32x32->64 multiplies at quarter rate, plus the rounding and packing)"}
     bf16 = None
     if not args.no_bf16:
         Qb, Kb, Gb = (t.to(torch.bfloat16) for t in (Q, K, G))

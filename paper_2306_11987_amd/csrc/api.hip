@@ -196,9 +196,8 @@ hqlss_status do_fwd_lsq(const void* X, const void* W, void* Y, int64_t N, int64_
                         hipStream_t s) {
   QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
   const LsqOut ox{l->step, sv->xq, sv->x_sumsq, l->delta_x};
-  const LsqOut ow{l->step + 1, sv->wq, nullptr, l->delta_w};
+  const LsqOut ow{l->step + 1, sv->wq, nullptr, l->delta_w, sv->wqT};  // W^ and W^^T
   HQ_TRY(launch_fwht_lsq(s, dt, k, jx, ox, jw, ow));
-  HQ_TRY(launch_transpose_packed(s, sv->wq, C, D, sv->wqT));
   GemmArgs g{};
   g.A = sv->xq; g.lda = D / 2;
   g.B = sv->wq; g.ldb = D / 2;
@@ -235,9 +234,8 @@ hqlss_status do_bmm_fwd(const void* Q, const void* K, void* T, int64_t B, int64_
                         const hqlss_bmm_lsq_t* l, hipStream_t s) {
   QJob jq = make_job_batched(Q, B, N, M), jk = make_job_batched(K, B, P, M);
   const LsqOut oq{l->step_q, sv->xq, sv->x_sumsq, l->delta_q};
-  const LsqOut ok{l->step_k, sv->wq, nullptr, l->delta_k};
+  const LsqOut ok{l->step_k, sv->wq, nullptr, l->delta_k, sv->wqT};  // K^ and K^^T per batch
   HQ_TRY(launch_fwht_lsq(s, dt, k, jq, oq, jk, ok));
-  HQ_TRY(launch_transpose_packed(s, sv->wq, P, M, sv->wqT, B));
   GemmArgs g{};
   g.A = sv->xq; g.lda = M / 2;
   g.B = sv->wq; g.ldb = M / 2;
@@ -478,8 +476,7 @@ int64_t resolve_budget(int64_t budget_rows, int64_t N) {
 namespace hqlss {
 
 const char* kernel_name(int id) {
-  static const char* names[kKCount] = {"fwht_absmax", "fwht_quant", "transpose_packed",
-                                       "bit_split", "lss_plan", "build_operands",
+  static const char* names[kKCount] = {"fwht_absmax", "fwht_quant", "bit_split", "lss_plan", "build_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
                                        "gemm_reduce", "copy", "hsize_max", "hsize_err",
                                        "hsize_pick", "lsq_quant", "lsq_step_grad"};

@@ -7,7 +7,7 @@ namespace hqlss {
 
 // Kernel ids for the timing log (kept in sync with kernel_name()).
 enum KernelId : int {
-  kKAbsmax = 0, kKQuant, kKTranspose, kKBitSplit, kKPlan, kKBuild,
+  kKAbsmax = 0, kKQuant, kKBitSplit, kKPlan, kKBuild,
   kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKHsizeMax, kKHsizeErr,
   kKHsizePick, kKLsqQuant, kKLsqStepGrad, kKCount
 };
@@ -65,13 +65,10 @@ struct LsqOut {
   uint8_t* packed;
   int32_t* row_sumsq;  // may be null
   uint16_t* delta;
+  uint8_t* packed_t;   // may be null; second job only: codes transposed, as for QOut
 };
 hipError_t launch_fwht_lsq(hipStream_t s, int dt, int log2b, const QJob& j0, const LsqOut& o0,
                            const QJob& j1, const LsqOut& o1);
-// packed [rows][cols/2] -> packed [cols][rows/2] (rows, cols multiples of 64), for each
-// of `batch` matrices stored one after the other.
-hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t rows, int64_t cols,
-                                   uint8_t* dst, int64_t batch = 1);
 // Bit split of dY [N][C] into two packed code planes, their row sums of squares, the
 // integer leverage scores scores[t] (upper row) and scores[score_pitch + t] (lower row),
 // and per-workgroup {count of non-zero scores, sum lo, sum hi, 0} in parts[0, j.wg).

@@ -4,7 +4,9 @@
 //    unnormalised Hadamard transform of each row (radix-2 butterflies, strides ascending,
 //    fp32), then per-tensor absmax and INT4 codes clamp(rint(v * fl(7/a)), -7, 7)
 //    (Sec. 3.1, Eq. 2), packed two per byte (App. A.6) with per-row sums of squares
-//    (the ||X_i|| factor of the leverage score, Sec. 4.2).  One launch serves X and W.
+//    (the ||X_i|| factor of the leverage score, Sec. 4.2).  One launch serves X and W,
+//    and its extra workgroups write W's codes transposed as well (the K-contiguous
+//    operand of the dX GEMM): each quantises one tile of W again and transposes it in LDS.
 //  * fwht_lsq: the same transform quantised at a caller-given (learned) step in one pass,
 //    with the fp16 deltas q - I r that the learned-step backward needs (Eq. 2, App. A.4).
 //  * bit_split: bit splitting of the output gradient (Sec. 4.2, Eq. 4): upper codes by
@@ -236,29 +238,36 @@ template <int LOG2B> struct TileT {
   static constexpr int TW = (1 << LOG2B) > 64 ? 128 : 64;
   static constexpr int LPR = TW / kVE;         // lanes per row
   static constexpr int R = kQThreads / LPR;    // rows per tile
-  static int64_t tiles(int64_t rows, int64_t cols) { return (rows + R - 1) / R * (cols / TW); }
+  __host__ __device__ static int64_t tiles(int64_t rows, int64_t cols) { return (rows + R - 1) / R * (cols / TW); }
 };
 
-template <int DT, int LOG2B>
-__device__ void quant_tile_t(const QJob& j, uint8_t* __restrict__ dst, float inv, int t) {
+// LSQ selects the code of the learned-step quantiser, clamp(rint(v inv), -7, 7) (the clamp
+// first, as in fwht_lsq_kernel), else rint(v inv) as in fwht_quant_kernel.
+template <int DT, int LOG2B, bool LSQ>
+__device__ void quant_tile_t(const void* src, int64_t rows, int64_t cols, uint8_t* __restrict__ dst,
+                             float inv, int t) {
   using T = TileT<LOG2B>;
   constexpr int TW = T::TW, LPR = T::LPR, R = T::R, PITCH = TW + 4;
   __shared__ uint8_t tile[R * PITCH];
   constexpr int EB = Elem<DT>::bytes;
-  const int64_t rows = j.rows, cols = j.cols, ntc = cols / TW;
+  const int64_t ntc = cols / TW;
   const int64_t r0 = (int64_t)(t / ntc) * R, c0 = (int64_t)(t % ntc) * TW;
   const int tid = threadIdx.x, rr = tid / LPR, sub = tid % LPR;
   {
     const int64_t r = r0 + rr < rows ? r0 + rr : rows - 1;
     float v[kVE];
-    load16<DT, HQ_NT_Q_LD>(static_cast<const char*>(j.src) + (r * cols + c0 + sub * kVE) * EB, v);
+    load16<DT, HQ_NT_Q_LD>(static_cast<const char*>(src) + (r * cols + c0 + sub * kVE) * EB, v);
     fwht16<LOG2B>(v, tid & 63);
     uint32_t* row = reinterpret_cast<uint32_t*>(tile + rr * PITCH + sub * kVE);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       uint32_t b = 0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) b |= (rne_bits(v[4 * w + e] * inv) & 15u) << (8 * e);
+      for (int e = 0; e < 4; ++e) {
+        const float x = v[4 * w + e] * inv;
+        const uint32_t y = LSQ ? __float_as_uint(__builtin_amdgcn_fmed3f(x, -7.0f, 7.0f) + kRne) : rne_bits(x);
+        b |= (y & 15u) << (8 * e);
+      }
       row[w] = b;
     }
   }
@@ -282,7 +291,8 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
   constexpr int U = 4;
   if ((int)blockIdx.x >= j0.wg + j1.wg) {  // uniform per workgroup
     const float a = reduce_parts(o1.part, o1.nparts);
-    quant_tile_t<DT, LOG2B>(j1, o1.packed_t, a > 0.f ? 7.0f / a : 0.f, (int)blockIdx.x - j0.wg - j1.wg);
+    quant_tile_t<DT, LOG2B, false>(j1.src, j1.rows, j1.cols, o1.packed_t, a > 0.f ? 7.0f / a : 0.f,
+                                   (int)blockIdx.x - j0.wg - j1.wg);
     return;
   }
   const bool second = (int)blockIdx.x >= j0.wg;
@@ -345,6 +355,17 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_lsq_kernel(QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
   constexpr int U = 4;
+  {  // workgroups past the row workgroups: job 1's transposed codes, one tile each
+    const int nrow = j0.wg * j0.batch + j1.wg * j1.batch;
+    if ((int)blockIdx.x >= nrow) {  // uniform per workgroup
+      const int nt = (int)TileT<LOG2B>::tiles(j1.rows, j1.cols);
+      const int tt = (int)blockIdx.x - nrow, b = tt / nt;
+      quant_tile_t<DT, LOG2B, true>(
+          static_cast<const char*>(j1.src) + (int64_t)b * j1.bstride * Elem<DT>::bytes, j1.rows, j1.cols,
+          o1.packed_t + (int64_t)b * j1.cols * (j1.rows / 2), 1.0f / o1.step[b], tt % nt);
+      return;
+    }
+  }
   const QPos qp = qpos(j0, j1);
   const QJob& j = qp.second ? j1 : j0;
   const LsqOut& o = qp.second ? o1 : o0;
@@ -411,40 +432,6 @@ __global__ __launch_bounds__(kQThreads) void fwht_lsq_kernel(QJob j0, QJob j1, L
         }
       }
     }
-  }
-}
-
-__device__ __forceinline__ int sext4(uint32_t n) { return (int)(n ^ 8u) - 8; }
-
-__global__ __launch_bounds__(256) void transpose_packed_kernel(const uint8_t* __restrict__ src,
-                                                               int64_t rows, int64_t cols,
-                                                               uint8_t* __restrict__ dst) {
-  __shared__ int8_t t[64][65];  // codes [row_local][col_local]
-  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
-  src += (int64_t)blockIdx.z * rows * (cols / 2);  // matrix of this batch
-  dst += (int64_t)blockIdx.z * rows * (cols / 2);
-  const int tid = threadIdx.x;
-  const int r = tid >> 2, q = (tid & 3) * 8;  // 64 rows x 4 groups of 8 bytes
-  {
-    const uint2 w = *reinterpret_cast<const uint2*>(src + (r0 + r) * (cols / 2) + c0 / 2 + q);
-    const uint32_t ww[2] = {w.x, w.y};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t byte = (ww[j >> 2] >> (8 * (j & 3))) & 0xFFu;
-      t[r][2 * (q + j)] = (int8_t)sext4(byte & 15u);
-      t[r][2 * (q + j) + 1] = (int8_t)sext4(byte >> 4);
-    }
-  }
-  __syncthreads();
-  {
-    uint32_t ww[2] = {0u, 0u};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = 2 * (q + j);
-      const uint32_t byte = ((uint32_t)t[c][r] & 15u) | (((uint32_t)t[c + 1][r] & 15u) << 4);
-      ww[j >> 2] |= byte << (8 * (j & 3));
-    }
-    *reinterpret_cast<uint2*>(dst + (c0 + r) * (rows / 2) + r0 / 2 + q) = make_uint2(ww[0], ww[1]);
   }
 }
 
@@ -895,8 +882,10 @@ template <int DT, int LOG2B> struct LsqF {
   static hipError_t run(hipStream_t s, QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
     const void* f = reinterpret_cast<const void*>(&fwht_lsq_kernel<DT, LOG2B>);
     fit_grid(j0, j1, resident_wgs(f));
+    const int64_t nt = o1.packed_t ? TileT<LOG2B>::tiles(j1.rows, j1.cols) * j1.batch : 0;
     timing_begin(s);
-    fwht_lsq_kernel<DT, LOG2B><<<j0.wg * j0.batch + j1.wg * j1.batch, kQThreads, 0, s>>>(j0, j1, o0, o1);
+    fwht_lsq_kernel<DT, LOG2B><<<(unsigned)(j0.wg * j0.batch + j1.wg * j1.batch + nt), kQThreads, 0, s>>>(
+        j0, j1, o0, o1);
     timing_end(s, kKLsqQuant);
     return hipGetLastError();
   }
@@ -961,15 +950,6 @@ hipError_t launch_fwht_lsq(hipStream_t s, int dt, int log2b, const QJob& j0, con
     case kBF16: return dispatch_block<LsqF, kBF16>(log2b, s, j0, j1, o0, o1);
   }
   return hipErrorInvalidValue;
-}
-
-hipError_t launch_transpose_packed(hipStream_t s, const uint8_t* src, int64_t rows, int64_t cols,
-                                   uint8_t* dst, int64_t batch) {
-  dim3 grid((unsigned)(cols / 64), (unsigned)(rows / 64), (unsigned)batch);
-  timing_begin(s);
-  transpose_packed_kernel<<<grid, 256, 0, s>>>(src, rows, cols, dst);
-  timing_end(s, kKTranspose);
-  return hipGetLastError();
 }
 
 hipError_t launch_bit_split(hipStream_t s, int dt, QJob& j, const float* part, int nparts,
