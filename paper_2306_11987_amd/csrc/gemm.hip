@@ -59,6 +59,10 @@ constexpr int kMidBN = 128;    // tile width of gradient GEMMs with few 256-wide
 #ifndef HQLSS_GEMM_MID_TILES
 #define HQLSS_GEMM_MID_TILES 1
 #endif
+// Split-K gradient GEMMs wider than 64 columns run 128-wide tiles: twice the tiles, so
+// about half the splits fill the device and half the int32 partials are written and
+// summed (and a GEMM whose 128-wide tiles fill one round alone is not split at all).
+constexpr bool split_mid(bool a_int4, int64_t N) { return !a_int4 && N > kNarrowBN; }
 constexpr int kKS = 128;  // K elements per stage
 #ifndef HQLSS_GEMM_FWD_BM
 #define HQLSS_GEMM_FWD_BM 128
@@ -151,11 +155,13 @@ __device__ __forceinline__ void fwht_lane(int* v, int lane) {
 // of chunk x: tiles in flight on one XCD then share their operand rows in its L2.  T counts
 // only the tiles with rows below M (the device-side row count of dX), so that the tiles
 // past it do not all fall on the last XCDs; workgroups beyond their chunk get no tile.
-// Returns false for those.  Split-K grids and small grids keep the plain order.
-__device__ __forceinline__ bool tile_of(int T, int tiles_n, bool split, int& tm, int& tn) {
+// Returns false for those.  Small grids keep the plain order.  In a grid with a z extent
+// (split-K index or batch) the XCD of workgroup (b, z) is (b + z gridDim.x) % 8: every
+// class b % 8 still sits on one XCD within its z slice, so the chunks hold there too.
+__device__ __forceinline__ bool tile_of(int T, int tiles_n, int& tm, int& tn) {
   const int b = blockIdx.x;
   int L = b;
-  if (!split && T >= 16) {
+  if (T >= 16) {
     const int x = b & 7, j = b >> 3, q = T >> 3, r = T & 7;
     if (j >= q + (x < r ? 1 : 0)) return false;
     L = x * q + min(x, r) + j;
@@ -260,7 +266,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_>::THREADS), (Cfg<BM, A4, WN, B
   const int tiles_n = (int)((g.N + BN - 1) / BN);
   const int t_valid = tiles_n * (int)((M + BM - 1) / BM);  // tiles with rows below M
   int tm, tn;
-  if (!tile_of(t_valid, tiles_n, nsplit > 1, tm, tn)) {  // whole workgroup: uniform exit before any barrier
+  if (!tile_of(t_valid, tiles_n, tm, tn)) {  // whole workgroup: uniform exit before any barrier
     if constexpr (LSQ) {
       if (tid == 0) g.ds_part[blockIdx.x] = 0.0;
     }
@@ -841,7 +847,8 @@ hipError_t run(hipStream_t s, const GemmArgs& g, int splits, int32_t* partial, i
   GemmArgs p = g;
   p.out = partial;
   p.ldo = g.N;
-  hipError_t e = gemm_t<BM, A4, kEpiPartial, DT, 0>(s, p, splits, id);
+  hipError_t e = split_mid(A4, g.N) ? gemm_t<BM, A4, kEpiPartial, DT, 0, kMidBN>(s, p, splits, id)
+                                     : gemm_t<BM, A4, kEpiPartial, DT, 0>(s, p, splits, id);
   if (e != hipSuccess) return e;
   return reduce_t<DT, EPI>(s, partial, splits, g);
 }
@@ -867,7 +874,8 @@ int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4) {
   if (g_split_override) return g_split_override;
   const int64_t bm = a_int4 ? tile_m<true>() : tile_m<false>();
   const int64_t slots = bm == 128 ? 512 : 256;  // workgroups in flight
-  const int64_t tiles = ((M + bm - 1) / bm) * ((N + kBN - 1) / kBN);
+  const int64_t bn = split_mid(a_int4, N) ? kMidBN : kBN;
+  const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   const int64_t stages = (K + kKS - 1) / kKS;
   if (2 * tiles >= slots || stages < 16) return 1;
   int64_t s = slots / tiles;        // all splits resident at once (no second round)
