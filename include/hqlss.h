@@ -304,11 +304,11 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t *plan, const hqlss
  * choice).  Workspace sizes follow the factor in force when they are queried. */
 void hqlss_debug_set_gemm_splits(int splits);
 
-/* Test hook: force the workgroup tile width (128 or 256 output columns) of the gradient
- * GEMMs that are not split along K and whose output is wider than 64 columns; any other
- * value restores the built-in choice.  Results do not depend on the width.  Workspace
- * sizes follow the width in force when they are queried. */
-void hqlss_debug_set_grad_tile_n(int bn);
+/* Test hook: force the workgroup tile width (128 or 256 output columns) of the forward
+ * GEMMs and of the gradient GEMMs whose output is wider than 64 columns, where they are
+ * not split along K; any other value restores the built-in choice.  Results do not depend
+ * on the width.  Workspace sizes follow the width in force when they are queried. */
+void hqlss_debug_set_gemm_tile_n(int bn);
 
 /* Benchmark hook: a plain device-to-device copy kernel ("copy") of `bytes` bytes (a
  * multiple of 16, both pointers 16-byte aligned, non-overlapping), asynchronous on

@@ -75,7 +75,7 @@ def _load() -> ctypes.CDLL:
         "hqlss_timing_read": (_int, [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _int]),
         "hqlss_kernel_name": (ctypes.c_char_p, [_int]),
         "hqlss_debug_set_gemm_splits": (None, [_int]),
-        "hqlss_debug_set_grad_tile_n": (None, [_int]),
+        "hqlss_debug_set_gemm_tile_n": (None, [_int]),
         "hqlss_debug_copy": (st, [_vp, _vp, _sz, _vp]),
     }
     for name, (res, args) in sig.items():
@@ -412,8 +412,8 @@ def debug_set_gemm_splits(splits: int) -> None:
     lib.hqlss_debug_set_gemm_splits(int(splits))
 
 
-def debug_set_grad_tile_n(bn: int) -> None:
-    lib.hqlss_debug_set_grad_tile_n(int(bn))
+def debug_set_gemm_tile_n(bn: int) -> None:
+    lib.hqlss_debug_set_gemm_tile_n(int(bn))
 
 
 def debug_copy(src: torch.Tensor, dst: torch.Tensor) -> None:

@@ -821,7 +821,7 @@ int hqlss_timing_read(int* ids, float* ms, int cap) {
 const char* hqlss_kernel_name(int id) { return hqlss::kernel_name(id); }
 
 void hqlss_debug_set_gemm_splits(int splits) { hqlss::gemm_set_split_override(splits); }
-void hqlss_debug_set_grad_tile_n(int bn) { hqlss::gemm_set_grad_tile_override(bn); }
+void hqlss_debug_set_gemm_tile_n(int bn) { hqlss::gemm_set_tile_override(bn); }
 
 hqlss_status hqlss_debug_copy(const void* src, void* dst, size_t bytes, void* stream) {
   if (!src || !dst) return HQLSS_ERR_NULL;

@@ -56,9 +56,6 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int kBN = 256;  // workgroup tile width (n)
 constexpr int kNarrowBN = 64;  // tile width of the gradient GEMMs for outputs <= 64 wide
 constexpr int kMidBN = 128;    // tile width of gradient GEMMs with few 256-wide tiles
-#ifndef HQLSS_GEMM_MID_TILES
-#define HQLSS_GEMM_MID_TILES 1
-#endif
 // Split-K gradient GEMMs wider than 64 columns run 128-wide tiles: twice the tiles, so
 // about half the splits fill the device and half the int32 partials are written and
 // summed (and a GEMM whose 128-wide tiles fill one round alone is not split at all).
@@ -759,7 +756,8 @@ int64_t reduce_grid(int64_t M, int64_t N) {
 // dimensions), which would otherwise leave most of a 256-wide tile idle
 template <int BM, bool A4, int EPI, int DT, int LOG2B, int BN_ = kBN>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
-  constexpr int WN = wave_n<A4, LOG2B>() < BN_ ? wave_n<A4, LOG2B>() : BN_;
+  // 128-wide INT4 x INT4 tiles: 64 x 64 wave tiles (one widened fragment per MFMA)
+  constexpr int WN = (A4 && BN_ == kMidBN) ? 64 : wave_n<A4, LOG2B>() < BN_ ? wave_n<A4, LOG2B>() : BN_;
   using C_ = Cfg<BM, A4, WN, BN_>;
   // one workgroup per tile of the M x N output (M the host-side bound; see tile_of)
   dim3 grid((unsigned)(((g.N + BN_ - 1) / BN_) * ((g.M + BM - 1) / BM)), 1u,
@@ -770,7 +768,7 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   return hipGetLastError();
 }
 
-int g_grad_bn_override = 0;  // test hook: 128 or 256 forces that width (0: the rule below)
+int g_bn_override = 0;  // test hook: 128 or 256 forces that width (0: the rules below)
 
 // Workgroup tile width of a gradient GEMM: 64 for outputs at most 64 wide; 128 when the
 // 256-wide tiles would fill at most three quarters of one round of two workgroups per CU
@@ -779,10 +777,20 @@ int g_grad_bn_override = 0;  // test hook: 128 or 256 forces that width (0: the 
 int grad_bn(int64_t M, int64_t N, int splits) {
   if (splits > 1) return kBN;
   if (N <= kNarrowBN) return kNarrowBN;
-  if (g_grad_bn_override) return g_grad_bn_override;
+  if (g_bn_override) return g_bn_override;
   const int64_t bm = tile_m<false>();
   const int64_t t256 = ((M + bm - 1) / bm) * ((N + kBN - 1) / kBN);
-  return (HQLSS_GEMM_MID_TILES && 4 * t256 <= 3 * 512) ? kMidBN : kBN;  // 256 CUs
+  return 4 * t256 <= 3 * 512 ? kMidBN : kBN;  // 512 = two workgroups on each of 256 CUs
+}
+
+// Tile width of a forward (INT4 x INT4) GEMM by the same rule, the tiles of all batches
+// counted; its 128-wide tiles use 64 x 64 wave tiles.
+int fwd_bn(int64_t M, int64_t N, int splits, int64_t batch) {
+  if (splits > 1) return kBN;
+  if (g_bn_override) return g_bn_override;
+  const int64_t bm = tile_m<true>();
+  const int64_t t256 = ((M + bm - 1) / bm) * ((N + kBN - 1) / kBN) * (batch > 0 ? batch : 1);
+  return 4 * t256 <= 3 * 512 ? kMidBN : kBN;
 }
 
 // the Hadamard block is a template parameter of the gradient epilogues
@@ -827,6 +835,7 @@ hipError_t gemm_b(hipStream_t s, const GemmArgs& g, int splits, int id) {
     }
     return hipErrorInvalidValue;
   } else {
+    if (fwd_bn(g.M, g.N, splits, g.batch) == kMidBN) return gemm_t<BM, A4, EPI, DT, 0, kMidBN>(s, g, splits, id);
     return gemm_t<BM, A4, EPI, DT, 0>(s, g, splits, id);
   }
 }
@@ -867,7 +876,7 @@ hipError_t run_dt(hipStream_t s, int dt, const GemmArgs& g, int splits, int32_t*
 
 static int g_split_override = 0;
 void gemm_set_split_override(int splits) { g_split_override = splits < 0 ? 0 : splits; }
-void gemm_set_grad_tile_override(int bn) { g_grad_bn_override = (bn == kMidBN || bn == kBN) ? bn : 0; }
+void gemm_set_tile_override(int bn) { g_bn_override = (bn == kMidBN || bn == kBN) ? bn : 0; }
 
 int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4) {
   (void)b_int4;

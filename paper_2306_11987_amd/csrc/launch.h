@@ -146,7 +146,7 @@ struct GemmArgs {
 int gemm_splits(int64_t M, int64_t N, int64_t K, bool a_int4, bool b_int4);
 size_t gemm_partial_bytes(int64_t M, int64_t N, int splits);
 void gemm_set_split_override(int splits);
-void gemm_set_grad_tile_override(int bn);
+void gemm_set_tile_override(int bn);
 hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4, const GemmArgs& g,
                        int splits, int32_t* partial);
 // Number of ds_part entries a kEpiDxL / kEpiDwL launch of this shape writes (one per

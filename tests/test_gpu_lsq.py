@@ -157,23 +157,26 @@ def test_lsq_forced_split_k(splits):
 
 
 @pytest.mark.parametrize("bn", [128, 256])
-def test_lsq_forced_grad_tile_width(bn):
-    """The masked gradient epilogues and their step-gradient partial sums (one per
-    workgroup, as many as the tile width gives) under 128- and 256-wide tiles."""
+def test_lsq_forced_gemm_tile_width(bn):
+    """The learned-step forward and the masked gradient epilogues with their step-gradient
+    partial sums (one per workgroup, as many as the tile width gives) under 128- and
+    256-wide tiles."""
     H = need_gpu()
     lin, X, W, G = _case((600, 448, 320, 5, "f16", "lognormal"), seed=8)
     N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
     sx, sw = _steps(X, W, k, 0.05)
     say(f"lsq forced gradient tile width {bn}")
-    H.debug_set_grad_tile_n(bn)
+    H.debug_set_gemm_tile_n(bn)
     try:
-        saved, lsq, _ = run_forward_lsq(H, X, W, k, dt, sx, sw)
+        saved, lsq, Y = run_forward_lsq(H, X, W, k, dt, sx, sw)
         f = O.lsq_forward(X, W, k, sx, sw)
+        check_forward_codes(saved, lsq, f)
+        check_float_output("Y", Y, f.Y, dt)
         b = O.lsq_backward(G, f, N // 2, 6, 0)
         dX, dW, dstep = run_backward_lsq(H, G, saved, lsq, N, D, C, k, dt, N // 2, 6, 0)
         check_backward(dX, dW, dstep, f, b, N, D, C, dt)
     finally:
-        H.debug_set_grad_tile_n(0)
+        H.debug_set_gemm_tile_n(0)
 
 
 def test_lsq_deterministic():

@@ -228,17 +228,18 @@ def test_forced_split_k_parity(splits):
 
 
 @pytest.mark.parametrize("bn", [128, 256])
-def test_forced_grad_tile_width(bn):
-    """Gradient GEMMs with 128- or 256-wide workgroup tiles on a shape that fills neither
-    width (D = 448 and C = 320 output columns and rows, 600 tokens): bit-exact against the
-    oracle under both widths."""
+def test_forced_gemm_tile_width(bn):
+    """Forward and gradient GEMMs with 128- or 256-wide workgroup tiles on a shape that
+    fills neither width (C = 320 and D = 448 output columns, 600 tokens): bit-exact against
+    the oracle under both widths."""
     H = need_gpu()
     lin, X, W, G = _case((600, 448, 320, 5, "f16", "lognormal"), seed=8)
     N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
-    say(f"forced gradient tile width {bn}")
-    H.debug_set_grad_tile_n(bn)
+    say(f"forced GEMM tile width {bn}")
+    H.debug_set_gemm_tile_n(bn)
     try:
-        saved, _ = run_forward(H, X, W, k, dt)
+        saved, Y = run_forward(H, X, W, k, dt)
+        check_forward(H, X, W, k, dt, saved, Y)
         f = O.hq_forward(X, W, k, compute_output=False)
         b = O.lss_backward(G, f, N // 2, 6, 0)
         _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N // 2, 6, 0)
@@ -246,4 +247,4 @@ def test_forced_grad_tile_width(bn):
         check_float_output("dX", dX, b.dX, dt)
         check_float_output("dW", dW, b.dW, dt)
     finally:
-        H.debug_set_grad_tile_n(0)
+        H.debug_set_gemm_tile_n(0)
