@@ -229,11 +229,13 @@ __global__ __launch_bounds__(kQThreads) void fwht_absmax_kernel(QJob j0, QJob j1
   }
 }
 
-// Transposed codes of one tile of a job: TW columns (whole Hadamard blocks) x R rows,
-// 16 elements per lane as in the row kernels, so the transform and the rounding are the
-// same operations on the same values.  The codes pass through LDS and leave as rows of
-// the transposed matrix: thread (d, q) packs rows 16 q .. 16 q + 15 of column d.  Rows
-// past the end are loaded from the last row and not stored.
+// One tile of the second job (W), quantised by one workgroup: TW columns (whole Hadamard
+// blocks) x R rows, 16 elements per lane as in the row kernels, so the transform and the
+// rounding are the same operations on the same values.  The workgroup writes the tile's
+// codes both ways: row-major from registers (as the row kernels do, with the fp16 deltas
+// of the learned-step mode) and transposed through LDS (thread (d, q) packs rows
+// 16 q .. 16 q + 15 of column d).  The tiles thus read W once and replace the row
+// workgroups of that job.  Rows past the end are loaded from the last row and not stored.
 template <int LOG2B> struct TileT {
   static constexpr int TW = (1 << LOG2B) > 64 ? 128 : 64;
   static constexpr int LPR = TW / kVE;         // lanes per row
@@ -241,11 +243,12 @@ template <int LOG2B> struct TileT {
   __host__ __device__ static int64_t tiles(int64_t rows, int64_t cols) { return (rows + R - 1) / R * (cols / TW); }
 };
 
-// LSQ selects the code of the learned-step quantiser, clamp(rint(v inv), -7, 7) (the clamp
-// first, as in fwht_lsq_kernel), else rint(v inv) as in fwht_quant_kernel.
+// LSQ selects the learned-step quantiser: code clamp(rint(v inv), -7, 7) (the clamp first)
+// and delta as in fwht_lsq_kernel; else the code rint(v inv) of fwht_quant_kernel.
 template <int DT, int LOG2B, bool LSQ>
-__device__ void quant_tile_t(const void* src, int64_t rows, int64_t cols, uint8_t* __restrict__ dst,
-                             float inv, int t) {
+__device__ void quant_tile(const void* src, int64_t rows, int64_t cols, float inv, int t,
+                           uint8_t* __restrict__ packed, uint16_t* __restrict__ delta,
+                           uint8_t* __restrict__ packed_t) {
   using T = TileT<LOG2B>;
   constexpr int TW = T::TW, LPR = T::LPR, R = T::R, PITCH = TW + 4;
   __shared__ uint8_t tile[R * PITCH];
@@ -254,22 +257,47 @@ __device__ void quant_tile_t(const void* src, int64_t rows, int64_t cols, uint8_
   const int64_t r0 = (int64_t)(t / ntc) * R, c0 = (int64_t)(t % ntc) * TW;
   const int tid = threadIdx.x, rr = tid / LPR, sub = tid % LPR;
   {
-    const int64_t r = r0 + rr < rows ? r0 + rr : rows - 1;
+    const bool ok = r0 + rr < rows;
+    const int64_t r = ok ? r0 + rr : rows - 1;
     float v[kVE];
     load16<DT, HQ_NT_Q_LD>(static_cast<const char*>(src) + (r * cols + c0 + sub * kVE) * EB, v);
     fwht16<LOG2B>(v, tid & 63);
+    uint32_t y[kVE], dh[kVE / 2];
+#pragma unroll
+    for (int e = 0; e < kVE; e += 2) {
+      uint32_t h[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const float x = v[e + u] * inv;
+        if constexpr (LSQ) {
+          const float rc = __builtin_amdgcn_fmed3f(x, -7.0f, 7.0f);
+          const float m = rc + kRne;
+          y[e + u] = __float_as_uint(m);
+          const float q = m - kRne;
+          const float d = (rc == x) ? q - x : q;
+          h[u] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)d);
+        } else {
+          y[e + u] = rne_bits(x);
+          h[u] = 0u;
+        }
+      }
+      dh[e / 2] = h[0] | (h[1] << 16);
+    }
+    const int64_t c = (c0 + sub * kVE) / kVE;  // 16-column chunk of the row
+    if (ok) {
+      st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(packed + r * (cols / 2)) + c,
+                             make_uint2(pack8_bits(y), pack8_bits(y + 8)));
+      if constexpr (LSQ) {
+        uint4* dp = reinterpret_cast<uint4*>(delta + r * cols) + 2 * c;
+        st_stream<HQ_NT_Q_ST>(dp, make_uint4(dh[0], dh[1], dh[2], dh[3]));
+        st_stream<HQ_NT_Q_ST>(dp + 1, make_uint4(dh[4], dh[5], dh[6], dh[7]));
+      }
+    }
     uint32_t* row = reinterpret_cast<uint32_t*>(tile + rr * PITCH + sub * kVE);
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      uint32_t b = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x = v[4 * w + e] * inv;
-        const uint32_t y = LSQ ? __float_as_uint(__builtin_amdgcn_fmed3f(x, -7.0f, 7.0f) + kRne) : rne_bits(x);
-        b |= (y & 15u) << (8 * e);
-      }
-      row[w] = b;
-    }
+    for (int w = 0; w < 4; ++w)
+      row[w] = (y[4 * w] & 15u) | ((y[4 * w + 1] & 15u) << 8) | ((y[4 * w + 2] & 15u) << 16) |
+               ((y[4 * w + 3] & 15u) << 24);
   }
   __syncthreads();
   const int d = tid / (R / 16), q = tid % (R / 16);
@@ -277,13 +305,13 @@ __device__ void quant_tile_t(const void* src, int64_t rows, int64_t cols, uint8_
     uint32_t w2[2] = {0u, 0u};
 #pragma unroll
     for (int i = 0; i < 16; ++i) w2[i >> 3] |= (uint32_t)tile[(16 * q + i) * PITCH + d] << (4 * (i & 7));
-    *reinterpret_cast<uint2*>(dst + (c0 + d) * (rows / 2) + r0 / 2 + 8 * q) = make_uint2(w2[0], w2[1]);
+    *reinterpret_cast<uint2*>(packed_t + (c0 + d) * (rows / 2) + r0 / 2 + 8 * q) = make_uint2(w2[0], w2[1]);
   }
 }
 
 // Codes of FWHT(rows) at the reduced maximum a; the first workgroup of each job also
-// stores a.  Workgroups past the two jobs' row workgroups write job 1's transposed codes
-// (one tile each) when o1.packed_t is set.  Row sums of squares are plain stores by the group's first lane.  The clamp
+// stores a.  When o1.packed_t is set, job 1 has no row workgroups (j1.wg = 0): workgroups
+// past job 0's quantise it by tiles (quant_tile), writing its codes and their transpose.  Row sums of squares are plain stores by the group's first lane.  The clamp
 // to +-7 of the definition never engages here: |v| <= a gives |v * fl(7/a)| <= 7 (1 + 2^-24),
 // which rounds to at most 7.
 template <int DT, int LOG2B>
@@ -291,8 +319,10 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
   constexpr int U = 4;
   if ((int)blockIdx.x >= j0.wg + j1.wg) {  // uniform per workgroup
     const float a = reduce_parts(o1.part, o1.nparts);
-    quant_tile_t<DT, LOG2B, false>(j1.src, j1.rows, j1.cols, o1.packed_t, a > 0.f ? 7.0f / a : 0.f,
-                                   (int)blockIdx.x - j0.wg - j1.wg);
+    const int t = (int)blockIdx.x - j0.wg - j1.wg;
+    if (t == 0 && threadIdx.x == 0) *o1.amax_out = a;
+    quant_tile<DT, LOG2B, false>(j1.src, j1.rows, j1.cols, a > 0.f ? 7.0f / a : 0.f, t, o1.packed,
+                                 nullptr, o1.packed_t);
     return;
   }
   const bool second = (int)blockIdx.x >= j0.wg;
@@ -355,14 +385,15 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_lsq_kernel(QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
   constexpr int U = 4;
-  {  // workgroups past the row workgroups: job 1's transposed codes, one tile each
+  {  // o1.packed_t set: job 1 by tiles (j1.wg = 0), one tile per workgroup past job 0's
     const int nrow = j0.wg * j0.batch + j1.wg * j1.batch;
     if ((int)blockIdx.x >= nrow) {  // uniform per workgroup
       const int nt = (int)TileT<LOG2B>::tiles(j1.rows, j1.cols);
       const int tt = (int)blockIdx.x - nrow, b = tt / nt;
-      quant_tile_t<DT, LOG2B, true>(
-          static_cast<const char*>(j1.src) + (int64_t)b * j1.bstride * Elem<DT>::bytes, j1.rows, j1.cols,
-          o1.packed_t + (int64_t)b * j1.cols * (j1.rows / 2), 1.0f / o1.step[b], tt % nt);
+      const int64_t rc = j1.rows * j1.cols;  // elements of one batch
+      quant_tile<DT, LOG2B, true>(static_cast<const char*>(j1.src) + (int64_t)b * j1.bstride * Elem<DT>::bytes,
+                                  j1.rows, j1.cols, 1.0f / o1.step[b], tt % nt, o1.packed + b * (rc / 2),
+                                  o1.delta + b * rc, o1.packed_t + b * (rc / 2));
       return;
     }
   }
@@ -869,8 +900,15 @@ template <int DT, int LOG2B> struct AbsmaxF {
 template <int DT, int LOG2B> struct QuantF {
   static hipError_t run(hipStream_t s, QJob j0, QJob j1, QOut o0, QOut o1) {
     const void* f = reinterpret_cast<const void*>(&fwht_quant_kernel<DT, LOG2B>);
-    fit_grid(j0, j1, resident_wgs(f));
-    const int64_t nt = o1.packed_t ? TileT<LOG2B>::tiles(j1.rows, j1.cols) : 0;
+    int64_t nt = 0;
+    if (o1.packed_t) {  // job 1 by tiles only
+      QJob none = make_job(nullptr, 0, j1.cols);
+      fit_grid(j0, none, resident_wgs(f));
+      j1.wg = 0;
+      nt = TileT<LOG2B>::tiles(j1.rows, j1.cols);
+    } else {
+      fit_grid(j0, j1, resident_wgs(f));
+    }
     timing_begin(s);
     fwht_quant_kernel<DT, LOG2B><<<(unsigned)(j0.wg + j1.wg + nt), kQThreads, 0, s>>>(j0, j1, o0, o1);
     timing_end(s, kKQuant);
@@ -881,8 +919,15 @@ template <int DT, int LOG2B> struct QuantF {
 template <int DT, int LOG2B> struct LsqF {
   static hipError_t run(hipStream_t s, QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
     const void* f = reinterpret_cast<const void*>(&fwht_lsq_kernel<DT, LOG2B>);
-    fit_grid(j0, j1, resident_wgs(f));
-    const int64_t nt = o1.packed_t ? TileT<LOG2B>::tiles(j1.rows, j1.cols) * j1.batch : 0;
+    int64_t nt = 0;
+    if (o1.packed_t) {  // job 1 by tiles only
+      QJob none = make_job(nullptr, 0, j1.cols);
+      fit_grid(j0, none, resident_wgs(f));
+      j1.wg = 0;
+      nt = TileT<LOG2B>::tiles(j1.rows, j1.cols) * j1.batch;
+    } else {
+      fit_grid(j0, j1, resident_wgs(f));
+    }
     timing_begin(s);
     fwht_lsq_kernel<DT, LOG2B><<<(unsigned)(j0.wg * j0.batch + j1.wg * j1.batch + nt), kQThreads, 0, s>>>(
         j0, j1, o0, o1);
