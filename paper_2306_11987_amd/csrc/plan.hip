@@ -249,12 +249,16 @@ __device__ __forceinline__ void weighted8(uint32_t up, uint32_t dn, int wu, int 
 }
 
 // One pass over the kept tokens builds every GEMM operand the sample selects: workgroup
-// (x, y) takes kept indices [64 x, 64 x + 64) and one 64-column block.  Blocks of the C
-// columns read q_up, q_dn and the weights, form A_t and write it row-major into Ag
-// (the dX operand) and, through an LDS transpose, column-major into At (the dW operand);
-// blocks of the D columns gather X^ rows into XtT.  The last block row zeroes the rows
-// of dX that belong to dropped tokens.  Rows of Ag and columns of At / XtT between n_kept
-// and the next multiple of 128 are written as zeros (the GEMMs read whole K steps).
+// (x, y) takes kept indices [128 x, 128 x + 128) and one block of up to 128 columns (the
+// last block of C or D may hold 64).  Blocks of the C columns read q_up, q_dn and the
+// weights, form A_t and write it row-major into Ag (the dX operand) and, through an LDS
+// transpose, column-major into At (the dW operand); blocks of the D columns gather X^ rows
+// into XtT.  Every row piece written is 128 bytes (64 for XtT), two full cache lines.
+// The last block row zeroes the rows of dX that belong to dropped tokens.  Rows of Ag and
+// columns of At / XtT between n_kept and the next multiple of 128 are written as zeros
+// (the GEMMs read whole K steps).
+constexpr int kBK = 128;  // kept indices per workgroup
+constexpr int kBC = 128;  // columns per workgroup
 template <int DT>
 __global__ __launch_bounds__(256) void build_operands_kernel(
     const uint8_t* __restrict__ qup, const uint8_t* __restrict__ qdn,
@@ -262,9 +266,9 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
     const int32_t* __restrict__ kept, const int32_t* __restrict__ n_kept,
     const uint8_t* __restrict__ xq, int64_t N, int64_t C, int64_t D, int8_t* __restrict__ Ag,
     int8_t* __restrict__ At, uint8_t* __restrict__ XtT, void* __restrict__ dX) {
-  __shared__ int8_t tile[64][65];  // [kept index][column]
+  __shared__ __attribute__((aligned(16))) int8_t tile[kBK][kBC + 4];  // [kept index][column]
   const int tid = threadIdx.x;
-  const int64_t cb = C / 64, db = D / 64;
+  const int64_t cb = (C + kBC - 1) / kBC, db = (D + kBC - 1) / kBC;
   {  // grid z: batch b of a batched call, every operand one block per batch
     const int64_t bt = blockIdx.z, kpad = (N + 127) / 128 * 128;
     qup += bt * N * (C / 2);
@@ -282,8 +286,8 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
   if ((int64_t)blockIdx.y == cb + db) {  // zero the dX rows of dropped tokens
     if (!dX) return;
     const int64_t bytes = D * Elem<DT>::bytes;
-    const int64_t t1 = (int64_t)blockIdx.x * 64 + 64 < N ? (int64_t)blockIdx.x * 64 + 64 : N;
-    for (int64_t t = (int64_t)blockIdx.x * 64 + (tid >> 6); t < t1; t += 4) {
+    const int64_t t0 = (int64_t)blockIdx.x * kBK, t1 = t0 + kBK < N ? t0 + kBK : N;
+    for (int64_t t = t0 + (tid >> 6); t < t1; t += 4) {
       if (w_up[t] + w_dn[t]) continue;
       char* row = static_cast<char*>(dX) + t * bytes;
       for (int64_t o = (tid & 63) * 16; o < bytes; o += 64 * 16)
@@ -293,19 +297,23 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
   }
   const int64_t nk = *n_kept;
   const int64_t kp = (nk + 127) / 128 * 128;
-  const int64_t i0 = (int64_t)blockIdx.x * 64;
+  const int64_t i0 = (int64_t)blockIdx.x * kBK;
   if (i0 >= kp) return;
   const int64_t pitch = (N + 127) / 128 * 128;  // K pitch of At (bytes) and 2x of XtT
   const bool isA = (int64_t)blockIdx.y < cb;
   if (isA ? (!Ag && !At) : !XtT) return;
-  const int64_t col0 = isA ? (int64_t)blockIdx.y * 64 : ((int64_t)blockIdx.y - cb) * 64;
-  {
-    const int r = tid >> 2, q = (tid & 3) * 16;  // 64 kept rows x 4 x 16 columns
+  const int64_t col0 = isA ? (int64_t)blockIdx.y * kBC : ((int64_t)blockIdx.y - cb) * kBC;
+  const int64_t ncol = isA ? C : D;
+  // 128 kept rows x 8 chunks of 16 columns, four per thread
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int item = tid + 256 * k, r = item >> 3, q = (item & 7) * 16;
     const int64_t i = i0 + r;
+    const bool inside = col0 + q < ncol;  // the last block of a 64-multiple width
     int v[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) v[j] = 0;
-    if (i < nk) {
+    if (i < nk && inside) {
       const int64_t t = kept[i];
       if (isA) {
         const int wu = w_up[t], wd = w_dn[t];
@@ -322,17 +330,23 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
         }
       }
     }
-    if (isA && Ag) {
+    if (isA && Ag && inside) {
       const uint2 lo = interleave8(v), hi = interleave8(v + 8);
       st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
     }
-    if (isA && !At) return;  // uniform: no transpose wanted
+    uint32_t* tp = reinterpret_cast<uint32_t*>(&tile[r][q]);  // 4-byte aligned: pitch 132
 #pragma unroll
-    for (int j = 0; j < 16; ++j) tile[r][q + j] = (int8_t)v[j];
+    for (int w = 0; w < 4; ++w)
+      tp[w] = ((uint32_t)v[4 * w] & 0xFFu) | (((uint32_t)v[4 * w + 1] & 0xFFu) << 8) |
+              (((uint32_t)v[4 * w + 2] & 0xFFu) << 16) | (((uint32_t)v[4 * w + 3] & 0xFFu) << 24);
   }
+  if (isA && !At) return;  // uniform: no transpose wanted
   __syncthreads();
-  {
-    const int c = tid >> 2, q = (tid & 3) * 16;  // 64 columns x 4 x 16 kept indices
+  // 128 columns x 8 chunks of 16 kept indices, four per thread
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int item = tid + 256 * k, c = item >> 3, q = (item & 7) * 16;
+    if (col0 + c >= ncol) continue;
     if (isA) {
       int a[16];
 #pragma unroll
@@ -379,7 +393,8 @@ hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, cons
                                  int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX,
                                  int64_t batch) {
   const int64_t pitch = (N + 127) / 128 * 128;
-  dim3 grid((unsigned)(pitch / 64), (unsigned)(C / 64 + D / 64 + 1), (unsigned)batch);
+  dim3 grid((unsigned)(pitch / kBK), (unsigned)((C + kBC - 1) / kBC + (D + kBC - 1) / kBC + 1),
+            (unsigned)batch);
   timing_begin(s);
   switch (dt) {
     case kF32:
