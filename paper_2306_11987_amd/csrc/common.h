@@ -234,11 +234,15 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
   return v;
 }
 
-// floor(sqrt(x)) for x < 2^64: a double estimate corrected by at most a few steps.
+// floor(sqrt(x)) for any 64-bit x: an estimate from the hardware double square root (one
+// instruction, not correctly rounded; the estimate is within a step or two of the root),
+// clamped to the 32-bit range and corrected in exact integers (no product overflows), so
+// the result is exact whatever the estimate's error.
 __device__ __forceinline__ uint32_t isqrt64(uint64_t x) {
-  uint64_t r = (uint64_t)sqrt((double)x);
+  uint64_t r = (uint64_t)__builtin_amdgcn_sqrt((double)x);
+  if (r > 0xFFFFFFFFull) r = 0xFFFFFFFFull;
   while (r * r > x) --r;
-  while ((r + 1) * (r + 1) <= x) ++r;
+  while (r < 0xFFFFFFFFull && (r + 1) * (r + 1) <= x) ++r;
   return (uint32_t)r;
 }
 

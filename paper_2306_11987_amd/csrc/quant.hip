@@ -547,16 +547,20 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
         if (++ip == g.iters) {  // end of the group's row
           su = group_sum(su, g.G);
           sd = group_sum(sd, g.G);
-          if (ok && g.sub == 0) {
-            o.sumsq_up[rb + r] = su;
-            o.sumsq_dn[rb + r] = sd;
+          // the group's lane 0 forms the upper row's score and lane 1 the lower row's
+          // (G >= 4), so a wave runs one square root per row end, not two in sequence
+          if (ok && g.sub < 2) {
             const uint64_t sx = (uint32_t)o.x_sumsq[rb + r];
-            const uint32_t cu = isqrt64(((uint64_t)(kBsRatio * kBsRatio) * (uint32_t)su * sx) << 16);
-            const uint32_t cd = isqrt64(((uint64_t)(uint32_t)sd * sx) << 16);
-            scores[r] = cu;
-            scores[o.score_pitch + r] = cd;
-            nnz += (cu > 0) + (cd > 0);
-            ssum += (uint64_t)cu + cd;
+            const bool upper = g.sub == 0;
+            const uint64_t k2 = upper ? (uint64_t)(kBsRatio * kBsRatio) * (uint32_t)su : (uint64_t)(uint32_t)sd;
+            const uint32_t c = isqrt64((k2 * sx) << 16);
+            if (upper) {
+              o.sumsq_up[rb + r] = su;
+              o.sumsq_dn[rb + r] = sd;
+            }
+            scores[(upper ? 0 : o.score_pitch) + r] = c;
+            nnz += c > 0;
+            ssum += c;
           }
           su = sd = 0;
           ip = 0;
