@@ -496,6 +496,9 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
   uint8_t* const qup = o.qup + rb * (C / 2);
   uint8_t* const qdn = o.qdn + rb * (C / 2);
   uint32_t* const scores = o.scores + (int64_t)b * 2 * o.score_pitch;
+  // a row's sums of squared codes are at most 49 C (codes within +-7); below 2^15 both fit
+  // one int in 16-bit halves without reaching its sign bit
+  const bool packed_sums = 49 * C < 32768;
   int64_t k = 0, kp = 0;
   int it = 0, ip = 0;
   int su = 0, sd = 0;
@@ -545,8 +548,14 @@ __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const floa
           st_stream2<HQ_NT_BS_ST>(reinterpret_cast<uint2*>(qdn) + o8, make_uint2(d0, d1));
         }
         if (++ip == g.iters) {  // end of the group's row
-          su = group_sum(su, g.G);
-          sd = group_sum(sd, g.G);
+          if (packed_sums) {  // one reduction of the two halves
+            const int p = group_sum(su | (sd << 16), g.G);
+            su = p & 0xFFFF;
+            sd = (int)((uint32_t)p >> 16);
+          } else {
+            su = group_sum(su, g.G);
+            sd = group_sum(sd, g.G);
+          }
           // the group's lane 0 forms the upper row's score and lane 1 the lower row's
           // (G >= 4), so a wave runs one square root per row end, not two in sequence
           if (ok && g.sub < 2) {
