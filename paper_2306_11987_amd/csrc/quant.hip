@@ -4,16 +4,19 @@
 //    unnormalised Hadamard transform of each row (radix-2 butterflies, strides ascending,
 //    fp32), then per-tensor absmax and INT4 codes clamp(rint(v * fl(7/a)), -7, 7)
 //    (Sec. 3.1, Eq. 2), packed two per byte (App. A.6) with per-row sums of squares
-//    (the ||X_i|| factor of the leverage score, Sec. 4.2).  One launch serves X and W,
-//    and its extra workgroups write W's codes transposed as well (the K-contiguous
-//    operand of the dX GEMM): each quantises one tile of W again and transposes it in LDS.
+//    (the ||X_i|| factor of the leverage score, Sec. 4.2).  One launch serves X and W:
+//    X by rows, W by tiles, each tile workgroup writing its codes row-major and also
+//    transposed through LDS (the K-contiguous operand of the dX GEMM), so W is read once.
 //  * fwht_lsq: the same transform quantised at a caller-given (learned) step in one pass,
-//    with the fp16 deltas q - I r that the learned-step backward needs (Eq. 2, App. A.4).
+//    with the fp16 deltas q - I r that the learned-step backward needs (Eq. 2, App. A.4);
+//    the second tensor by tiles as above.
 //  * bit_split: bit splitting of the output gradient (Sec. 4.2, Eq. 4): upper codes by
 //    round-to-nearest at s_up = a/7, lower codes by stochastic rounding of 14 x the exact
 //    residual (s_dn = s_up / 14), Philox stream 0.  It also forms the integer leverage
 //    scores of both stacked rows of every token and per-workgroup totals of them, which
-//    is all the sampler needs.
+//    is all the sampler needs.  At a row's end the group reduces the two row sums (one
+//    packed reduction for rows of at most 640 columns) and two of its lanes form the two
+//    scores, each with one integer square root.
 //
 // Work decomposition: a row belongs to a group of G lanes (G = the largest power of two
 // <= 64 dividing cols/16), so a wave holds 64/G rows and every per-row result (sum of
@@ -311,9 +314,10 @@ __device__ void quant_tile(const void* src, int64_t rows, int64_t cols, float in
 
 // Codes of FWHT(rows) at the reduced maximum a; the first workgroup of each job also
 // stores a.  When o1.packed_t is set, job 1 has no row workgroups (j1.wg = 0): workgroups
-// past job 0's quantise it by tiles (quant_tile), writing its codes and their transpose.  Row sums of squares are plain stores by the group's first lane.  The clamp
-// to +-7 of the definition never engages here: |v| <= a gives |v * fl(7/a)| <= 7 (1 + 2^-24),
-// which rounds to at most 7.
+// past job 0's quantise it by tiles (quant_tile), writing its codes and their transpose.
+// Row sums of squares are plain stores by the group's first lane.  The clamp to +-7 of the
+// definition never engages here: |v| <= a gives |v * fl(7/a)| <= 7 (1 + 2^-24), which
+// rounds to at most 7.
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1, QOut o0, QOut o1) {
   constexpr int U = 4;
