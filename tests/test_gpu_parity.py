@@ -205,6 +205,27 @@ def test_sampler_max_tokens():
     check_float_output("dW", dW, b.dW, dt)
 
 
+@pytest.mark.parametrize("N", [3000, 6000, 12000, 16384])
+def test_sampler_clamp_sizes(N):
+    """The clamp-and-rescale loop live (budget N/4) on both sides of the sampler's size
+    limits: the 256-thread build (N <= 4096) and the 1024-thread one; one or two
+    compaction rounds (N > 8192); up to the largest N whose scores the clamp rounds hold
+    in registers (2N = 32768; test_sampler_max_tokens covers the memory path).  Plan and
+    both gradients against the oracle."""
+    H = need_gpu()
+    lin, X, W, G = _case((N, 64, 128, 5, "f16", "lognormal"), seed=N)
+    D, C, k, dt = lin.D, lin.C, lin.log2_block, lin.dtype
+    say(f"sampler clamp at N={N}")
+    saved, _ = run_forward(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)
+    b = O.lss_backward(G, f, N // 4, 5, 7)
+    assert (b.plan.e_dn > 0).any()
+    _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N // 4, 5, 7)
+    check_plan(plan, b)
+    check_float_output("dX", dX, b.dX, dt)
+    check_float_output("dW", dW, b.dW, dt)
+
+
 @pytest.mark.parametrize("splits", [2, 3])
 def test_forced_split_k_parity(splits):
     """Every GEMM split along K into int32 partials and re-summed: still bit-exact."""
