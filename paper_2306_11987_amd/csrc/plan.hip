@@ -121,17 +121,28 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     int64_t k = 0;
     for (;;) {
       R = B - k;
+      // R c >= S  <=>  c >= ceil(S / R) for integers and R > 0: one division per round
+      // instead of a 64-bit product per score.  S = 0 admits every non-zero score (as
+      // R c >= 0 does); R = 0 with S > 0 admits none.
+      const uint64_t T = S == 0 ? 1 : R <= 0 ? ~uint64_t(0) : (S + (uint64_t)R - 1) / (uint64_t)R;
       uint64_t cnt = 0, sum = 0;
       if (in_regs) {
 #pragma unroll
         for (int j = 0; j < kPlanRegs; ++j) {
           const uint32_t c = cs[j];
-          if (c && (uint64_t)R * c >= S) { ++cnt; sum += c; }
+          if (c && c >= T) { ++cnt; sum += c; }
         }
-      } else {
-        for (int64_t i = tid; i < n2; i += kPlanThreads) {
-          const uint32_t c = scores[i < N ? i : pitch + (i - N)];
-          if (c && (uint64_t)R * c >= S) { ++cnt; sum += c; }
+      } else {  // eight loads in flight per thread
+        for (int64_t i0 = tid; i0 < n2; i0 += 8 * (int64_t)kPlanThreads) {
+          uint32_t c8[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int64_t i = i0 + (int64_t)u * kPlanThreads;
+            c8[u] = i < n2 ? scores[i < N ? i : pitch + (i - N)] : 0u;
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (c8[u] && c8[u] >= T) { ++cnt; sum += c8[u]; }
         }
       }
       block_sum2_u64<kPlanWaves>(cnt, sum, red);
