@@ -125,12 +125,18 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
       // instead of a 64-bit product per score.  S = 0 admits every non-zero score (as
       // R c >= 0 does); R = 0 with S > 0 admits none.
       const uint64_t T = S == 0 ? 1 : R <= 0 ? ~uint64_t(0) : (S + (uint64_t)R - 1) / (uint64_t)R;
-      uint64_t cnt = 0, sum = 0;
-      if (in_regs) {
+      // T >= 1, so c >= T implies c > 0; a threshold past the 32-bit scores admits none
+      const uint32_t T32 = (uint32_t)T;
+      uint32_t n = 0;
+      uint64_t sum = 0;
+      if (T > 0xFFFFFFFFull) {  // uniform
+      } else if (in_regs) {
 #pragma unroll
         for (int j = 0; j < kPlanRegs; ++j) {
           const uint32_t c = cs[j];
-          if (c && c >= T) { ++cnt; sum += c; }
+          const bool in = c >= T32;
+          n += in;
+          sum += in ? c : 0u;
         }
       } else {  // eight loads in flight per thread
         for (int64_t i0 = tid; i0 < n2; i0 += 8 * (int64_t)kPlanThreads) {
@@ -141,10 +147,14 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
             c8[u] = i < n2 ? scores[i < N ? i : pitch + (i - N)] : 0u;
           }
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
-            if (c8[u] && c8[u] >= T) { ++cnt; sum += c8[u]; }
+          for (int u = 0; u < 8; ++u) {
+            const bool in = c8[u] >= T32;
+            n += in;
+            sum += in ? c8[u] : 0u;
+          }
         }
       }
+      uint64_t cnt = n;
       block_sum2_u64<kPlanWaves>(cnt, sum, red);
       if ((int64_t)cnt == k) break;  // nothing newly clamped
       k = (int64_t)cnt;
@@ -171,9 +181,15 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
         if (all_nonzero_kept || rc >= S) {
           wd = 1;
         } else {
+          // e = min(cap, largest e with rc 2^e <= S), here 0 < rc < S: from the bit lengths
+          // of rc and S and one comparison
           const int cap = wu ? 2 : 4;
-          int e = 0;
-          while (e < cap && (rc << (e + 1)) <= S) ++e;
+          int e = cap;
+          if (rc != 0) {
+            const int e0 = __builtin_clzll(rc) - __builtin_clzll(S);
+            const int m = (rc << e0) <= S ? e0 : e0 - 1;
+            e = m < cap ? m : cap;
+          }
           wd = (u16_of(rnd, j) < (1u << (16 - e))) ? (1u << e) : 0u;
         }
       }
