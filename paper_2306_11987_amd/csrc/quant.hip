@@ -21,7 +21,7 @@
 // Work decomposition: a row belongs to a group of G lanes (G = the largest power of two
 // <= 64 dividing cols/16), so a wave holds 64/G rows and every per-row result (sum of
 // squares, scores) is one plain store: no atomics, nothing to pre-zero.  Each lane loads
-// 16 consecutive elements per step and keeps several steps in flight.  A Hadamard block
+// 16 consecutive elements per step and keeps two steps in flight.  A Hadamard block
 // of b = 2^k <= 128 columns lives in b/16 consecutive lanes of one group (b/16 <= G for
 // every admitted shape), so strides 1..8 run in registers and strides 16..64 are lane
 // exchanges folded into the butterfly add (DPP) or a swizzle.  Per-tensor maxima leave
@@ -192,7 +192,9 @@ template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_absmax_kernel(QJob j0, QJob j1,
                                                                 float* __restrict__ part0,
                                                                 float* __restrict__ part1) {
-  constexpr int U = 4;  // steps in flight
+  // steps in flight: 2 measured faster than 4 (fewer registers, more waves per SIMD;
+  // -5 % per FFN step's maximum passes, -9 % on the 4096..11008-wide sweep) and than 8
+  constexpr int U = 2;
   __shared__ float red[kQWaves];
   const QPos q = qpos(j0, j1);
   const QJob& j = q.second ? j1 : j0;
@@ -320,7 +322,7 @@ __device__ void quant_tile(const void* src, int64_t rows, int64_t cols, float in
 // rounds to at most 7.
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1, QOut o0, QOut o1) {
-  constexpr int U = 4;
+  constexpr int U = 2;  // steps in flight (2 measured faster than 4, as for the maximum)
   if ((int)blockIdx.x >= j0.wg + j1.wg) {  // uniform per workgroup
     const float a = reduce_parts(o1.part, o1.nparts);
     const int t = (int)blockIdx.x - j0.wg - j1.wg;
@@ -388,7 +390,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
 // from delta alone.
 template <int DT, int LOG2B>
 __global__ __launch_bounds__(kQThreads) void fwht_lsq_kernel(QJob j0, QJob j1, LsqOut o0, LsqOut o1) {
-  constexpr int U = 4;
+  constexpr int U = 2;
   {  // o1.packed_t set: job 1 by tiles (j1.wg = 0), one tile per workgroup past job 0's
     const int nrow = j0.wg * j0.batch + j1.wg * j1.batch;
     if ((int)blockIdx.x >= nrow) {  // uniform per workgroup
