@@ -481,7 +481,9 @@ template <int DT>
 __global__ __launch_bounds__(kQThreads) void bit_split_kernel(QJob j, const float* __restrict__ part,
                                                               int nparts, BsOut o, uint64_t seed,
                                                               uint64_t offset) {
-  constexpr int U = 2;
+  // one 16-element step per loop pass: the Philox state and the two code planes already
+  // hold many registers, and one step (more waves per SIMD) measured 9 % faster than two
+  constexpr int U = 1;
   __shared__ uint64_t red_s[kQWaves];
   __shared__ uint32_t red_n[kQWaves];
   // batch b of a batched job: its own maximum, outputs and Philox counter range
