@@ -68,6 +68,9 @@ def parse():
     p.add_argument("--workload", type=int, choices=sorted(WORKLOAD_KEYS), default=1,
                    help="1: BERT-base FFN pair (default); 2: GPT-2-medium linears; "
                         "3: GEMM sweep N=16384 (4096..11008, bf16); 4: BERT-large encoder block linears")
+    p.add_argument("--rotate", type=int, default=1, metavar="K",
+                   help="cycle the steps over K copies of the inputs at different addresses "
+                        "(no cross-step cache reuse; the bf16 comparison cycles likewise)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="before the steps, run the library's plain copy kernel once over MIB MiB "
                         "(reference for hardware traffic counters)")
@@ -170,7 +173,18 @@ def main():
                                  lin.budget, seed, offsets[i], e["ws"])
             offsets[i] += e["adv"]
 
+    # --rotate K: K copies of every input; step s reads copy s % K
+    rot = max(1, args.rotate)
+    for e in L:
+        e["sets"] = [(e["X"], e["W"], e["G"])] + [
+            (e["X"].clone(), e["W"].clone(), e["G"].clone()) for _ in range(rot - 1)]
+    cur = [0]
+
     def step():
+        if rot > 1:
+            for e in L:
+                e["X"], e["W"], e["G"] = e["sets"][cur[0] % rot]
+            cur[0] += 1
         fwd()
         bwd()
 
@@ -298,16 +312,15 @@ def main():
     # ---- bf16 reference: the same three GEMMs per linear through torch (hipBLASLt)
     bf16 = None
     if not args.no_bf16:
-        B = []
-        for e in L:
-            lin = e["lin"]
-            B.append((e["X"].to(torch.bfloat16), e["W"].to(torch.bfloat16), e["G"].to(torch.bfloat16)))
+        Bs = [[tuple(t.to(torch.bfloat16) for t in e["sets"][k]) for e in L] for k in range(rot)]
+        bcur = [0]
 
         def bstep():
-            for X, W, G in B:
+            for X, W, G in Bs[bcur[0] % rot]:
                 torch.matmul(X, W.t())
                 torch.matmul(G, W)
                 torch.matmul(G.t(), X)
+            bcur[0] += 1
 
         for _ in range(args.warmup):
             bstep()
@@ -345,6 +358,7 @@ def main():
         "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
         "ms_per_step_with_kernel_events": round(ms_step_events, 4),
         "us_per_step_fwd_bwd": [round(fwd_us, 1), round(bwd_us, 1)],
+        "input_sets": rot,
         "roofline": roof,
         "cpu_baseline": cpu,
         "hbm_kernels": hbm,
