@@ -1,14 +1,25 @@
 """Benchmark: INT4 HQ-MM / LSS-MM linear fwd+bwd on one MI355X.
 
 One step = forward (HQ-MM) and backward (LSS-MM: dX and dW from one shared sample) of
-both linears of the BERT-base FFN pair: N = 16384 tokens (batch 32 x seq 512),
-768 -> 3072 and 3072 -> 768, fp16 inputs, Hadamard block 32, LSS budget N.
-Inputs are seeded synthetic tensors with the paper's structure (outlier channels in X,
-heavy-tailed row norms in dY), resident in HBM before timing starts.
+every linear of the workload.  The default workload is the square and rectangular GEMM
+sweep: N = 16384 tokens, (D, C) = (4096, 4096), (4096, 11008), (11008, 4096),
+(8192, 8192), bf16 inputs, Hadamard block 128, LSS budget N.  Inputs are seeded
+synthetic tensors with the paper's structure (outlier channels in X, heavy-tailed row
+norms in dY), resident in HBM before timing starts; the steps cycle over enough copies
+of them that no step reads inputs a previous step left in the 256 MB MALL.
+
+Timing: W warm-up steps, then K timed steps with one HIP event pair per step; the step
+time is the median over the K steps (the wall-clock mean is printed beside it).
 
 Metric: effective TOPS = sum over linears of 6 N C D / step time (the dense-equivalent
 work of fwd + dX + dW), also as a fraction of the int8 MFMA peak, beside the same three
 GEMMs per linear in bf16 through torch (hipBLASLt) and the CPU oracle on a token slice.
+Each linear is also timed alone (`per_linear`), and the error of its outputs against
+the unquantised fp64 products is reported (`quant_error_vs_fp64`, untimed).
+
+--workload 1, 2 or 4 runs the same step on the other linear-layer workloads instead
+(the BERT-base FFN pair N = 16384; GPT-2-medium linears N = 8192; the BERT-large
+encoder block linears).
 
 --mode bmm times the attention BMM T = BMM(Q, K^T) of App. A.1 instead (per-batch learned
 steps, per-batch sampling): BERT-base attention scores, 32 sequences x 12 heads = 384
@@ -17,13 +28,9 @@ step; effective TOPS = 6 B N P M / step time, beside the same three products per
 bf16 torch.bmm.
 
 --mode lsq times the learned-step-size variant instead (Eq. 2 with caller-given steps,
-App. A.4 gradients including the step-size gradients), on the same workload with steps set
+App. A.3 gradients including the step-size gradients), on the same workload with steps set
 before timing to half of each tensor's dynamic step (s = max|V H| / 14, so the largest
 entries clip).
-
---workload 2, 3 or 4 runs the same step on the other linear-layer workloads instead
-(GPT-2-medium linears N = 8192; the GEMM sweep N = 16384 up to 11008 wide, bf16; the
-BERT-large encoder block linears).
 
 Prints ONE JSON line.
 """
@@ -42,6 +49,7 @@ sys.path.insert(0, ROOT)
 
 INT8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
 HBM_PEAK_GBS = 8000.0
+MALL_BYTES = 256 << 20  # MI355X last-level (Infinity) cache
 # vector ALU: 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz (the fp32 vector peak of
 # 157.3 TFLOP/s counts a packed FMA, 4 flops, per slot)
 VALU_PEAK_TSLOTS = 256 * 4 * 16 * 2.4e9 / 1e12
@@ -58,19 +66,22 @@ WORKLOAD_KEYS = {1: "bert_base_ffn", 2: "gpt2_medium", 3: "gemm_sweep", 4: "bert
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time")
     p.add_argument("--mode", choices=("dynamic", "lsq", "bmm"), default="dynamic",
                    help="quantiser: per-tensor maxima (default) or learned step sizes")
-    p.add_argument("--workload", type=int, choices=sorted(WORKLOAD_KEYS), default=1,
-                   help="1: BERT-base FFN pair (default); 2: GPT-2-medium linears; "
-                        "3: GEMM sweep N=16384 (4096..11008, bf16); 4: BERT-large encoder block linears")
-    p.add_argument("--rotate", type=int, default=1, metavar="K",
+    p.add_argument("--workload", type=int, choices=sorted(WORKLOAD_KEYS), default=3,
+                   help="1: BERT-base FFN pair; 2: GPT-2-medium linears; "
+                        "3: GEMM sweep N=16384 (4096..11008, bf16; default); 4: BERT-large encoder block linears")
+    p.add_argument("--rotate", type=int, default=0, metavar="K",
                    help="cycle the steps over K copies of the inputs at different addresses "
-                        "(no cross-step cache reuse; the bf16 comparison cycles likewise)")
+                        "(no cross-step cache reuse; the bf16 comparison cycles likewise); "
+                        "0 (default): enough copies that one cycle exceeds twice the 256 MB MALL")
+    p.add_argument("--no-error", action="store_true",
+                   help="skip the (untimed) error of the outputs against the unquantised fp64 products")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="before the steps, run the library's plain copy kernel once over MIB MiB "
                         "(reference for hardware traffic counters)")
@@ -99,6 +110,37 @@ def committed_traffic(kernel: str, workload: str):
     return float(m_b.group(1))
 
 
+def _median(xs):
+    s = sorted(xs)
+    n = len(s)
+    return 0.5 * (s[(n - 1) // 2] + s[n // 2]) if n else float("nan")
+
+
+def _timed_steps(torch, fn, steps):
+    """Run fn `steps` times with a HIP event pair around each call on the current stream
+    (the stream every library launch and torch op here is issued on).  Returns the wall
+    time of the whole bracket (synchronised on both sides) and the per-step event times."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3
+    return wall_ms, [a.elapsed_time(b) for a, b in evs]
+
+
+def _auto_rotation(L, eb):
+    """Copies of the inputs such that one cycle of them exceeds twice the 256 MB MALL:
+    a step then never reads inputs the previous steps left in the cache."""
+    set_bytes = sum(eb * (e["lin"].N * e["lin"].D + e["lin"].C * e["lin"].D + e["lin"].N * e["lin"].C)
+                    for e in L)
+    return max(1, -(-(2 * MALL_BYTES) // set_bytes))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -121,6 +163,7 @@ def main():
     lins = wl.linears
     N = lins[0].N
     tdt = {"f16": torch.float16, "bf16": torch.bfloat16, "f32": torch.float32}[lins[0].dtype]
+    eb = {"f16": 2, "bf16": 2, "f32": 4}[lins[0].dtype]
 
     # ---- inputs resident in HBM, state and workspaces preallocated
     L = []
@@ -153,37 +196,46 @@ def main():
             e["wsf"] = H.workspace(H.WS_FWD_LSQ, lin.N, lin.D, lin.C, dev)
         torch.cuda.synchronize()
 
+    def fwd_one(e):
+        if lsq_mode:
+            H.hq_linear_fwd_lsq(e["X"], e["W"], e["Y"], e["saved"], e["lsq"], e["lin"].log2_block,
+                                e["wsf"])
+        else:
+            H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
+
+    def bwd_one(i):
+        e = L[i]
+        lin = e["lin"]
+        if lsq_mode:
+            H.lss_linear_bwd_lsq(e["G"], e["saved"], e["lsq"], e["dX"], e["dW"], e["dstep"], lin.D,
+                                 lin.log2_block, lin.budget, seed, offsets[i], e["ws"])
+        else:
+            H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block,
+                             lin.budget, seed, offsets[i], e["ws"])
+        offsets[i] += e["adv"]
+
     def fwd():
         for e in L:
-            if lsq_mode:
-                H.hq_linear_fwd_lsq(e["X"], e["W"], e["Y"], e["saved"], e["lsq"], e["lin"].log2_block,
-                                    e["wsf"])
-            else:
-                H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
+            fwd_one(e)
 
     def bwd():
         for i in reversed(range(len(L))):
-            e = L[i]
-            lin = e["lin"]
-            if lsq_mode:
-                H.lss_linear_bwd_lsq(e["G"], e["saved"], e["lsq"], e["dX"], e["dW"], e["dstep"], lin.D,
-                                     lin.log2_block, lin.budget, seed, offsets[i], e["ws"])
-            else:
-                H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block,
-                                 lin.budget, seed, offsets[i], e["ws"])
-            offsets[i] += e["adv"]
+            bwd_one(i)
 
     # --rotate K: K copies of every input; step s reads copy s % K
-    rot = max(1, args.rotate)
+    rot = args.rotate if args.rotate > 0 else _auto_rotation(L, eb)
     for e in L:
         e["sets"] = [(e["X"], e["W"], e["G"])] + [
             (e["X"].clone(), e["W"].clone(), e["G"].clone()) for _ in range(rot - 1)]
     cur = [0]
 
+    def select(e, k):
+        e["X"], e["W"], e["G"] = e["sets"][k % rot]
+
     def step():
         if rot > 1:
             for e in L:
-                e["X"], e["W"], e["G"] = e["sets"][cur[0] % rot]
+                select(e, cur[0])
             cur[0] += 1
         fwd()
         bwd()
@@ -220,15 +272,12 @@ def main():
     H.timing_enable(False)
     ms_step_events = (t1 - t0) * 1e3 / args.steps
 
-    # untimed rerun of the same steps without event bracketing, for the headline time
+    # ---- the headline: the same steps again without per-kernel events; one event pair
+    # per step, the median step time reported (the wall time of all steps beside it)
     offsets[:] = step_offsets
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / args.steps
+    wall_ms, step_ms = _timed_steps(torch, step, args.steps)
+    ms_step = _median(step_ms)
+    ms_step_wall = wall_ms / args.steps
 
     ops_step = sum(6.0 * e["lin"].N * e["lin"].C * e["lin"].D for e in L)
     tops = ops_step / (ms_step * 1e-3) / 1e12
@@ -268,6 +317,7 @@ def main():
             ks.append(int(plan.n_kept.item()))
             off += e["adv"]
         kept.append(float(np.mean(ks)))
+        del plan, wsp
 
     # dominant kernel and its roofline
     dom = max(kernels, key=lambda k: kernels[k]["us_per_step"])
@@ -283,31 +333,85 @@ def main():
                 "unit": "TFLOP/s", "frac": round(ach / INT8_PEAK_TOPS, 4),
                 "traffic": committed_traffic(dom, WORKLOAD_KEYS[cfg_id] + ("_lsq" if lsq_mode else "")),
                 "algorithmic_ops_per_launch": algo,
-                "note": "int8 MFMA ops (multiply-adds x 2) of the kept-token GEMM"}
+                "note": "int8 MFMA ops (multiply-adds x 2) of the kept-token GEMM, averaged over "
+                        "the workload's linears; traffic: HBM bytes per launch from rocprofv3 "
+                        "FETCH_SIZE + WRITE_SIZE, calibrated on a copy kernel"}
+    gemms = {}
+    for nm in ("gemm_fwd", "gemm_dx", "gemm_dw"):
+        if nm not in kernels:
+            continue
+        if nm == "gemm_fwd":
+            ops = sum(2.0 * e["lin"].N * e["lin"].C * e["lin"].D for e in L)
+        else:
+            ops = sum(2.0 * k * e["lin"].C * e["lin"].D for k, e in zip(kept, L))
+        us = kernels[nm]["us_per_step"] + (kernels["gemm_reduce"]["us_per_step"]
+                                           if nm == "gemm_dw" and "gemm_reduce" in kernels else 0.0)
+        gemms[nm] = {"frac": round(ops / (us * 1e-6) / 1e12 / INT8_PEAK_TOPS, 4),
+                     "us_per_step": round(us, 1)}
 
-    # ---- memory-bound kernels against the HBM peak: algorithmic bytes of one step (every
-    # tensor read once and every result written once) over the kernel's time per step
-    ab = {}
-    eb = {"f16": 2, "bf16": 2, "f32": 4}[lins[0].dtype]
-    for e, kt in zip(L, kept):
-        N_, D_, C_ = e["lin"].N, e["lin"].D, e["lin"].C
-        if lsq_mode:  # one read, codes + fp16 deltas written, row sums of X
-            ab["lsq_quant"] = ab.get("lsq_quant", 0.0) + (eb + 2.5) * (N_ + C_) * D_ + 0.5 * C_ * D_ + 4 * N_
-        else:  # the maximum pass reads X and W; the quantiser reads them again, writes the
-            # codes of X, W and W^T
-            ab["fwht_absmax"] = ab.get("fwht_absmax", 0.0) + eb * (N_ + C_) * D_
-            ab["fwht_quant"] = ab.get("fwht_quant", 0.0) + (eb + 0.5) * (N_ + C_) * D_ + 0.5 * C_ * D_ + 4 * N_
-        ab["fwht_absmax"] = ab.get("fwht_absmax", 0.0) + eb * N_ * C_  # maximum of dY
-        # dY read; two INT4 code planes written; row sums and the two scores per token
-        ab["bit_split"] = ab.get("bit_split", 0.0) + (eb + 1.0) * N_ * C_ + 20 * N_
-        # codes of the kept rows read, A and A^T written; gathered X codes read and written
-        ab["build_operands"] = ab.get("build_operands", 0.0) + 3.0 * kt * C_ + 1.0 * kt * D_
+    # ---- memory-bound stages against the HBM peak, with algorithmic bytes of one read
+    # of each input and one write of each result (the second read of a dynamic per-tensor
+    # scale is implementation cost): F2+F3 (maximum + quantiser of X and W) and B1+B2
+    # (maximum + bit split of dY), each over the summed time of its kernels
+    stages = {}
+    if lsq_mode:
+        b_q = sum((eb + 2.5) * (e["lin"].N + e["lin"].C) * e["lin"].D + 0.5 * e["lin"].C * e["lin"].D
+                  + 4 * (e["lin"].N + e["lin"].C) for e in L)
+        stages["F2+F3 lsq_quant"] = (b_q, ["lsq_quant"])
+    else:
+        b_q = sum((eb + 0.5) * (e["lin"].N + e["lin"].C) * e["lin"].D + 0.5 * e["lin"].C * e["lin"].D
+                  + 4 * (e["lin"].N + e["lin"].C) for e in L)
+        stages["F2+F3 absmax+quant"] = (b_q, ["fwht_absmax:fwd", "fwht_quant"])
+    b_g = sum((eb + 1.0) * e["lin"].N * e["lin"].C + 8 * e["lin"].N for e in L)
+    stages["B1+B2 absmax+bit_split"] = (b_g, ["fwht_absmax:bwd", "bit_split"])
+    # the maximum kernel serves both F2 and B1: split its time by launch position
+    absmax_fwd = absmax_bwd = 0.0
+    if per_step * args.steps == len(log):
+        for st in range(args.steps):
+            chunk = log[st * per_step:(st + 1) * per_step]
+            for j, (kid, ms) in enumerate(chunk):
+                if H.kernel_name(kid) == "fwht_absmax":
+                    if j < n_fwd:
+                        absmax_fwd += 1e3 * ms
+                    else:
+                        absmax_bwd += 1e3 * ms
+        absmax_fwd /= args.steps
+        absmax_bwd /= args.steps
+    part_us = {"fwht_absmax:fwd": absmax_fwd, "fwht_absmax:bwd": absmax_bwd}
     hbm = {}
-    for nm, b in ab.items():
-        if nm in kernels:
-            gbs = b / (kernels[nm]["us_per_step"] * 1e-6) / 1e9
-            hbm[nm] = {"algorithmic_MB_per_step": round(b / 1e6, 2), "achieved_GBps": round(gbs, 1),
-                       "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    for stage, (b, ks) in stages.items():
+        us = sum(part_us[k] if k in part_us else kernels.get(k, {}).get("us_per_step", 0.0) for k in ks)
+        if us > 0:
+            gbs = b / (us * 1e-6) / 1e9
+            hbm[stage] = {"algorithmic_MB_per_step": round(b / 1e6, 2), "us_per_step": round(us, 1),
+                          "achieved_GBps": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    overhead = {k: round(kernels[k]["us_per_step"], 1)
+                for k in ("build_operands", "lss_plan", "gemm_reduce", "lsq_step_grad") if k in kernels}
+
+    # ---- per linear: that linear's fwd + bwd alone, median of per-step event times
+    per_linear = []
+    n_lin_steps = max(5, min(args.steps, 20))
+    for i, e in enumerate(L):
+        lin = e["lin"]
+        c = [0]
+
+        def lstep(e=e, i=i, c=c):
+            if rot > 1:
+                select(e, c[0])
+                c[0] += 1
+            fwd_one(e)
+            bwd_one(i)
+
+        for _ in range(2):
+            lstep()
+        _, ts = _timed_steps(torch, lstep, n_lin_steps)
+        ms_l = _median(ts)
+        ops_l = 6.0 * lin.N * lin.C * lin.D
+        per_linear.append({"D": lin.D, "C": lin.C, "ms": round(ms_l, 4),
+                           "tops": round(ops_l / (ms_l * 1e-3) / 1e12, 1),
+                           "frac_int8_peak": round(ops_l / (ms_l * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+                           "kept_tokens": round(kept[i], 1),
+                           "kept_over_budget": round(kept[i] / (lin.budget or lin.N), 4)})
 
     # ---- bf16 reference: the same three GEMMs per linear through torch (hipBLASLt)
     bf16 = None
@@ -324,14 +428,49 @@ def main():
 
         for _ in range(args.warmup):
             bstep()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            bstep()
-        torch.cuda.synchronize()
-        bms = (time.perf_counter() - t0) * 1e3 / args.steps
+        _, bts = _timed_steps(torch, bstep, args.steps)
+        bms = _median(bts)
         bf16 = {"ms_per_step": round(bms, 4), "tops": round(ops_step / (bms * 1e-3) / 1e12, 2),
                 "speedup_int4_over_bf16": round(bms / ms_step, 3)}
+        for i, e in enumerate(L):
+            c = [0]
+
+            def bl(i=i, c=c):
+                X, W, G = Bs[c[0] % rot][i]
+                torch.matmul(X, W.t())
+                torch.matmul(G, W)
+                torch.matmul(G.t(), X)
+                c[0] += 1
+
+            for _ in range(2):
+                bl()
+            _, ts = _timed_steps(torch, bl, n_lin_steps)
+            per_linear[i]["bf16_ms"] = round(_median(ts), 4)
+            per_linear[i]["speedup_int4_over_bf16"] = round(per_linear[i]["bf16_ms"] / per_linear[i]["ms"], 3)
+        del Bs
+
+    # ---- error of the outputs against the unquantised fp64 products (untimed): relative
+    # Frobenius norm of Y - X W^T, dX - dY W, dW - dY^T X for the last step's outputs
+    qerr = None
+    if not args.no_error:
+        qerr = []
+        for i, e in enumerate(L):
+            select(e, 0)
+            fwd_one(e)
+            bwd_one(i)
+            torch.cuda.synchronize()
+            X64, W64, G64 = (t.to(torch.float64) for t in (e["X"], e["W"], e["G"]))
+
+            def rel(got, ref):
+                return float(torch.linalg.norm(got.to(torch.float64) - ref) / torch.linalg.norm(ref))
+
+            r = {"D": e["lin"].D, "C": e["lin"].C,
+                 "Y": round(rel(e["Y"], X64 @ W64.t()), 4),
+                 "dX": round(rel(e["dX"], G64 @ W64), 4),
+                 "dW": round(rel(e["dW"], G64.t() @ X64), 4)}
+            qerr.append(r)
+            del X64, W64, G64
+            torch.cuda.empty_cache()
 
     # ---- CPU oracle on a bounded token slice of the same workload
     cpu = None
@@ -356,12 +495,19 @@ def main():
                    "quantizer": "lsq (s = max|V H| / 14)" if lsq_mode else "per-tensor max",
                    "kept_tokens": [round(k, 1) for k in kept]},
         "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
+        "timing": "median of per-step HIP-event times over the timed steps",
+        "ms_per_step_wall_mean": round(ms_step_wall, 4),
+        "ms_per_step_min_max": [round(min(step_ms), 4), round(max(step_ms), 4)],
         "ms_per_step_with_kernel_events": round(ms_step_events, 4),
         "us_per_step_fwd_bwd": [round(fwd_us, 1), round(bwd_us, 1)],
         "input_sets": rot,
         "roofline": roof,
         "cpu_baseline": cpu,
-        "hbm_kernels": hbm,
+        "gemm_frac_int8_peak": gemms,
+        "hbm_stages": hbm,
+        "overhead_us_per_step": overhead,
+        "per_linear": per_linear,
+        "quant_error_vs_fp64": qerr,
         "bf16": bf16,
         "kernels": {k: {kk: round(vv, 3) for kk, vv in v.items()} for k, v in sorted(kernels.items())},
     }
@@ -523,51 +669,106 @@ def cpu_baseline_bmm(np, synth, target_s: float):
             "seconds": round(t, 2)}
 
 
+def _host_info():
+    """CPU model and the cores this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        nproc = os.cpu_count() or 1
+    return model, nproc
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        return 1
+
+
 def cpu_baseline(lins, cfg_id: int, target_s: float, lsq_mode: bool = False):
-    """The oracle, as it stands, on the first n tokens of each linear (fwd + bwd)."""
+    """The oracle, as it stands, on the first n tokens of the workload's linears: the
+    forward, the dX backward and the dW backward each timed three times (median), linear
+    after linear until about target_s of CPU work is spent (at least one linear)."""
     import numpy as np
 
     import oracle as O
     import synth
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        threads = 1
-
-    def run(n):
-        ops = 0.0
-        t = 0.0
-        for li, lin in enumerate(lins):
+    def ops_of(n, lin):
+        if lsq_mode:
+            k = lin.log2_block
+            sub = synth.Linear(lin.name, n, lin.D, lin.C, k, lin.dtype, lin.x_outlier_channels,
+                               lin.x_outlier_scale, lin.grad_kind, n)
+            X, W, G = synth.linear_inputs(sub, cfg_id, lins.index(lin))
+            sx = O.absmax(O.fwht_rows(X, k)) / np.float32(14.0)
+            sw = O.absmax(O.fwht_rows(W, k)) / np.float32(14.0)
+            fw = lambda: O.lsq_forward(X, W, k, sx, sw)
+            f = fw()
+            dx = lambda: O.lsq_backward(G, f, n, 0, 0, need_dw=False)
+            dw = lambda: O.lsq_backward(G, f, n, 0, 0, need_dx=False)
+        else:
             sub = synth.Linear(lin.name, n, lin.D, lin.C, lin.log2_block, lin.dtype,
                                lin.x_outlier_channels, lin.x_outlier_scale, lin.grad_kind, n)
-            X, W, G = synth.linear_inputs(sub, cfg_id, li)
-            t0 = time.perf_counter()
-            if lsq_mode:
-                k = lin.log2_block
-                sx = O.absmax(O.fwht_rows(X, k)) / np.float32(14.0)
-                sw = O.absmax(O.fwht_rows(W, k)) / np.float32(14.0)
-                f = O.lsq_forward(X, W, k, sx, sw)
-                O.lsq_backward(G, f, n, 0, 0)
-            else:
-                f = O.hq_forward(X, W, lin.log2_block)
-                O.lss_backward(G, f, n, 0, 0)
-            t += time.perf_counter() - t0
-            ops += 6.0 * n * lin.C * lin.D
-        return t, ops
+            X, W, G = synth.linear_inputs(sub, cfg_id, lins.index(lin))
+            fw = lambda: O.hq_forward(X, W, lin.log2_block)
+            f = fw()
+            dx = lambda: O.lss_backward(G, f, n, 0, 0, need_dw=False)
+            dw = lambda: O.lss_backward(G, f, n, 0, 0, need_dx=False)
+        return fw, dx, dw
 
-    n = 256
-    t, ops = run(n)
-    for _ in range(3):  # grow the slice until it is about target_s of CPU work
-        if t >= 0.7 * target_s or n >= lins[0].N:
+    def med3(fn):
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return _median(ts), sum(ts)
+
+    def run(n):
+        spent = 0.0
+        per_op = {"fwd": 0.0, "dx": 0.0, "dw": 0.0}
+        ops = 0.0
+        used = []
+        for lin in lins:
+            if used and spent >= target_s:
+                break
+            for name, fn in zip(("fwd", "dx", "dw"), ops_of(n, lin)):
+                m, t = med3(fn)
+                per_op[name] += m
+                spent += t
+            ops += 6.0 * n * lin.C * lin.D
+            used.append(f"{lin.D}x{lin.C}")
+        return per_op, ops, used, spent
+
+    n = min(256, lins[0].N)
+    per_op, ops, used, spent = run(n)
+    for _ in range(3):  # a larger token slice while the sample is well under target_s
+        if spent >= 0.3 * target_s or n >= lins[0].N:
             break
-        n = int(min(lins[0].N, max(n + 64, n * target_s / max(t, 1e-3))) // 64 * 64)
-        t, ops = run(n)
-    return {"value": round(ops / t / 1e12, 6), "unit": "TOPS", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {n} of {lins[0].N} tokens of each linear, fwd + bwd (budget = {n}"
-                      f"{', learned step sizes' if lsq_mode else ''}); "
-                      f"{t:.1f} s", "seconds": round(t, 2)}
+        n = int(min(lins[0].N, max(2 * n, n * 0.7 * target_s / max(spent, 1e-3))) // 64 * 64)
+        per_op, ops, used, spent = run(n)
+    total = sum(per_op.values())
+    model, nproc = _host_info()
+    return {"value": round(ops / total / 1e12, 6), "unit": "TOPS", "cores": int(_blas_threads()),
+            "kind": "oracle",
+            "sample": f"first {n} of {lins[0].N} tokens of the linears {', '.join(used)} (of "
+                      f"{len(lins)}), fwd, dX and dW each the median of 3 runs (budget = {n}"
+                      f"{', learned step sizes' if lsq_mode else ''}); {spent:.1f} s of CPU work",
+            "median_s_per_op": {k: round(v, 3) for k, v in per_op.items()},
+            "cpu_model": model, "nproc": nproc,
+            "threads_note": "cores = BLAS threads of the integer products; the oracle's "
+                            "element-wise numpy steps run on one thread",
+            "seconds": round(spent, 2)}
 
 
 if __name__ == "__main__":

@@ -39,7 +39,8 @@
  *             non-zero hqlss_status is returned and nothing is enqueued.  A failed
  *             launch returns HQLSS_ERR_HIP.  No C++ exception crosses this ABI.
  * Threads     Calls may be issued from several host threads on different streams, with
- *             distinct buffers; the kernel-timing facility below is single-threaded.
+ *             distinct buffers.  The test hooks and the kernel-timing log below are
+ *             per calling thread.
  * RNG         Philox4x32-10 (Salmon et al., SC'11) with key = (lo32(seed), hi32(seed)) and
  *             counter = (lo32(blk), hi32(blk), stream, 0), blk = offset + (i >> 3);
  *             element i uses 16-bit half (i & 1) of output word ((i >> 1) & 3).
@@ -98,7 +99,7 @@ typedef struct {
   float *amax_g;     /* [1]       a_g = max|dY|  (s_up = a_g / 7, s_dn = s_up / 14)      */
 } lss_plan_t;
 
-/* Learned-step-size (LSQ) mode (Sec. 3.1, Eq. 2; App. A.4): static step sizes given by the
+/* Learned-step-size (LSQ) mode (Sec. 3.1, Eq. 2; App. A.3): static step sizes given by the
  * caller instead of the per-tensor maxima.  step holds s_X, s_W as device fp32 scalars, the
  * steps of the transformed tensors X H_u and W H_u (unnormalised Hadamard domain, so a code
  * q stands for s q there); each must be finite and at least 2^-126, else the codes are
@@ -152,7 +153,7 @@ hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int
                            void *stream);
 
 /* HQ-MM forward with learned step sizes (Sec. 3.3 Procedure HQ-MM with step 2 done by LSQ,
- * Eq. 2; App. A.4).
+ * Eq. 2; App. A.3).
  *   1. v_x = X H_u, v_w = W H_u in fp32, as hq_linear_fwd;
  *   2. r = fl(v fl(1/s)), codes clamp(rint(r), -7, 7) -> saved; delta -> lsq (one pass,
  *      no maximum);
@@ -247,7 +248,7 @@ hqlss_status lss_linear_bwd_dw(const void *dY, const hqlss_saved_t *saved, void 
                                int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
                                size_t ws_bytes, void *stream);
 
-/* LSS-MM backward of the learned-step-size forward (Sec. 4, App. A.4): the sample and
+/* LSS-MM backward of the learned-step-size forward (Sec. 4, App. A.3): the sample and
  * bit split of lss_linear_bwd, then with the unmasked integer accumulators acc_dx = A_T W^
  * and acc_dw = A_T^T X^_T
  *   dX[t] = fl(alpha_dx * FWHT_b(I_X[t] o acc_dx[t])), dW = fl(alpha_dw * FWHT_b(I_W o acc_dw))
@@ -301,13 +302,16 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t *plan, const hqlss
                                   size_t ws_bytes, void *stream);
 
 /* Test hook: force the split-K factor of every integer GEMM (0 restores the built-in
- * choice).  Workspace sizes follow the factor in force when they are queried. */
+ * choice).  Workspace sizes follow the factor in force when they are queried.  The
+ * setting is per calling thread: it applies to the calls (and workspace queries) made
+ * by the thread that set it, and never to another thread's. */
 void hqlss_debug_set_gemm_splits(int splits);
 
 /* Test hook: force the workgroup tile width (128 or 256 output columns) of the forward
  * GEMMs and of the gradient GEMMs whose output is wider than 64 columns, where they are
  * not split along K; any other value restores the built-in choice.  Results do not depend
- * on the width.  Workspace sizes follow the width in force when they are queried. */
+ * on the width.  Workspace sizes follow the width in force when they are queried.  Per
+ * calling thread, as the split hook. */
 void hqlss_debug_set_gemm_tile_n(int bn);
 
 /* Benchmark hook: a plain device-to-device copy kernel ("copy") of `bytes` bytes (a
@@ -319,7 +323,8 @@ hqlss_status hqlss_debug_copy(const void *src, void *dst, size_t bytes, void *st
 /* ---- kernel timing (benchmarks) ------------------------------------------------------
  * When enabled, every kernel the library launches is bracketed by two HIP events
  * recorded on the launch stream.  hqlss_timing_read waits for them, writes up to `cap`
- * (kernel id, milliseconds) pairs and clears the log; hqlss_kernel_name maps ids. */
+ * (kernel id, milliseconds) pairs and clears the log; hqlss_kernel_name maps ids.  The
+ * log is per calling thread: a thread records and reads only its own launches. */
 hqlss_status hqlss_timing_enable(int on);
 int hqlss_timing_read(int *ids, float *ms, int cap);
 const char *hqlss_kernel_name(int id);

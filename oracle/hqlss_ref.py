@@ -465,7 +465,7 @@ def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: 
 
 
 # --------------------------------------------------------------------------
-# Learned step size mode (Sec. 3.1 Eq. 2, Sec. 4, App. A.4)
+# Learned step size mode (Sec. 3.1 Eq. 2, Sec. 4, App. A.3)
 # --------------------------------------------------------------------------
 # Readings (listed with their reasons in the design notes):
 # * the caller's step sizes s_x, s_w belong to the unnormalised transform v = V H_u
@@ -473,7 +473,7 @@ def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: 
 #   exactly as in the dynamic mode;
 # * v / s is taken as r = fl(v * fl(1/s)) in float32, codes clamp(rint(r), -7, 7);
 # * the clip mask of Sec. 4 is taken on r: I = [-7 <= r <= 7] (Hadamard domain);
-# * delta(s) = int_s(v) - I o (v / s) of App. A.4 is formed as q - I r (exact in float32)
+# * delta(s) = int_s(v) - I o (v / s) of App. A.3 is formed as q - I r (exact in float32)
 #   and kept as float16, in place of the fp16 copy of the input that the paper's
 #   implementation keeps for the LSQ backward (App. A.6); |delta| <= 1/2 inside the range
 #   and |delta| = 7 where clipped,
@@ -481,14 +481,14 @@ def lss_backward(G: np.ndarray, fwd: HQForward, budget: int, seed: int, offset: 
 # * the STE gradients mask the integer accumulators in the Hadamard domain, then apply
 #   H^T (mask first: chain rule), and the step-size gradients are
 #   grad s = g(s) (s_other s_dn / 2^k) sum(acc o delta), g(s) = 1 / sqrt(Q_P numel),
-#   the chain rule through s q (App. A.4), with grad_Y replaced by the LSS estimate.
+#   the chain rule through s q (App. A.3), with grad_Y replaced by the LSS estimate.
 
 
 def quantize_lsq(v: np.ndarray, s: float):
     """int_s(v) = round(clamp(v / s, -7, 7)) with a given step s > 0 (Eq. 2).
 
     Returns (codes int8, mask bool, delta float16): the clip mask I of Sec. 4 and
-    delta = q - I o (v / s) of App. A.4 (see the readings above)."""
+    delta = q - I o (v / s) of App. A.3 (see the readings above)."""
     v = np.asarray(v, dtype=np.float32)
     s = np.float32(s)
     assert s > 0 and np.isfinite(s)
@@ -501,7 +501,7 @@ def quantize_lsq(v: np.ndarray, s: float):
 
 
 def lsq_grad_scale(numel: int) -> float:
-    """g(s) = 1 / sqrt(Q_P numel), the step-size gradient scale of App. A.4."""
+    """g(s) = 1 / sqrt(Q_P numel), the step-size gradient scale of App. A.3."""
     return 1.0 / math.sqrt(QMAX * int(numel))
 
 
@@ -554,7 +554,7 @@ class LSQBackward:
 def lsq_backward(G: np.ndarray, fwd: LSQForward, budget: int, seed: int, offset: int,
                  need_dx: bool = True, need_dw: bool = True,
                  delta_x: np.ndarray = None, delta_w: np.ndarray = None) -> LSQBackward:
-    """Gradients of HQ-MM with learned step sizes by LSS-MM (Sec. 4, App. A.4).
+    """Gradients of HQ-MM with learned step sizes by LSS-MM (Sec. 4, App. A.3).
 
     grad_X = s_W (I_X o grad_Y W^) H^T, grad_W = s_X (grad_Y^T X^ o I_W) H^T, and the
     step-size gradients g(s) s_other sum(grad_Y W^ o delta_X) (resp. grad_Y^T X^ o

@@ -161,7 +161,9 @@ struct TimingLog {
   size_t used = 0;
   bool overflow = false;
 };
-TimingLog g_log;
+// Per calling thread: a benchmark hook, so concurrent callers on other threads neither
+// record into nor read another thread's log.
+thread_local TimingLog g_log;
 constexpr size_t kLogPairs = 4096;
 
 // ---------------------------------------------------------------- the two passes
@@ -340,7 +342,7 @@ hqlss_status do_bmm_bwd(const void* dT, const hqlss_saved_t* sv, const hqlss_bmm
     HQ_TRY(launch_gemm(s, kEpiDwL, dt, false, true, g, 1, nullptr));
   }
   const bool sq = dQ && dstep_q, sk = dK && dstep_k;
-  if (sq || sk) {  // g(s) = 1 / sqrt(Q_P numel) per batch (App. A.4)
+  if (sq || sk) {  // g(s) = 1 / sqrt(Q_P numel) per batch (App. A.3)
     const double gq = 1.0 / std::sqrt(7.0 * (double)N * (double)M);
     const double gk = 1.0 / std::sqrt(7.0 * (double)P * (double)M);
     HQ_TRY(launch_lsq_step_grad(s, px, sq ? d.tiles_dx : 0, pw, sk ? d.tiles_dw : 0, ag,
@@ -439,7 +441,7 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
     }
   }
   if (lsq && dstep) {
-    // g(s) = 1 / sqrt(Q_P numel) with Q_P = 7 (App. A.4)
+    // g(s) = 1 / sqrt(Q_P numel) with Q_P = 7 (App. A.3)
     const double gx = 1.0 / std::sqrt(7.0 * (double)N * (double)D);
     const double gw = 1.0 / std::sqrt(7.0 * (double)C * (double)D);
     HQ_TRY(launch_lsq_step_grad(s, px, px ? lsq_parts_dx(N, D, C) : 0, pw,

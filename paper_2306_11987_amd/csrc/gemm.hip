@@ -38,7 +38,7 @@
 // wait on this wave's own loads plus one barrier.
 // Epilogue: results are staged through LDS in row chunks so that each store instruction
 // writes contiguous 16-byte pieces of whole output rows.  The learned-step gradient
-// epilogues first sum acc * delta (fp64) and zero the clipped accumulators (App. A.4).
+// epilogues first sum acc * delta (fp64) and zero the clipped accumulators (App. A.3).
 // Grid z is either the split-K index (int32 partial tiles, summed by reduce_epilogue) or
 // the batch of a batched launch (per-batch operand and output strides).  Workgroups take
 // tiles in an XCD-aware order over the tiles with rows below the device-side row count.
@@ -502,7 +502,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_>::THREADS), (Cfg<BM, A4, WN, B
   const int nh = (C_::WN / 2) * (lane >> 5);
   double lsq_sum = 0.0;
   if constexpr (LSQ) {
-    // sum of acc * delta over this workgroup's valid entries, then the clip mask (App. A.4):
+    // sum of acc * delta over this workgroup's valid entries, then the clip mask (App. A.3):
     // both use the integer accumulator before the transform H^T.  Rows past M hold
     // re-read data and are skipped; N is a multiple of the block, so the mask never mixes
     // valid and invalid columns inside one transform.
@@ -703,7 +703,7 @@ __global__ __launch_bounds__(256) void reduce_epilogue_kernel(const int32_t* __r
   }
 }
 
-// Step-size gradients (App. A.4): ds = g(s) alpha sum(acc * delta) in fp64 over the
+// Step-size gradients (App. A.3): ds = g(s) alpha sum(acc * delta) in fp64 over the
 // per-workgroup partials, summed by one workgroup in a fixed order (deterministic).
 __global__ __launch_bounds__(256) void lsq_step_grad_kernel(const double* __restrict__ px, int64_t nx,
                                                             const double* __restrict__ pw, int64_t nw,
@@ -768,7 +768,9 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   return hipGetLastError();
 }
 
-int g_bn_override = 0;  // test hook: 128 or 256 forces that width (0: the rules below)
+// Test hooks, per calling thread (a forced width or split-K factor set by one thread
+// never reaches another thread's calls): 128 or 256 forces that width (0: the rules below).
+thread_local int g_bn_override = 0;
 
 // Workgroup tile width of a gradient GEMM: 64 for outputs at most 64 wide; 128 when the
 // 256-wide tiles would fill at most three quarters of one round of two workgroups per CU
@@ -874,7 +876,7 @@ hipError_t run_dt(hipStream_t s, int dt, const GemmArgs& g, int splits, int32_t*
 
 }  // namespace
 
-static int g_split_override = 0;
+static thread_local int g_split_override = 0;
 void gemm_set_split_override(int splits) { g_split_override = splits < 0 ? 0 : splits; }
 void gemm_set_tile_override(int bn) { g_bn_override = (bn == kMidBN || bn == kBN) ? bn : 0; }
 

@@ -8,7 +8,7 @@
 //    X by rows, W by tiles, each tile workgroup writing its codes row-major and also
 //    transposed through LDS (the K-contiguous operand of the dX GEMM), so W is read once.
 //  * fwht_lsq: the same transform quantised at a caller-given (learned) step in one pass,
-//    with the fp16 deltas q - I r that the learned-step backward needs (Eq. 2, App. A.4);
+//    with the fp16 deltas q - I r that the learned-step backward needs (Eq. 2, App. A.3);
 //    the second tensor by tiles as above.
 //  * bit_split: bit splitting of the output gradient (Sec. 4.2, Eq. 4): upper codes by
 //    round-to-nearest at s_up = a/7, lower codes by stochastic rounding of 14 x the exact
@@ -381,7 +381,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
 
 // Learned-step-size codes (Eq. 2 at a caller-given step, after the transform of Sec. 3.3):
 // r = fl(v * fl(1/s)), q = clamp(rint(r), -7, 7) and delta = q - [-7 <= r <= 7] r, the
-// term that the step-size gradient weights (App. A.4).  One pass: no maximum is needed.
+// term that the step-size gradient weights (App. A.3).  One pass: no maximum is needed.
 // The clamp comes first (med3), so the magic-number rounding only sees |x| <= 7, and
 // rint(clamp(r)) = clamp(rint(r)) as the bounds are integers.  q - r is exact in fp32 (q
 // and r lie within a factor of two of each other, or q = 0), then rounded to fp16 (to

@@ -1,4 +1,4 @@
-"""GPU parity of the learned-step-size mode (Eq. 2 with Sec. 3.3; App. A.4) through the C ABI.
+"""GPU parity of the learned-step-size mode (Eq. 2 with Sec. 3.3; App. A.3) through the C ABI.
 
 Bit-exact: codes, row sums, fp16 deltas, the sample.  Float outputs (Y, dX, dW): as in
 the dynamic mode, 1e-5 relative (fp32) or one unit in the last place of the output dtype

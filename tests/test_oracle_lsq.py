@@ -1,4 +1,4 @@
-"""Pins of the oracle's learned-step-size mode (Sec. 3.1 Eq. 2, Sec. 4, App. A.4).
+"""Pins of the oracle's learned-step-size mode (Sec. 3.1 Eq. 2, Sec. 4, App. A.3).
 
 Each pin ties the oracle to something other than itself: a textbook quantiser, the
 dynamic mode where the two must agree, the straight-through-estimator derivatives that
@@ -143,7 +143,7 @@ def test_lsq_gradients_equal_autograd(k):
 
 
 def test_lsq_grad_scale_values():
-    # g(s) = 1 / sqrt(Q_P * numel) with Q_P = 7 (App. A.4): 7 * 448 = 56^2, 7 * 28 = 14^2
+    # g(s) = 1 / sqrt(Q_P * numel) with Q_P = 7 (App. A.3): 7 * 448 = 56^2, 7 * 28 = 14^2
     assert O.lsq_grad_scale(448) == 1 / 56
     assert O.lsq_grad_scale(28) == 1 / 14
     # the autograd pin's shapes: 7 * 24 * 32 and 7 * 16 * 32
