@@ -133,17 +133,29 @@ def test_exact_reconstruction_on_gpu():
     assert np.array_equal(to_np(Y).astype(np.float64), exact)
 
 
-# (workload id, linear index) at full size: the benchmark's BERT-base FFN pair, and one
-# or two linears of each other workload (GPT-2-medium b = 128, the bf16 square/rectangular
-# sweep, the BERT-large block)
-FULL_SIZE = [(1, 0), (1, 1), (2, 0), (2, 3), (3, 2), (4, 0), (4, 4)]
+# (workload id, linear index) at full size: every distinct linear of the named workloads
+# (the BERT-large block's Q, K, V and O share one shape; Q stands for them)
+FULL_SIZE = [(1, 0), (1, 1), (2, 0), (2, 1), (2, 2), (2, 3), (3, 0), (3, 1), (3, 2), (3, 3),
+             (4, 0), (4, 4), (4, 5)]
+N_Y_ROWS, N_DX_TOKENS, N_DW_ROWS = 256, 256, 64
+
+
+def _acc_rows(H, which, plan, saved, N, D, C, rows, shape):
+    """Whole rows of one GEMM's int32 accumulators (hqlss_debug_gemm_acc), copied back."""
+    acc = torch.empty(*shape, dtype=torch.int32, device="cuda")
+    ws = H.workspace(H.WS_FWD if which == 0 else H.WS_FROM_PLAN, N, D, C)
+    H.debug_gemm_acc(which, plan, saved, acc, N, D, C, ws)
+    out = to_np(acc[torch.from_numpy(rows).cuda()])
+    del acc, ws
+    return out
 
 
 @pytest.mark.parametrize("case", FULL_SIZE, ids=lambda c: f"w{c[0]}_{synth.workload(c[0]).linears[c[1]].name}")
 def test_full_size_sampled(case):
     """A linear of a named workload at full size, in the configuration the benchmark uses
-    (budget N): codes of every row, the whole sample, and sampled output blocks checked
-    against the oracle computing them one by one."""
+    (budget N): the codes of every row and the whole sample bit for bit; whole int32
+    accumulator rows of all three GEMMs (sampled tokens and channels) bit for bit; sampled
+    output rows of Y, dX and dW against the oracle computing them one by one."""
     H = need_gpu()
     cid, li = case
     lin = synth.workload(cid).linears[li]
@@ -159,9 +171,13 @@ def test_full_size_sampled(case):
     assert np.array_equal(to_np(saved.wqT), O.pack_int4(f.wq.T.copy()))
     assert np.array_equal(to_np(saved.x_sumsq), f.x_sumsq.astype(np.int32))
     rng = np.random.default_rng(cid * 10 + li)
-    rows = rng.choice(N, 64, replace=False)
-    ref = float(f.s_x) * float(f.s_w) * 2.0 ** -k * (f.xq[rows].astype(np.float64) @ f.wq.T.astype(np.float64))
+    rows = np.sort(rng.choice(N, N_Y_ROWS, replace=False))
+    accf = f.xq[rows].astype(np.float64) @ f.wq.T.astype(np.float64)
+    got = _acc_rows(H, 0, None, saved, N, D, C, rows, (N, C))
+    assert np.array_equal(got, accf.astype(np.int32)), "forward int32 accumulator rows"
+    ref = float(f.s_x) * float(f.s_w) * 2.0 ** -k * accf
     check_float_output("Y rows", Y[torch.from_numpy(rows).cuda()], ref, dt)
+    del X, W
 
     seed, offset = 42, 1000
     b = O.lss_backward(G, f, N, seed, offset, need_dx=False, need_dw=False)
@@ -171,17 +187,22 @@ def test_full_size_sampled(case):
     A = b.A.astype(np.float64)
     kept = b.plan.kept
     a_dx, a_dw = b.alpha_dx, b.alpha_dw
-    # dX on sampled kept tokens and dropped tokens
-    toks = rng.choice(kept, 32, replace=False)
+    # dX: sampled kept tokens (accumulator rows sit at the tokens' positions in the kept list)
+    pos = np.sort(rng.choice(len(kept), min(N_DX_TOKENS, len(kept)), replace=False))
+    toks = kept[pos]
     accx = A[toks] @ f.wq.astype(np.float64)
+    got = _acc_rows(H, 1, plan, saved, N, D, C, pos, (N, D))
+    assert np.array_equal(got, accx.astype(np.int32)), "dX int32 accumulator rows"
     refx = a_dx * O.fwht_rows(accx.astype(np.int64), k).astype(np.float64)
     check_float_output("dX rows", dX[torch.from_numpy(toks).cuda()], refx, dt)
     dropped = np.setdiff1d(np.arange(N), kept)
     if len(dropped):
-        assert not dX[torch.from_numpy(dropped[:64]).cuda()].float().abs().sum().item()
-    # dW on sampled rows c (all D columns, so whole Hadamard blocks)
-    cs = rng.choice(C, 16, replace=False)
+        assert not dX[torch.from_numpy(dropped[:N_DX_TOKENS]).cuda()].float().abs().sum().item()
+    # dW: sampled rows c (all D columns, so whole Hadamard blocks)
+    cs = np.sort(rng.choice(C, N_DW_ROWS, replace=False))
     accw = A[kept][:, cs].T @ f.xq[kept].astype(np.float64)
+    got = _acc_rows(H, 2, plan, saved, N, D, C, cs, (C, D))
+    assert np.array_equal(got, accw.astype(np.int32)), "dW int32 accumulator rows"
     refw = a_dw * O.fwht_rows(accw.astype(np.int64), k).astype(np.float64)
     check_float_output("dW rows", dW[torch.from_numpy(cs).cuda()], refw, dt)
 
