@@ -148,20 +148,47 @@ __device__ __forceinline__ void fwht_lane(int* v, int lane) {
 
 // XCD-aware tile order.  The hardware dispatches workgroups to the 8 XCDs round-robin by
 // linear id, so workgroup b runs on XCD b % 8.  The T tiles (row-major, n fastest) are cut
-// into 8 contiguous chunks, one per XCD, and the j-th workgroup of XCD x takes position j
-// of chunk x: tiles in flight on one XCD then share their operand rows in its L2.  T counts
-// only the tiles with rows below M (the device-side row count of dX), so that the tiles
-// past it do not all fall on the last XCDs; workgroups beyond their chunk get no tile.
-// Returns false for those.  Small grids keep the plain order.  In a grid with a z extent
-// (split-K index or batch) the XCD of workgroup (b, z) is (b + z gridDim.x) % 8: every
-// class b % 8 still sits on one XCD within its z slice, so the chunks hold there too.
+// into 8 contiguous chunks, one per XCD, and the j-th workgroup of XCD x takes the j-th
+// tile of chunk x.  T counts only the tiles with rows below M (the device-side row count
+// of dX), so that the tiles past it do not all fall on the last XCDs; workgroups beyond
+// their chunk get no tile.  Returns false for those.  Small grids keep the plain order.
+// In a grid with a z extent (split-K index or batch) the XCD of workgroup (b, z) is
+// (b + z gridDim.x) % 8: every class b % 8 still sits on one XCD within its z slice, so
+// the chunks hold there too.
+//
+// Within a chunk, the whole tile rows are walked in column groups of G tiles: all rows of
+// the chunk for columns [0, G), then for [G, 2G), ...  The workgroups resident on one XCD
+// at a time (about 64) then cover a block of about 64 / G rows by G columns, so they share
+// G operand panels of one side and 64 / G of the other in that XCD's L2, instead of the
+// two rows by all columns of the plain order.  The chunk's partial first and last rows
+// come after its whole rows, in the plain order.
+template <int G>
+__device__ __forceinline__ int grouped_tile(int j, int s, int len, int tiles_n) {
+  const int rf = (s + tiles_n - 1) / tiles_n, rl = (s + len) / tiles_n;
+  if (rl - rf < 2) return s + j;
+  const int R = rl - rf, nfull = R * tiles_n, head = rf * tiles_n - s;
+  if (j < nfull) {
+    const int nfg = tiles_n / G;
+    if (j < nfg * R * G) {
+      const int g = j / (R * G), inner = j - g * (R * G);
+      return (rf + inner / G) * tiles_n + g * G + inner % G;
+    }
+    const int rem = j - nfg * R * G, gl = tiles_n - nfg * G;
+    return (rf + rem / gl) * tiles_n + nfg * G + rem % gl;
+  }
+  if (j < nfull + head) return s + (j - nfull);
+  return rl * tiles_n + (j - nfull - head);
+}
+
+template <int G>
 __device__ __forceinline__ bool tile_of(int T, int tiles_n, int& tm, int& tn) {
   const int b = blockIdx.x;
   int L = b;
   if (T >= 16) {
     const int x = b & 7, j = b >> 3, q = T >> 3, r = T & 7;
-    if (j >= q + (x < r ? 1 : 0)) return false;
-    L = x * q + min(x, r) + j;
+    const int len = q + (x < r ? 1 : 0);
+    if (j >= len) return false;
+    L = grouped_tile<G>(j, x * q + min(x, r), len, tiles_n);
   } else if (b >= T) {
     return false;
   }
@@ -263,7 +290,9 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_>::THREADS), (Cfg<BM, A4, WN, B
   const int tiles_n = (int)((g.N + BN - 1) / BN);
   const int t_valid = tiles_n * (int)((M + BM - 1) / BM);  // tiles with rows below M
   int tm, tn;
-  if (!tile_of(t_valid, tiles_n, tm, tn)) {  // whole workgroup: uniform exit before any barrier
+  // column groups: 4 tiles for INT4 x INT4 (the 256-wide B panels are twice the A panels),
+  // 8 for int8 x INT4 (equal panels)
+  if (!tile_of<A4 ? 4 : 8>(t_valid, tiles_n, tm, tn)) {  // uniform exit before any barrier
     if constexpr (LSQ) {
       if (tid == 0) g.ds_part[blockIdx.x] = 0.0;
     }
