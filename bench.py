@@ -80,6 +80,8 @@ def parse():
                    help="cycle the steps over K copies of the inputs at different addresses "
                         "(no cross-step cache reuse; the bf16 comparison cycles likewise); "
                         "0 (default): enough copies that one cycle exceeds twice the 256 MB MALL")
+    p.add_argument("--no-per-linear", action="store_true",
+                   help="skip timing each linear alone (profiling runs)")
     p.add_argument("--no-error", action="store_true",
                    help="skip the (untimed) error of the outputs against the unquantised fp64 products")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -108,6 +110,11 @@ def committed_traffic(kernel: str, workload: str):
     if not (m_src and m_b) or m_src.group(1) != gemm_source_digest():
         return None
     return float(m_b.group(1))
+
+
+def progress(msg):
+    """One progress line on stderr per finished stage (the JSON line stays alone on stdout)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
 def _median(xs):
@@ -181,6 +188,7 @@ def main():
                  adv=H.lss_philox_offset_advance(lin.N, lin.C))
         L.append(e)
     del X, W, G
+    progress(f"inputs resident: {wl.name}")
     seed = 0
     offsets = [0] * len(L)
     lsq_mode = args.mode == "lsq"
@@ -278,6 +286,7 @@ def main():
     wall_ms, step_ms = _timed_steps(torch, step, args.steps)
     ms_step = _median(step_ms)
     ms_step_wall = wall_ms / args.steps
+    progress(f"timed steps done: median {ms_step:.4f} ms per step")
 
     ops_step = sum(6.0 * e["lin"].N * e["lin"].C * e["lin"].D for e in L)
     tops = ops_step / (ms_step * 1e-3) / 1e12
@@ -391,7 +400,7 @@ def main():
     # ---- per linear: that linear's fwd + bwd alone, median of per-step event times
     per_linear = []
     n_lin_steps = max(5, min(args.steps, 20))
-    for i, e in enumerate(L):
+    for i, e in (() if args.no_per_linear else enumerate(L)):
         lin = e["lin"]
         c = [0]
 
@@ -413,6 +422,7 @@ def main():
                            "kept_tokens": round(kept[i], 1),
                            "kept_over_budget": round(kept[i] / (lin.budget or lin.N), 4)})
 
+    progress("per-linear timings done")
     # ---- bf16 reference: the same three GEMMs per linear through torch (hipBLASLt)
     bf16 = None
     if not args.no_bf16:
@@ -432,7 +442,7 @@ def main():
         bms = _median(bts)
         bf16 = {"ms_per_step": round(bms, 4), "tops": round(ops_step / (bms * 1e-3) / 1e12, 2),
                 "speedup_int4_over_bf16": round(bms / ms_step, 3)}
-        for i, e in enumerate(L):
+        for i, e in enumerate(L[:len(per_linear)]):
             c = [0]
 
             def bl(i=i, c=c):
@@ -472,10 +482,12 @@ def main():
             del X64, W64, G64
             torch.cuda.empty_cache()
 
+    progress("bf16 and error checks done")
     # ---- CPU oracle on a bounded token slice of the same workload
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(lins, cfg_id, args.cpu_seconds, lsq_mode)
+        progress("CPU baseline done")
 
     out = {
         "metric": METRIC,
