@@ -70,7 +70,9 @@ typedef enum {
   HQLSS_ERR_WORKSPACE = 6, /* ws_bytes smaller than hqlss_workspace_bytes(...)          */
   HQLSS_ERR_OVERFLOW = 7,  /* an int32 accumulator or an int64 score could overflow    */
   HQLSS_ERR_HIP = 8,       /* a HIP launch or runtime call failed                       */
-  HQLSS_ERR_ARG = 9        /* any other invalid argument (e.g. budget, which)           */
+  HQLSS_ERR_ARG = 9,       /* any other invalid argument (e.g. budget, which)           */
+  HQLSS_ERR_SCRATCH = 10   /* the shape needs more scratch than the static array holds
+                              (allocation-free entry point only)                         */
 } hqlss_status;
 
 /* State written by the forward pass and read by the backward pass: the codes X^ and W^,
@@ -151,6 +153,24 @@ hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int
                            int64_t C, hqlss_dtype dt, int log2_block,
                            const hqlss_saved_t *saved, void *ws, size_t ws_bytes,
                            void *stream);
+
+/* Allocation-free HQ-MM forward, for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.  Identical to
+ * hq_linear_fwd (same steps, arguments, layouts, results and errors) except that the
+ * workspace is not passed: the absmax and split-K partials live in a static device array of
+ * HQLSS_STATIC_SCRATCH_BYTES that the library owns, one copy per GPU, held until the
+ * process ends.  Nothing is allocated or freed by the call.
+ *   - HQLSS_ERR_SCRATCH when hqlss_workspace_bytes(HQLSS_WS_FWD, N, D, C) exceeds
+ *     HQLSS_STATIC_SCRATCH_BYTES (only small outputs over a long K split along K and need
+ *     more than the absmax partials); use hq_linear_fwd then.
+ *   - The array keeps the last call's contents; nothing in it needs to start at zero (every
+ *     partial is written before it is read).
+ *   - Calls that overlap on one GPU (several streams or threads) race on the array:
+ *     serialise them.  The current HIP device must be the device of `stream`. */
+#define HQLSS_STATIC_SCRATCH_BYTES ((size_t)8 << 20)
+hqlss_status hq_linear_fwd_noalloc(const void *X, const void *W, void *Y, int64_t N, int64_t D,
+                                   int64_t C, hqlss_dtype dt, int log2_block,
+                                   const hqlss_saved_t *saved, void *stream);
 
 /* HQ-MM forward with learned step sizes (Sec. 3.3 Procedure HQ-MM with step 2 done by LSQ,
  * Eq. 2; App. A.3).

@@ -15,6 +15,7 @@ WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN, WS_HSIZE = 0, 1, 2,
 WS_FWD_LSQ, WS_BWD_LSQ = 7, 8
 WS_BMM_FWD, WS_BMM_BWD = 0, 1
 BUDGET_KEEP_NONZERO = -1  # HQLSS_BUDGET_KEEP_NONZERO: keep every non-zero gradient row
+STATIC_SCRATCH_BYTES = 8 << 20  # HQLSS_STATIC_SCRATCH_BYTES: the allocation-free forward's scratch
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
 _vp, _i64, _u64, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int, ctypes.c_size_t
@@ -46,6 +47,8 @@ def _load() -> ctypes.CDLL:
         "hqlss_workspace_bytes": (_sz, [_int, _i64, _i64, _i64]),
         "hq_linear_fwd": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
                                _vp, _sz, _vp]),
+        "hq_linear_fwd_noalloc": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int,
+                                       ctypes.POINTER(_SavedC), _vp]),
         "hq_linear_fwd_lsq": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
                                    ctypes.POINTER(_LsqC), _vp, _sz, _vp]),
         "lss_linear_bwd_lsq": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_LsqC), _vp, _vp, _vp,
@@ -276,6 +279,16 @@ def hq_linear_fwd(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Save
     sv = saved.c()
     _check(lib.hq_linear_fwd(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
                              ctypes.byref(sv), p, n, _stream(X)), "hq_linear_fwd")
+
+
+def hq_linear_fwd_noalloc(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Saved,
+                          log2_block: int) -> None:
+    """hq_linear_fwd without a workspace: the library's static device scratch is used."""
+    N, D = X.shape
+    C = W.shape[0]
+    sv = saved.c()
+    _check(lib.hq_linear_fwd_noalloc(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
+                                     ctypes.byref(sv), _stream(X)), "hq_linear_fwd_noalloc")
 
 
 def hq_linear_fwd_lsq(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Saved, lsq: LSQ,

@@ -2,7 +2,9 @@
 // HQ-MM (forward) and LSS-MM (backward) on the caller's stream.  See include/hqlss.h.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "../../include/hqlss.h"
@@ -151,6 +153,36 @@ void plan_from_ws(Carve& w, int64_t N, int64_t C, lss_plan_t* p) {
   p->kept = w.take<int32_t>(4 * N);
   p->n_kept = w.take<int32_t>(4);
   p->amax_g = w.take<float>(4);
+}
+
+// ---------------------------------------------------------------- static scratch
+// Device memory of the allocation-free forward (hq_linear_fwd_noalloc): the absmax and
+// split-K partials that hq_linear_fwd keeps in its caller's workspace.  Each GPU holds its
+// own copy of the array, at its own address, until the process ends.  In host code the
+// array's name is only a host-side stand-in: kernels get the device address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[HQLSS_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device
+std::mutex g_scratch_mu;
+
+// The device address of `scratch` on the current device, looked up once per device (with
+// that device current) and cached.
+hqlss_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return HQLSS_ERR_HIP;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return HQLSS_ERR_HIP;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return HQLSS_OK;
 }
 
 // ---------------------------------------------------------------- timing log
@@ -587,6 +619,8 @@ const char* hqlss_status_string(hqlss_status s) {
     case HQLSS_ERR_OVERFLOW: return "shape would overflow an int32 accumulator or int64 score";
     case HQLSS_ERR_HIP: return "HIP launch or runtime error";
     case HQLSS_ERR_ARG: return "invalid argument";
+    case HQLSS_ERR_SCRATCH:
+      return "shape needs more scratch than the static array (HQLSS_STATIC_SCRATCH_BYTES) holds";
   }
   return "unknown status";
 }
@@ -604,6 +638,23 @@ hqlss_status hq_linear_fwd(const void* X, const void* W, void* Y, int64_t N, int
   if ((st = check_fwd_overflow(D))) return st;
   if (!ws || ws_bytes < fwd_bytes(N, D, C)) return HQLSS_ERR_WORKSPACE;
   if (!a16(ws)) return HQLSS_ERR_ALIGN;
+  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
+}
+
+hqlss_status hq_linear_fwd_noalloc(const void* X, const void* W, void* Y, int64_t N, int64_t D,
+                                   int64_t C, hqlss_dtype dt, int log2_block,
+                                   const hqlss_saved_t* saved, void* stream) {
+  if (!X || !W || !Y) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if ((st = check_block(log2_block, D))) return st;
+  if ((st = check_dtype(dt))) return st;
+  if ((st = check_saved(saved))) return st;
+  if (!a16(X) || !a16(W) || !a16(Y)) return HQLSS_ERR_ALIGN;
+  if ((st = check_fwd_overflow(D))) return st;
+  if (fwd_bytes(N, D, C) > HQLSS_STATIC_SCRATCH_BYTES) return HQLSS_ERR_SCRATCH;
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws))) return st;
   return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
 }
 

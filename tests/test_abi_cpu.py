@@ -22,7 +22,7 @@ pytestmark = pytest.mark.skipif(torch.cuda.device_count() > 0,
 H = pytest.importorskip("paper_2306_11987_amd", reason="libhqlss.so not built")
 lib = H.lib
 
-OK, NULL, SHAPE, BLOCK, ALIGN, DTYPE, WS, OVF, HIP, ARG = range(10)
+OK, NULL, SHAPE, BLOCK, ALIGN, DTYPE, WS, OVF, HIP, ARG, SCRATCH = range(11)
 
 
 def declared_functions():
@@ -42,7 +42,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in range(10):
+    for s in range(11):
         assert H.status_string(s) and H.status_string(s) != "unknown status"
     assert H.status_string(99) == "unknown status"
 
@@ -98,6 +98,32 @@ def test_fwd_argument_errors():
     s = _saved()
     assert lib.hq_linear_fwd(FAKE, FAKE, FAKE, 128, 256, 256, 0, 5, ctypes.byref(s), None, 0, None) == WS
     assert lib.hq_linear_fwd(FAKE, FAKE, FAKE, 128, 256, 256, 0, 5, ctypes.byref(s), FAKE, 16, None) == WS
+
+
+def fwd_noalloc(X=FAKE, W=FAKE, Y=FAKE, N=128, D=256, C=256, dt=0, k=5, saved=None):
+    s = saved if saved is not None else _saved()
+    return lib.hq_linear_fwd_noalloc(X, W, Y, N, D, C, dt, k, ctypes.byref(s), None)
+
+
+def test_fwd_noalloc_argument_errors():
+    """The allocation-free forward validates as hq_linear_fwd does, and rejects shapes whose
+    forward scratch exceeds the static array, before any HIP call."""
+    txt = open(HEADER).read()
+    m = re.search(r"#define HQLSS_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", txt)
+    assert m and int(m.group(1)) << int(m.group(2)) == H.STATIC_SCRATCH_BYTES
+    assert fwd_noalloc(X=None) == NULL
+    assert fwd_noalloc(saved=_saved(wqT=None)) == NULL
+    assert fwd_noalloc(N=0) == SHAPE
+    assert fwd_noalloc(D=100) == SHAPE
+    assert fwd_noalloc(k=8) == BLOCK
+    assert fwd_noalloc(dt=3) == DTYPE
+    assert fwd_noalloc(Y=FAKE + 4) == ALIGN
+    assert fwd_noalloc(D=1 << 20, C=64, N=1) == OVF
+    # small outputs over a long K split along K: their partials exceed the static array
+    N, D, C = 2048, 16384, 2048
+    assert H.workspace_bytes(H.WS_FWD, N, D, C) > H.STATIC_SCRATCH_BYTES
+    assert fwd_noalloc(N=N, D=D, C=C) == SCRATCH
+    assert H.workspace_bytes(H.WS_FWD, 16384, 4096, 4096) <= H.STATIC_SCRATCH_BYTES
 
 
 def bwd(dY=FAKE, dX=FAKE, dW=FAKE, N=128, D=256, C=256, dt=0, k=5, budget=0, ws=FAKE, nbytes=1 << 40):
