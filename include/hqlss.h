@@ -136,7 +136,7 @@ typedef struct {
 /* Workspace sizes (bytes) for the entry points below, which = HQLSS_WS_*. */
 enum { HQLSS_WS_FWD = 0, HQLSS_WS_BWD_DX = 1, HQLSS_WS_BWD_DW = 2, HQLSS_WS_BWD = 3,
        HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5, HQLSS_WS_HSIZE = 6, HQLSS_WS_FWD_LSQ = 7,
-       HQLSS_WS_BWD_LSQ = 8 };
+       HQLSS_WS_BWD_LSQ = 8, HQLSS_WS_FWD_FP6 = 9 };
 /* Workspace sizes of the batched entry points (B problems of the given shape). */
 enum { HQLSS_WS_BMM_FWD = 0, HQLSS_WS_BMM_BWD = 1 };
 size_t hqlss_bmm_workspace_bytes(int which, int64_t B, int64_t N, int64_t M, int64_t P);
@@ -171,6 +171,20 @@ hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int
 hqlss_status hq_linear_fwd_noalloc(const void *X, const void *W, void *Y, int64_t N, int64_t D,
                                    int64_t C, hqlss_dtype dt, int log2_block,
                                    const hqlss_saved_t *saved, void *stream);
+
+/* FP6 route of HQ-MM (Sec. 3.3, Eq. 3; Procedure HQ-MM), for gfx950's FP6 matrix cores:
+ * every INT4 code |q| <= 7 is exact in e2m3 and the fp32 accumulation of their products is
+ * exact (integers below 2^24), so the product runs on the FP6 MFMA at twice the int8 rate
+ * and Y equals hq_linear_fwd's bit for bit.  Steps, arguments and errors as hq_linear_fwd;
+ * only the saved codes differ in layout: saved->xq [N][D], saved->wq [C][D] and saved->wqT
+ * [D][C] hold one byte per code, every 32 codes of a row being 24 bytes of e2m3 fields
+ * (code i at bits 6i..6i+5 of the little-endian 192-bit group) and 8 zero bytes.
+ * e2m3 (OCP Microscaling Formats): sign, 2 exponent bits with bias 1, 3 mantissa bits.
+ * ws: at least hqlss_workspace_bytes(HQLSS_WS_FWD_FP6, ...) bytes. */
+hqlss_status hq_linear_fwd_fp6(const void *X, const void *W, void *Y, int64_t N, int64_t D,
+                               int64_t C, hqlss_dtype dt, int log2_block,
+                               const hqlss_saved_t *saved, void *ws, size_t ws_bytes,
+                               void *stream);
 
 /* HQ-MM forward with learned step sizes (Sec. 3.3 Procedure HQ-MM with step 2 done by LSQ,
  * Eq. 2; App. A.3).
@@ -316,7 +330,8 @@ const char *hqlss_status_string(hqlss_status s);
  *   which 0: acc[N][C]   = X^ W^^T                     (inputs: saved)
  *   which 1: acc[T][D]   = A_T W^  (rows in kept order, T = n_kept rows written)
  *   which 2: acc[C][D]   = A_T^T X^_T
- * acc is an int32 device buffer of N*C (0), N*D (1) or C*D (2) elements. */
+ *   which 10: which 0 on the FP6 route (saved written by hq_linear_fwd_fp6)
+ * acc is an int32 device buffer of N*C (0, 10), N*D (1) or C*D (2) elements. */
 hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t *plan, const hqlss_saved_t *saved,
                                   int32_t *acc, int64_t N, int64_t D, int64_t C, void *ws,
                                   size_t ws_bytes, void *stream);

@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhqlss.so")
 
 WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN, WS_HSIZE = 0, 1, 2, 3, 4, 5, 6
-WS_FWD_LSQ, WS_BWD_LSQ = 7, 8
+WS_FWD_LSQ, WS_BWD_LSQ, WS_FWD_FP6 = 7, 8, 9
 WS_BMM_FWD, WS_BMM_BWD = 0, 1
 BUDGET_KEEP_NONZERO = -1  # HQLSS_BUDGET_KEEP_NONZERO: keep every non-zero gradient row
 STATIC_SCRATCH_BYTES = 8 << 20  # HQLSS_STATIC_SCRATCH_BYTES: the allocation-free forward's scratch
@@ -49,6 +49,8 @@ def _load() -> ctypes.CDLL:
                                _vp, _sz, _vp]),
         "hq_linear_fwd_noalloc": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int,
                                        ctypes.POINTER(_SavedC), _vp]),
+        "hq_linear_fwd_fp6": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
+                                   _vp, _sz, _vp]),
         "hq_linear_fwd_lsq": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
                                    ctypes.POINTER(_LsqC), _vp, _sz, _vp]),
         "lss_linear_bwd_lsq": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_LsqC), _vp, _vp, _vp,
@@ -289,6 +291,26 @@ def hq_linear_fwd_noalloc(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, sav
     sv = saved.c()
     _check(lib.hq_linear_fwd_noalloc(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
                                      ctypes.byref(sv), _stream(X)), "hq_linear_fwd_noalloc")
+
+
+def saved_fp6_empty(N: int, D: int, C: int, device="cuda") -> "Saved":
+    """Saved state of the FP6 route: one byte per code (padded FP6 layout)."""
+    u8 = dict(dtype=torch.uint8, device=device)
+    return Saved(torch.empty(N, D, **u8), torch.empty(C, D, **u8), torch.empty(D, C, **u8),
+                 torch.empty(N, dtype=torch.int32, device=device),
+                 torch.empty(2, dtype=torch.float32, device=device))
+
+
+def hq_linear_fwd_fp6(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Saved, log2_block: int,
+                      ws: Optional[torch.Tensor] = None) -> None:
+    N, D = X.shape
+    C = W.shape[0]
+    if ws is None:
+        ws = workspace(WS_FWD_FP6, N, D, C, X.device)
+    p, n = _ws(ws)
+    sv = saved.c()
+    _check(lib.hq_linear_fwd_fp6(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
+                                 ctypes.byref(sv), p, n, _stream(X)), "hq_linear_fwd_fp6")
 
 
 def hq_linear_fwd_lsq(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Saved, lsq: LSQ,

@@ -101,6 +101,13 @@ size_t dw_gemm_partial(int64_t N, int64_t D, int64_t C) {
   return al(gemm_partial_bytes(C, D, gemm_splits(C, D, (N + 127) / 128 * 128, false, true)));
 }
 size_t fwd_bytes(int64_t N, int64_t D, int64_t C) { return kFwdHead + fwd_gemm_partial(N, D, C); }
+// FP6 route: the forward's INT4 codes (X^, W^, W^^T) staged before their conversion
+size_t fwd6_partial(int64_t N, int64_t D, int64_t C) {
+  return al(gemm_partial_bytes(N, C, gemm6_splits(N, C, D)));
+}
+size_t fwd6_bytes(int64_t N, int64_t D, int64_t C) {
+  return kFwdHead + al(N * D / 2) + al(C * D / 2) + al(D * C / 2) + fwd6_partial(N, D, C);
+}
 // absmax partials of dY, leverage scores [2][round_up(N, 8)], bit-split partials
 int64_t score_pitch(int64_t N) { return rup(N, 8); }
 size_t plan_scratch_bytes(int64_t N) {
@@ -221,6 +228,41 @@ hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D,
     const int sp = gemm_splits(N, C, D, true, true);
     int32_t* part = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kFwdHead);
     HQ_TRY(launch_gemm(s, kEpiFwd, dt, true, true, g, sp, part));
+  }
+  return HQLSS_OK;
+}
+
+// FP6 route of the forward: the same maxima and INT4 codes as do_fwd (staged in the
+// workspace), converted to the padded FP6 layout of the saved state, then the product on
+// the FP6 MFMA.  Y equals do_fwd's bit for bit.
+hqlss_status do_fwd_fp6(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
+                        int dt, int k, const hqlss_saved_t* sv, void* ws, hipStream_t s) {
+  uint32_t* amax = reinterpret_cast<uint32_t*>(sv->amax);
+  float* px = static_cast<float*>(ws);  // [2][kQMaxWg] absmax partials
+  float* pw = px + kQMaxWg;
+  Carve w{static_cast<char*>(ws), kFwdHead, fwd6_bytes(N, D, C)};
+  uint8_t* xq4 = w.take<uint8_t>(N * D / 2);
+  uint8_t* wq4 = w.take<uint8_t>(C * D / 2);
+  uint8_t* wqT4 = w.take<uint8_t>(D * C / 2);
+  int32_t* part = w.take<int32_t>(fwd6_partial(N, D, C));
+  QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
+  HQ_TRY(launch_fwht_absmax(s, dt, k, jx, px, jw, pw));
+  const QOut ox{px, jx.wg, sv->amax, xq4, sv->x_sumsq};
+  const QOut ow{pw, jw.wg, sv->amax + 1, wq4, nullptr, wqT4};
+  HQ_TRY(launch_fwht_quant(s, dt, k, jx, ox, jw, ow));
+  HQ_TRY(launch_int4_to_fp6(s, xq4, sv->xq, N, D));
+  HQ_TRY(launch_int4_to_fp6(s, wq4, sv->wq, C, D));
+  HQ_TRY(launch_int4_to_fp6(s, wqT4, sv->wqT, D, C));
+  if (Y) {
+    GemmArgs g{};
+    g.A = sv->xq; g.lda = D;
+    g.B = sv->wq; g.ldb = D;
+    g.M = N; g.N = C; g.K = D;
+    g.out = Y; g.ldo = C;
+    g.amax1 = amax; g.amax2 = amax + 1;
+    g.denom = (float)(int64_t(1) << k);
+    g.log2b = k;
+    HQ_TRY(launch_gemm6(s, kEpiFwd, dt, g, gemm6_splits(N, C, D), part));
   }
   return HQLSS_OK;
 }
@@ -513,7 +555,7 @@ const char* kernel_name(int id) {
   static const char* names[kKCount] = {"fwht_absmax", "fwht_quant", "bit_split", "lss_plan", "build_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
                                        "gemm_reduce", "copy", "hsize_max", "hsize_err",
-                                       "hsize_pick", "lsq_quant", "lsq_step_grad"};
+                                       "hsize_pick", "lsq_quant", "lsq_step_grad", "fp6_convert"};
   return (id >= 0 && id < kKCount) ? names[id] : "?";
 }
 
@@ -545,6 +587,7 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
     case HQLSS_WS_PLAN: return plan_scratch_bytes(N);
     case HQLSS_WS_HSIZE: return hsize_bytes();
     case HQLSS_WS_FWD_LSQ: return fwd_gemm_partial(N, D, C);
+    case HQLSS_WS_FWD_FP6: return fwd6_bytes(N, D, C);
     case HQLSS_WS_BWD_LSQ:
       return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C) + dw_bytes(N, D, C) +
              lsq_parts_bytes(N, D, C, true, true);
@@ -656,6 +699,22 @@ hqlss_status hq_linear_fwd_noalloc(const void* X, const void* W, void* Y, int64_
   void* ws = nullptr;
   if ((st = scratch_address(&ws))) return st;
   return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
+}
+
+hqlss_status hq_linear_fwd_fp6(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
+                               hqlss_dtype dt, int log2_block, const hqlss_saved_t* saved, void* ws,
+                               size_t ws_bytes, void* stream) {
+  if (!X || !W || !Y) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_shape(N, D, C))) return st;
+  if ((st = check_block(log2_block, D))) return st;
+  if ((st = check_dtype(dt))) return st;
+  if ((st = check_saved(saved))) return st;
+  if (!a16(X) || !a16(W) || !a16(Y)) return HQLSS_ERR_ALIGN;
+  if ((st = check_fwd_overflow(D))) return st;
+  if (!ws || ws_bytes < fwd6_bytes(N, D, C)) return HQLSS_ERR_WORKSPACE;
+  if (!a16(ws)) return HQLSS_ERR_ALIGN;
+  return do_fwd_fp6(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
 }
 
 hqlss_status hq_linear_fwd_lsq(const void* X, const void* W, void* Y, int64_t N, int64_t D,
@@ -827,6 +886,19 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t* plan, const hqlss
     int32_t* part = sp > 1 ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kFwdHead)
                            : nullptr;
     return hip_status(launch_gemm(s, kEpiAcc, HQLSS_F32, true, true, g, sp, part));
+  }
+  if (which == 10) {  // the forward product on the FP6 route (saved codes in the FP6 layout)
+    if ((st = check_fwd_overflow(D))) return st;
+    GemmArgs g{};
+    g.A = saved->xq; g.lda = D;
+    g.B = saved->wq; g.ldb = D;
+    g.M = N; g.N = C; g.K = D;
+    g.out = acc; g.ldo = C;
+    const int sp = gemm6_splits(N, C, D);
+    if (sp > 1 && (!ws || ws_bytes < kFwdHead + fwd6_partial(N, D, C))) return HQLSS_ERR_WORKSPACE;
+    int32_t* part = sp > 1 ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kFwdHead)
+                           : nullptr;
+    return hip_status(launch_gemm6(s, kEpiAcc, HQLSS_F32, g, sp, part));
   }
   if (which != 1 && which != 2) return HQLSS_ERR_ARG;
   if ((st = check_plan(plan))) return st;

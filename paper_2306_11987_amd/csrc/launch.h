@@ -9,7 +9,7 @@ namespace hqlss {
 enum KernelId : int {
   kKAbsmax = 0, kKQuant, kKBitSplit, kKPlan, kKBuild,
   kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKHsizeMax, kKHsizeErr,
-  kKHsizePick, kKLsqQuant, kKLsqStepGrad, kKCount
+  kKHsizePick, kKLsqQuant, kKLsqStepGrad, kKFp6Convert, kKCount
 };
 const char* kernel_name(int id);
 
@@ -149,6 +149,20 @@ void gemm_set_split_override(int splits);
 void gemm_set_tile_override(int bn);
 hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4, const GemmArgs& g,
                        int splits, int32_t* partial);
+// Tile widths the launchers choose (forward, gradients), and the split-K reduction with the
+// epilogue of `epi` on its own (kEpiAcc, kEpiFwd, kEpiDx, kEpiDw).
+int gemm_fwd_bn(int64_t M, int64_t N, int splits, int64_t batch);
+int gemm_grad_bn(int64_t M, int64_t N, int splits);
+hipError_t launch_gemm_reduce(hipStream_t s, int epi, int dt, const int32_t* P, int S, const GemmArgs& g);
+// The same products on the FP6 MFMA: both operands in the padded FP6 layout of
+// launch_int4_to_fp6 (lda, ldb = K bytes), results identical to launch_gemm's.
+hipError_t launch_gemm6(hipStream_t s, int epi, int dt, const GemmArgs& g, int splits, int32_t* partial);
+int gemm6_splits(int64_t M, int64_t N, int64_t K);  // split-K factor of launch_gemm6
+int gemm_split_override();                          // the test hook's forced factor (0: none)
+// Packed INT4 codes [rows][K/2] (two's complement nibbles, even k in the low nibble) to the
+// padded FP6 layout [rows][K]: every 32 codes become 24 bytes of e2m3 fields (field i at
+// bits 6i..6i+5, little-endian) followed by 8 zero bytes.  K a multiple of 64.
+hipError_t launch_int4_to_fp6(hipStream_t s, const uint8_t* src, uint8_t* dst, int64_t rows, int64_t K);
 // Number of ds_part entries a kEpiDxL / kEpiDwL launch of this shape writes (one per
 // workgroup: of the GEMM, or of the reduction after split-K; every entry is written, 0 by
 // workgroups without rows).

@@ -127,3 +127,27 @@ def check_backward_acc(H, plan, saved, b, N, D, C):
     torch.cuda.synchronize()
     assert np.array_equal(to_np(acc)[:nk], b.acc_dx.astype(np.int32)), "dX int32 accumulators"
     assert np.array_equal(to_np(accw), b.acc_dw.astype(np.int32)), "dW int32 accumulators"
+
+
+# ---------------------------------------------------------------- FP6 route (test side)
+# e2m3 (OCP Microscaling Formats): sign bit, 2 exponent bits with bias 1, 3 mantissa bits;
+# exponent 0 is subnormal (value m / 8).
+def e2m3_value(f: int) -> float:
+    s, e, m = (f >> 5) & 1, (f >> 3) & 3, f & 7
+    v = m / 8.0 if e == 0 else 2.0 ** (e - 1) * (1.0 + m / 8.0)
+    return -v if s else v
+
+
+E2M3_TABLE = np.array([e2m3_value(f) for f in range(64)])
+
+
+def decode_fp6_rows(b: np.ndarray) -> np.ndarray:
+    """Padded FP6 rows [R][K] (uint8) -> values [R][K]: every 32 codes are 24 bytes of 6-bit
+    fields (code i at bits 6i..6i+5 of the little-endian group) and 8 bytes that must be 0."""
+    b = np.asarray(b, dtype=np.uint8)
+    R, K = b.shape
+    g = b.reshape(R, K // 32, 32)
+    assert not g[:, :, 24:].any(), "pad bytes of the FP6 layout are not zero"
+    bits = np.unpackbits(g[:, :, :24], axis=-1, bitorder="little")  # [R][G][192]
+    f = bits.reshape(R, K // 32, 32, 6) @ (1 << np.arange(6))
+    return E2M3_TABLE[f].reshape(R, K)
