@@ -48,6 +48,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 INT8_PEAK_TOPS = 5000.0  # MI355X dense int8 MFMA
+FP6_PEAK_TOPS = 10100.0  # MI355X dense FP6 MFMA
 HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 << 20  # MI355X last-level (Infinity) cache
 # vector ALU: 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz (the fp32 vector peak of
@@ -71,8 +72,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time")
-    p.add_argument("--mode", choices=("dynamic", "lsq", "bmm"), default="dynamic",
-                   help="quantiser: per-tensor maxima (default) or learned step sizes")
+    p.add_argument("--mode", choices=("dynamic", "lsq", "bmm", "fp6"), default="dynamic",
+                   help="dynamic: per-tensor maxima on the int8 MFMA route (default); fp6: the same "
+                        "operator on the FP6 MFMA route; lsq: learned step sizes; bmm: attention BMM")
     p.add_argument("--workload", type=int, choices=sorted(WORKLOAD_KEYS), default=3,
                    help="1: BERT-base FFN pair; 2: GPT-2-medium linears; "
                         "3: GEMM sweep N=16384 (4096..11008, bf16; default); 4: BERT-large encoder block linears")
@@ -182,9 +184,9 @@ def main():
                  Y=torch.empty(lin.N, lin.C, device=dev, dtype=tdt),
                  dX=torch.empty(lin.N, lin.D, device=dev, dtype=tdt),
                  dW=torch.empty(lin.C, lin.D, device=dev, dtype=tdt),
-                 saved=H.Saved.empty(lin.N, lin.D, lin.C, dev),
-                 ws=H.workspace(H.WS_BWD, lin.N, lin.D, lin.C, dev),
-                 wsf=H.workspace(H.WS_FWD, lin.N, lin.D, lin.C, dev),
+                 saved=(H.saved_fp6_empty if args.mode == "fp6" else H.Saved.empty)(lin.N, lin.D, lin.C, dev),
+                 ws=H.workspace(H.WS_BWD_FP6 if args.mode == "fp6" else H.WS_BWD, lin.N, lin.D, lin.C, dev),
+                 wsf=H.workspace(H.WS_FWD_FP6 if args.mode == "fp6" else H.WS_FWD, lin.N, lin.D, lin.C, dev),
                  adv=H.lss_philox_offset_advance(lin.N, lin.C))
         L.append(e)
     del X, W, G
@@ -192,6 +194,7 @@ def main():
     seed = 0
     offsets = [0] * len(L)
     lsq_mode = args.mode == "lsq"
+    fp6_mode = args.mode == "fp6"
     if lsq_mode:
         # steps (untimed): half of the dynamic step a / 7 of each tensor, a from the library
         for e in L:
@@ -208,6 +211,8 @@ def main():
         if lsq_mode:
             H.hq_linear_fwd_lsq(e["X"], e["W"], e["Y"], e["saved"], e["lsq"], e["lin"].log2_block,
                                 e["wsf"])
+        elif fp6_mode:
+            H.hq_linear_fwd_fp6(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
         else:
             H.hq_linear_fwd(e["X"], e["W"], e["Y"], e["saved"], e["lin"].log2_block, e["wsf"])
 
@@ -217,6 +222,9 @@ def main():
         if lsq_mode:
             H.lss_linear_bwd_lsq(e["G"], e["saved"], e["lsq"], e["dX"], e["dW"], e["dstep"], lin.D,
                                  lin.log2_block, lin.budget, seed, offsets[i], e["ws"])
+        elif fp6_mode:
+            H.lss_linear_bwd_fp6(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block,
+                                 lin.budget, seed, offsets[i], e["ws"])
         else:
             H.lss_linear_bwd(e["G"], e["saved"], e["dX"], e["dW"], lin.D, lin.log2_block,
                              lin.budget, seed, offsets[i], e["ws"])
@@ -336,13 +344,14 @@ def main():
     elif dom in ("gemm_dx", "gemm_dw"):
         algo = float(np.mean([2.0 * k * e["lin"].C * e["lin"].D for k, e in zip(kept, L)]))
     roof = None
+    peak = FP6_PEAK_TOPS if fp6_mode else INT8_PEAK_TOPS
     if algo is not None:
         ach = algo / (kernels[dom]["avg_us"] * 1e-6) / 1e12
-        roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": INT8_PEAK_TOPS,
-                "unit": "TFLOP/s", "frac": round(ach / INT8_PEAK_TOPS, 4),
-                "traffic": committed_traffic(dom, WORKLOAD_KEYS[cfg_id] + ("_lsq" if lsq_mode else "")),
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                "traffic": committed_traffic(dom, WORKLOAD_KEYS[cfg_id] + ("_lsq" if lsq_mode else "_fp6" if fp6_mode else "")),
                 "algorithmic_ops_per_launch": algo,
-                "note": "int8 MFMA ops (multiply-adds x 2) of the kept-token GEMM, averaged over "
+                "note": ("FP6" if fp6_mode else "int8") + " MFMA ops (multiply-adds x 2) of the kept-token GEMM, averaged over "
                         "the workload's linears; traffic: HBM bytes per launch from rocprofv3 "
                         "FETCH_SIZE + WRITE_SIZE, calibrated on a copy kernel"}
     gemms = {}
@@ -355,7 +364,7 @@ def main():
             ops = sum(2.0 * k * e["lin"].C * e["lin"].D for k, e in zip(kept, L))
         us = kernels[nm]["us_per_step"] + (kernels["gemm_reduce"]["us_per_step"]
                                            if nm == "gemm_dw" and "gemm_reduce" in kernels else 0.0)
-        gemms[nm] = {"frac": round(ops / (us * 1e-6) / 1e12 / INT8_PEAK_TOPS, 4),
+        gemms[nm] = {"frac": round(ops / (us * 1e-6) / 1e12 / peak, 4),
                      "us_per_step": round(us, 1)}
 
     # ---- memory-bound stages against the HBM peak, with algorithmic bytes of one read
@@ -395,7 +404,8 @@ def main():
             hbm[stage] = {"algorithmic_MB_per_step": round(b / 1e6, 2), "us_per_step": round(us, 1),
                           "achieved_GBps": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
     overhead = {k: round(kernels[k]["us_per_step"], 1)
-                for k in ("build_operands", "lss_plan", "gemm_reduce", "lsq_step_grad") if k in kernels}
+                for k in ("build_operands", "lss_plan", "gemm_reduce", "lsq_step_grad", "fp6_convert",
+                          "fp6_plan", "fp6_build") if k in kernels}
 
     # ---- per linear: that linear's fwd + bwd alone, median of per-step event times
     per_linear = []
@@ -500,11 +510,12 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "i8",
+        "dtype": "fp6-e2m3" if fp6_mode else "i8",
         "data": "synthetic",
         "config": {"workload": wl.name, "N": N, "linears": [[e["lin"].D, e["lin"].C] for e in L],
                    "log2_block": lins[0].log2_block, "io_dtype": lins[0].dtype, "budget": lins[0].budget,
                    "quantizer": "lsq (s = max|V H| / 14)" if lsq_mode else "per-tensor max",
+                   "route": "FP6 MFMA (e2m3 codes)" if fp6_mode else "int8 MFMA",
                    "kept_tokens": [round(k, 1) for k in kept]},
         "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
         "timing": "median of per-step HIP-event times over the timed steps",
@@ -515,7 +526,8 @@ def main():
         "input_sets": rot,
         "roofline": roof,
         "cpu_baseline": cpu,
-        "gemm_frac_int8_peak": gemms,
+        "gemm_frac_of_peak": gemms,
+        "gemm_peak_tops": peak,
         "hbm_stages": hbm,
         "overhead_us_per_step": overhead,
         "per_linear": per_linear,

@@ -136,7 +136,8 @@ typedef struct {
 /* Workspace sizes (bytes) for the entry points below, which = HQLSS_WS_*. */
 enum { HQLSS_WS_FWD = 0, HQLSS_WS_BWD_DX = 1, HQLSS_WS_BWD_DW = 2, HQLSS_WS_BWD = 3,
        HQLSS_WS_FROM_PLAN = 4, HQLSS_WS_PLAN = 5, HQLSS_WS_HSIZE = 6, HQLSS_WS_FWD_LSQ = 7,
-       HQLSS_WS_BWD_LSQ = 8, HQLSS_WS_FWD_FP6 = 9 };
+       HQLSS_WS_BWD_LSQ = 8, HQLSS_WS_FWD_FP6 = 9, HQLSS_WS_BWD_FP6 = 10,
+       HQLSS_WS_FROM_PLAN_FP6 = 11 };
 /* Workspace sizes of the batched entry points (B problems of the given shape). */
 enum { HQLSS_WS_BMM_FWD = 0, HQLSS_WS_BMM_BWD = 1 };
 size_t hqlss_bmm_workspace_bytes(int which, int64_t B, int64_t N, int64_t M, int64_t P);
@@ -185,6 +186,22 @@ hqlss_status hq_linear_fwd_fp6(const void *X, const void *W, void *Y, int64_t N,
                                int64_t C, hqlss_dtype dt, int log2_block,
                                const hqlss_saved_t *saved, void *ws, size_t ws_bytes,
                                void *stream);
+
+/* FP6 route of LSS-MM (Sec. 4.2, Procedure LSS-MM, App. A.3), after hq_linear_fwd_fp6 (saved
+ * in the FP6 layout): the same bit split, leverage scores and sample as lss_linear_bwd, and
+ * dX, dW equal to its outputs bit for bit; the two products run on the FP6 MFMA.  The
+ * weighted rows 14 w_up q_up + w_dn q_dn do not fit e2m3, so the route keeps the two code
+ * planes apart and applies the weights exactly on the fp32 accumulators: dX rows of tokens
+ * with an upper row run a first K pass over the upper codes, scaled by 14 / w_dn before the
+ * lower pass and by w_dn after it; dW takes its K entries grouped by weight 2^4 .. 2^0 (an
+ * upper row, weight 14 = 8 + 4 + 2, once in each of three classes) and doubles its sums at
+ * every class boundary.  Arguments, sampling and errors as lss_linear_bwd, plus
+ * HQLSS_ERR_OVERFLOW for C > 11412 (the upper-pass sums must stay exact in fp32).
+ * ws: at least hqlss_workspace_bytes(HQLSS_WS_BWD_FP6, ...) bytes. */
+hqlss_status lss_linear_bwd_fp6(const void *dY, const hqlss_saved_t *saved, void *dX, void *dW,
+                                int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                                int64_t budget_rows, uint64_t seed, uint64_t offset, void *ws,
+                                size_t ws_bytes, void *stream);
 
 /* HQ-MM forward with learned step sizes (Sec. 3.3 Procedure HQ-MM with step 2 done by LSQ,
  * Eq. 2; App. A.3).
@@ -330,8 +347,9 @@ const char *hqlss_status_string(hqlss_status s);
  *   which 0: acc[N][C]   = X^ W^^T                     (inputs: saved)
  *   which 1: acc[T][D]   = A_T W^  (rows in kept order, T = n_kept rows written)
  *   which 2: acc[C][D]   = A_T^T X^_T
- *   which 10: which 0 on the FP6 route (saved written by hq_linear_fwd_fp6)
- * acc is an int32 device buffer of N*C (0, 10), N*D (1) or C*D (2) elements. */
+ *   which 10, 11, 12: which 0, 1, 2 on the FP6 route (saved written by hq_linear_fwd_fp6;
+ *            11 and 12 need hqlss_workspace_bytes(HQLSS_WS_FROM_PLAN_FP6, ...) bytes)
+ * acc is an int32 device buffer of N*C (0, 10), N*D (1, 11) or C*D (2, 12) elements. */
 hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t *plan, const hqlss_saved_t *saved,
                                   int32_t *acc, int64_t N, int64_t D, int64_t C, void *ws,
                                   size_t ws_bytes, void *stream);

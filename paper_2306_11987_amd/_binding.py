@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhqlss.so")
 
 WS_FWD, WS_BWD_DX, WS_BWD_DW, WS_BWD, WS_FROM_PLAN, WS_PLAN, WS_HSIZE = 0, 1, 2, 3, 4, 5, 6
-WS_FWD_LSQ, WS_BWD_LSQ, WS_FWD_FP6 = 7, 8, 9
+WS_FWD_LSQ, WS_BWD_LSQ, WS_FWD_FP6, WS_BWD_FP6, WS_FROM_PLAN_FP6 = 7, 8, 9, 10, 11
 WS_BMM_FWD, WS_BMM_BWD = 0, 1
 BUDGET_KEEP_NONZERO = -1  # HQLSS_BUDGET_KEEP_NONZERO: keep every non-zero gradient row
 STATIC_SCRATCH_BYTES = 8 << 20  # HQLSS_STATIC_SCRATCH_BYTES: the allocation-free forward's scratch
@@ -51,6 +51,8 @@ def _load() -> ctypes.CDLL:
                                        ctypes.POINTER(_SavedC), _vp]),
         "hq_linear_fwd_fp6": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
                                    _vp, _sz, _vp]),
+        "lss_linear_bwd_fp6": (st, [_vp, ctypes.POINTER(_SavedC), _vp, _vp, _i64, _i64, _i64, _int, _int,
+                                    _i64, _u64, _u64, _vp, _sz, _vp]),
         "hq_linear_fwd_lsq": (st, [_vp, _vp, _vp, _i64, _i64, _i64, _int, _int, ctypes.POINTER(_SavedC),
                                    ctypes.POINTER(_LsqC), _vp, _sz, _vp]),
         "lss_linear_bwd_lsq": (st, [_vp, ctypes.POINTER(_SavedC), ctypes.POINTER(_LsqC), _vp, _vp, _vp,
@@ -311,6 +313,19 @@ def hq_linear_fwd_fp6(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: 
     sv = saved.c()
     _check(lib.hq_linear_fwd_fp6(_ptr(X), _ptr(W), _ptr(Y), N, D, C, _dt(X), int(log2_block),
                                  ctypes.byref(sv), p, n, _stream(X)), "hq_linear_fwd_fp6")
+
+
+def lss_linear_bwd_fp6(dY: torch.Tensor, saved: Saved, dX: Optional[torch.Tensor], dW: Optional[torch.Tensor],
+                       D: int, log2_block: int, budget: int = 0, seed: int = 0, offset: int = 0,
+                       ws: Optional[torch.Tensor] = None) -> None:
+    N, C = dY.shape
+    if ws is None:
+        ws = workspace(WS_BWD_FP6, N, D, C, dY.device)
+    p, n = _ws(ws)
+    sv = saved.c()
+    _check(lib.lss_linear_bwd_fp6(_ptr(dY), ctypes.byref(sv), _ptr(dX), _ptr(dW), N, D, C, _dt(dY),
+                                  int(log2_block), int(budget), int(seed), int(offset), p, n, _stream(dY)),
+           "lss_linear_bwd_fp6")
 
 
 def hq_linear_fwd_lsq(X: torch.Tensor, W: torch.Tensor, Y: torch.Tensor, saved: Saved, lsq: LSQ,

@@ -108,6 +108,26 @@ size_t fwd6_partial(int64_t N, int64_t D, int64_t C) {
 size_t fwd6_bytes(int64_t N, int64_t D, int64_t C) {
   return kFwdHead + al(N * D / 2) + al(C * D / 2) + al(D * C / 2) + fwd6_partial(N, D, C);
 }
+// FP6 backward: K entries of dW (lower rows, plus each upper row in three weight classes,
+// each class padded to 128) and their split-K factor; the fp32 sums stay exact while
+// 882 N < 2^24 (every entry's weighted products of one output add to at most 126 x 7 per
+// token), else each split holds at most 21376 entries (784 per entry)
+int64_t ecap6(int64_t N) { return rup(4 * N + 640, 128); }
+int dw6_splits(int64_t N, int64_t D, int64_t C) {
+  int sp = gemm6_splits(C, D, ecap6(N));
+  if (882 * N >= (int64_t(1) << 24)) {
+    const int need = (int)((ecap6(N) + 21375) / 21376);
+    if (sp < need) sp = need;
+  }
+  return sp;
+}
+size_t dx6_bytes(int64_t N, int64_t D, int64_t C) {
+  return al(N * C) + al(rup(N, 256) * C) + al(gemm_partial_bytes(N, D, gemm6_splits(N, D, C)));
+}
+size_t dw6_bytes(int64_t N, int64_t D, int64_t C) {
+  return al(C * ecap6(N)) + al(D * ecap6(N)) + al(gemm_partial_bytes(C, D, dw6_splits(N, D, C)));
+}
+size_t plan6_bytes(int64_t N) { return al(4 * N) + al(4 * ecap6(N)) + al(64); }
 // absmax partials of dY, leverage scores [2][round_up(N, 8)], bit-split partials
 int64_t score_pitch(int64_t N) { return rup(N, 8); }
 size_t plan_scratch_bytes(int64_t N) {
@@ -525,6 +545,80 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   return HQLSS_OK;
 }
 
+// FP6 route of the backward GEMMs: the same plan, operands in the padded FP6 layout ordered
+// for the route's exact weights (fp6_plan), products on the FP6 MFMA.  Every accumulator and
+// output equals do_grads' bit for bit.
+hqlss_status do_grads_fp6(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, void* dW,
+                          int32_t* acc, int which_acc, int64_t N, int64_t D, int64_t C, int dt,
+                          int k, Carve& w, hipStream_t s) {
+  const uint32_t* amax = reinterpret_cast<const uint32_t*>(sv->amax);
+  const uint32_t* ag = reinterpret_cast<const uint32_t*>(p->amax_g);
+  const float denom = (float)(kBsRatio * (int64_t(1) << k));
+  const bool want_dx = dX || (acc && which_acc == 1);
+  const bool want_dw = dW || (acc && which_acc == 2);
+  const int64_t ecap = ecap6(N);
+  int32_t* order6 = w.take<int32_t>(4 * N);
+  int32_t* ent = w.take<int32_t>(4 * ecap);
+  int32_t* cnt = w.take<int32_t>(64);  // [0] n_up, [8..12] class bounds
+  uint8_t *a_dn = nullptr, *a_up = nullptr, *a_dw = nullptr, *x_dw = nullptr;
+  int32_t *part_dx = nullptr, *part_dw = nullptr;
+  const int sp_dx = gemm6_splits(N, D, C), sp_dw = dw6_splits(N, D, C);
+  if (want_dx) {
+    a_dn = w.take<uint8_t>(N * C);
+    a_up = w.take<uint8_t>(rup(N, 256) * C);
+    part_dx = w.take<int32_t>(gemm_partial_bytes(N, D, sp_dx));
+  }
+  if (want_dw) {
+    a_dw = w.take<uint8_t>(C * ecap);
+    x_dw = w.take<uint8_t>(D * ecap);
+    part_dw = w.take<int32_t>(gemm_partial_bytes(C, D, sp_dw));
+  }
+  if (!w.ok()) return HQLSS_ERR_WORKSPACE;
+  HQ_TRY(launch_fp6_plan(s, p->w_up, p->w_dn, N, order6, cnt, ent, cnt + 8));
+  HQ_TRY(launch_fp6_build(s, dt, p->qup, p->qdn, p->w_up, p->w_dn, order6, p->n_kept, cnt, ent,
+                          cnt + 8, sv->xq, N, C, D, ecap, a_dn, a_up, a_dw, x_dw, dX));
+  if (want_dx) {
+    GemmArgs g{};
+    g.A = a_dn; g.lda = C;
+    g.B = sv->wqT; g.ldb = C;
+    g.M = N; g.m_dev = p->n_kept; g.N = D; g.K = C;
+    g.out_rows = order6;
+    g.amax1 = ag; g.amax2 = amax + 1; g.denom = denom; g.log2b = k;
+    g.f6_kind = 1; g.A2 = a_up; g.m2_dev = cnt; g.w_up = p->w_up; g.w_dn = p->w_dn;
+    if (dX) {
+      g.out = dX; g.ldo = D;
+      HQ_TRY(launch_gemm6(s, kEpiDx, dt, g, sp_dx, part_dx));
+    }
+    if (acc && which_acc == 1) {
+      g.out = acc; g.ldo = D;
+      HQ_TRY(launch_gemm6(s, kEpiAcc, dt, g, sp_dx, part_dx));
+    }
+  }
+  if (want_dw) {
+    GemmArgs g{};
+    g.A = a_dw; g.lda = ecap;
+    g.B = x_dw; g.ldb = ecap;
+    g.M = C; g.N = D; g.K = ecap; g.k_dev = cnt + 12;
+    g.amax1 = ag; g.amax2 = amax; g.denom = denom; g.log2b = k;
+    g.f6_kind = 2; g.kcls = cnt + 8;
+    if (dW) {
+      g.out = dW; g.ldo = D;
+      HQ_TRY(launch_gemm6(s, kEpiDw, dt, g, sp_dw, part_dw));
+    }
+    if (acc && which_acc == 2) {
+      g.out = acc; g.ldo = D;
+      HQ_TRY(launch_gemm6(s, kEpiAcc, dt, g, sp_dw, part_dw));
+    }
+  }
+  return HQLSS_OK;
+}
+
+// the FP6 backward's extra shape limit: the dX sums of 14 / w_dn times the upper pass plus
+// the lower pass are half-integers below 735 C, exact in fp32 for C <= 11412
+hqlss_status check_bwd6_overflow(int64_t C) {
+  return 2 * 735 * C < (int64_t(1) << 24) ? HQLSS_OK : HQLSS_ERR_OVERFLOW;
+}
+
 hqlss_status check_bwd_common(const void* dY, const hqlss_saved_t* saved, int64_t N, int64_t D,
                               int64_t C, int dt, int log2_block, int64_t budget,
                               bool need_amax = true) {
@@ -555,7 +649,8 @@ const char* kernel_name(int id) {
   static const char* names[kKCount] = {"fwht_absmax", "fwht_quant", "bit_split", "lss_plan", "build_operands",
                                        "gemm_fwd", "gemm_dx", "gemm_dw", "gemm_acc",
                                        "gemm_reduce", "copy", "hsize_max", "hsize_err",
-                                       "hsize_pick", "lsq_quant", "lsq_step_grad", "fp6_convert"};
+                                       "hsize_pick", "lsq_quant", "lsq_step_grad", "fp6_convert",
+                                       "fp6_plan", "fp6_build"};
   return (id >= 0 && id < kKCount) ? names[id] : "?";
 }
 
@@ -588,6 +683,10 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
     case HQLSS_WS_HSIZE: return hsize_bytes();
     case HQLSS_WS_FWD_LSQ: return fwd_gemm_partial(N, D, C);
     case HQLSS_WS_FWD_FP6: return fwd6_bytes(N, D, C);
+    case HQLSS_WS_BWD_FP6:
+      return plan_bytes(N, C) + plan_scratch_bytes(N) + plan6_bytes(N) + dx6_bytes(N, D, C) +
+             dw6_bytes(N, D, C);
+    case HQLSS_WS_FROM_PLAN_FP6: return plan6_bytes(N) + dx6_bytes(N, D, C) + dw6_bytes(N, D, C);
     case HQLSS_WS_BWD_LSQ:
       return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C) + dw_bytes(N, D, C) +
              lsq_parts_bytes(N, D, C, true, true);
@@ -824,6 +923,27 @@ hqlss_status lss_linear_bwd(const void* dY, const hqlss_saved_t* saved, void* dX
                   ws_bytes, stream);
 }
 
+hqlss_status lss_linear_bwd_fp6(const void* dY, const hqlss_saved_t* saved, void* dX, void* dW,
+                                int64_t N, int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
+                                int64_t budget_rows, uint64_t seed, uint64_t offset, void* ws,
+                                size_t ws_bytes, void* stream) {
+  if (!dX && !dW) return HQLSS_ERR_NULL;
+  hqlss_status st;
+  if ((st = check_bwd_common(dY, saved, N, D, C, dt, log2_block, budget_rows))) return st;
+  if ((st = check_bwd6_overflow(C))) return st;
+  if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
+  const size_t need = plan_bytes(N, C) + plan_scratch_bytes(N) + plan6_bytes(N) +
+                      (dX ? dx6_bytes(N, D, C) : 0) + (dW ? dw6_bytes(N, D, C) : 0);
+  if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carve w{static_cast<char*>(ws), 0, ws_bytes};
+  lss_plan_t p;
+  plan_from_ws(w, N, C, &p);
+  const int64_t B = resolve_budget(budget_rows, N);
+  if ((st = do_plan(dY, saved, &p, N, C, dt, B, seed, offset, w, s))) return st;
+  return do_grads_fp6(&p, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w, s);
+}
+
 hqlss_status lss_linear_bwd_dx(const void* dY, const hqlss_saved_t* saved, void* dX, int64_t N,
                                int64_t D, int64_t C, hqlss_dtype dt, int log2_block,
                                int64_t budget_rows, uint64_t seed, uint64_t offset, void* ws,
@@ -899,6 +1019,16 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t* plan, const hqlss
     int32_t* part = sp > 1 ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kFwdHead)
                            : nullptr;
     return hip_status(launch_gemm6(s, kEpiAcc, HQLSS_F32, g, sp, part));
+  }
+  if (which == 11 || which == 12) {  // the gradient products on the FP6 route
+    if ((st = check_plan(plan))) return st;
+    if ((st = check_bwd_overflow(N, D, C, 0))) return st;
+    if ((st = check_bwd6_overflow(C))) return st;
+    const size_t need = plan6_bytes(N) + (which == 11 ? dx6_bytes(N, D, C) : dw6_bytes(N, D, C));
+    if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
+    if (!a16(ws)) return HQLSS_ERR_ALIGN;
+    Carve w{static_cast<char*>(ws), 0, ws_bytes};
+    return do_grads_fp6(plan, saved, nullptr, nullptr, acc, which - 10, N, D, C, HQLSS_F32, 0, w, s);
   }
   if (which != 1 && which != 2) return HQLSS_ERR_ARG;
   if ((st = check_plan(plan))) return st;

@@ -15,15 +15,41 @@ namespace {
 // FP6 workgroup tiles: 256 x 256, one workgroup of 8 waves per CU, stages of 128 k.
 constexpr int kBM6 = 256;
 
-template <int EPI, int DT>
+template <int F6K, int EPI, int DT, int LOG2B>
 hipError_t run6(hipStream_t s, const GemmArgs& g, int splits, int32_t* partial, int id) {
-  if (splits <= 1) return gemm_t<kBM6, true, EPI, DT, 0, kBN, true>(s, g, 1, id);
+  if (splits <= 1) return gemm_t<kBM6, true, EPI, DT, LOG2B, kBN, true, F6K>(s, g, 1, id);
   GemmArgs p = g;
   p.out = partial;
   p.ldo = g.N;
-  hipError_t e = gemm_t<kBM6, true, kEpiPartial, DT, 0, kBN, true>(s, p, splits, id);
+  hipError_t e = gemm_t<kBM6, true, kEpiPartial, DT, 0, kBN, true, F6K>(s, p, splits, id);
   if (e != hipSuccess) return e;
   return launch_gemm_reduce(s, EPI, DT, partial, splits, g);
+}
+
+// the Hadamard block is a template parameter of the gradient epilogues
+template <int F6K, int EPI, int DT>
+hipError_t run6_b(hipStream_t s, const GemmArgs& g, int splits, int32_t* partial, int id) {
+  switch (g.log2b) {
+    case 0: return run6<F6K, EPI, DT, 0>(s, g, splits, partial, id);
+    case 1: return run6<F6K, EPI, DT, 1>(s, g, splits, partial, id);
+    case 2: return run6<F6K, EPI, DT, 2>(s, g, splits, partial, id);
+    case 3: return run6<F6K, EPI, DT, 3>(s, g, splits, partial, id);
+    case 4: return run6<F6K, EPI, DT, 4>(s, g, splits, partial, id);
+    case 5: return run6<F6K, EPI, DT, 5>(s, g, splits, partial, id);
+    case 6: return run6<F6K, EPI, DT, 6>(s, g, splits, partial, id);
+    case 7: return run6<F6K, EPI, DT, 7>(s, g, splits, partial, id);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <int F6K, int EPI>
+hipError_t run6_dt(hipStream_t s, int dt, const GemmArgs& g, int splits, int32_t* partial, int id) {
+  switch (dt) {
+    case kF32: return run6_b<F6K, EPI, kF32>(s, g, splits, partial, id);
+    case kF16: return run6_b<F6K, EPI, kF16>(s, g, splits, partial, id);
+    case kBF16: return run6_b<F6K, EPI, kBF16>(s, g, splits, partial, id);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -42,12 +68,22 @@ int gemm6_splits(int64_t M, int64_t N, int64_t K) {
 }
 
 hipError_t launch_gemm6(hipStream_t s, int epi, int dt, const GemmArgs& g, int splits, int32_t* partial) {
-  if (epi == kEpiAcc) return run6<kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
+  if (g.f6_kind == kF6Dx) {
+    if (epi == kEpiAcc) return run6<kF6Dx, kEpiAcc, kF32, 0>(s, g, splits, partial, kKGemmAcc);
+    if (epi == kEpiDx) return run6_dt<kF6Dx, kEpiDx>(s, dt, g, splits, partial, kKGemmDx);
+    return hipErrorInvalidValue;
+  }
+  if (g.f6_kind == kF6Dw) {
+    if (epi == kEpiAcc) return run6<kF6Dw, kEpiAcc, kF32, 0>(s, g, splits, partial, kKGemmAcc);
+    if (epi == kEpiDw) return run6_dt<kF6Dw, kEpiDw>(s, dt, g, splits, partial, kKGemmDw);
+    return hipErrorInvalidValue;
+  }
+  if (epi == kEpiAcc) return run6<0, kEpiAcc, kF32, 0>(s, g, splits, partial, kKGemmAcc);
   if (epi == kEpiFwd) {
     switch (dt) {
-      case kF32: return run6<kEpiFwd, kF32>(s, g, splits, partial, kKGemmFwd);
-      case kF16: return run6<kEpiFwd, kF16>(s, g, splits, partial, kKGemmFwd);
-      case kBF16: return run6<kEpiFwd, kBF16>(s, g, splits, partial, kKGemmFwd);
+      case kF32: return run6<0, kEpiFwd, kF32, 0>(s, g, splits, partial, kKGemmFwd);
+      case kF16: return run6<0, kEpiFwd, kF16, 0>(s, g, splits, partial, kKGemmFwd);
+      case kBF16: return run6<0, kEpiFwd, kBF16, 0>(s, g, splits, partial, kKGemmFwd);
     }
   }
   return hipErrorInvalidValue;

@@ -224,7 +224,10 @@ __device__ __forceinline__ double block_sum_f64(double v, double* red) {
   return t;
 }
 
-template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B, int BN_, bool F6 = false>
+// F6K (FP6 route): 0 the plain product (forward), kF6Dx the dX product (two K passes for tiles
+// holding upper tokens, row weights), kF6Dw the dW product (weight classes along K)
+constexpr int kF6Dx = 1, kF6Dw = 2;
+template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B, int BN_, bool F6 = false, int F6K = 0>
 __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, WN, BN_, F6>::OCC)) void gemm_kernel(GemmArgs g) {
   using C_ = Cfg<BM, A4, WN, BN_, F6>;
   constexpr int TI = C_::TI, TJ = C_::TJ, BN = C_::BN;
@@ -290,8 +293,16 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
   }
   int64_t K = g.K;
   if (g.k_dev) K = ((int64_t)*g.k_dev + 127) / 128 * 128;
+  // FP6 dX tiles holding upper-row tokens (rows below *m2_dev) run two K passes, first over
+  // the upper codes (A2), then the lower ones (A), each of npass stages
+  int npass = 0;
+  bool two = false;
+  if constexpr (F6 && F6K == kF6Dx) {
+    npass = (int)((K + C_::KS - 1) / C_::KS);
+    two = m0 < (int64_t)*g.m2_dev;
+  }
   // split-K range of this workgroup (whole stages)
-  const int nst_all = (int)((K + C_::KS - 1) / C_::KS);
+  const int nst_all = two ? 2 * npass : (int)((K + C_::KS - 1) / C_::KS);
   const int per = (nst_all + nsplit - 1) / nsplit;
   const int st0 = zsplit * per;
   const int nst = max(0, min(nst_all, st0 + per) - st0);
@@ -309,7 +320,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     int64_t gm = m0 + r;
     gm = gm < M ? gm : M - 1;
     ca[x] = c * 16;
-    pa[x] = static_cast<const uint8_t*>(g.A) + gm * g.lda + (int64_t)st0 * C_::RA + c * 16;
+    pa[x] = static_cast<const uint8_t*>(g.A) + gm * g.lda + (F6 ? 0 : (int64_t)st0 * C_::RA) + c * 16;
   }
 #pragma unroll
   for (int x = 0; x < C_::B_BPW; ++x) {
@@ -318,12 +329,45 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     int64_t gn = n0 + b_row_of_slot<C_::WN>(s);
     gn = gn < g.N ? gn : g.N - 1;
     cb[x] = c * 16;
-    pb[x] = static_cast<const uint8_t*>(g.B) + gn * g.ldb + (int64_t)st0 * C_::RB + c * 16;
+    pb[x] = static_cast<const uint8_t*>(g.B) + gn * g.ldb + (F6 ? 0 : (int64_t)st0 * C_::RB) + c * 16;
   }
   // issue the loads of local stage st into buffer st % NBUF; chunks past K are zeroed
+  // FP6: the byte offset of global stage gs in the rows (a byte per code, same for A and B),
+  // and for two-pass tiles the upper operand A2 in the first pass
+  const int64_t dA2 = (F6K == kF6Dx && two) ? static_cast<const uint8_t*>(g.A2) - static_cast<const uint8_t*>(g.A) : 0;
   auto issue = [&](int st) {
     uint8_t* sa = smem + (st % C_::NBUF) * C_::STAGE;
     uint8_t* sb = sa + C_::A_BYTES;
+    if constexpr (F6) {
+      const int gs = st0 + st;
+      const bool upper = two && gs < npass;
+      const int64_t kin = (int64_t)(two && !upper ? gs - npass : gs) * C_::RA;
+      const int64_t da = upper ? dA2 : 0;
+      if (kin + C_::RA <= K) {
+#pragma unroll
+        for (int x = 0; x < C_::A_BPW; ++x) dma16(pa[x] + da + kin, sa + (wid * C_::A_BPW + x) * 1024);
+#pragma unroll
+        for (int x = 0; x < C_::B_BPW; ++x) dma16(pb[x] + kin, sb + (wid * C_::B_BPW + x) * 1024);
+        return;
+      }
+#pragma unroll
+      for (int x = 0; x < C_::A_BPW; ++x) {
+        uint8_t* dst = sa + (wid * C_::A_BPW + x) * 1024;
+        if (kin + ca[x] < K)
+          dma16(pa[x] + da + kin, dst);
+        else
+          *reinterpret_cast<uint4*>(dst + lane * 16) = make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int x = 0; x < C_::B_BPW; ++x) {
+        uint8_t* dst = sb + (wid * C_::B_BPW + x) * 1024;
+        if (kin + cb[x] < K)
+          dma16(pb[x] + kin, dst);
+        else
+          *reinterpret_cast<uint4*>(dst + lane * 16) = make_uint4(0u, 0u, 0u, 0u);
+      }
+      return;
+    }
     const int64_t ka = (int64_t)(st0 + st) * C_::RA, kb = (int64_t)(st0 + st) * C_::RB;
     if (ka + C_::RA <= Ka && kb + C_::RB <= Kb) {  // whole stage inside K: straight line
 #pragma unroll
@@ -513,6 +557,71 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // up to 2 LDS reads
       }
     };
+    // Weights the GEMM applies to its fp32 accumulators (all exact: powers of two, and for
+    // dX 14 / w_dn in {14, 7, 3.5} on half-integers below 2^23).
+    //   dX: row m of token t accumulates f1 x (upper pass) + lower pass, times f2, with
+    //   f1 = 14 / w_dn (14 if w_dn = 0, whose lower row is zero) and f2 = max(w_dn, 1),
+    //   giving 14 w_up acc_up + w_dn acc_dn.
+    //   dW: the K entries come in classes of weight 2^4 .. 2^0 (class bounds kcls); crossing
+    //   from class e to e' doubles the sum e - e' times (Horner), and the sum ends times
+    //   2^(class of the last stage).
+    // The K loop runs in segments between the stages where a weight is due, so the loop
+    // body itself never touches the accumulators outside the MFMAs.
+    int b3 = 0, b2 = 0, b1 = 0, b0 = 0;
+    if constexpr (F6K == kF6Dw) {
+      b3 = g.kcls[0]; b2 = g.kcls[1]; b1 = g.kcls[2]; b0 = g.kcls[3];
+    }
+    auto cls_of = [&](int gs) {  // weight class of global stage gs (128 entries)
+      const int e = gs * C_::KS;
+      return 4 - (e >= b3) - (e >= b2) - (e >= b1) - (e >= b0);
+    };
+    auto next_bound = [&](int gs) {  // first global stage after gs where a weight is due
+      int nb = 1 << 30;
+      if constexpr (F6K == kF6Dx) {
+        if (two && gs < npass) nb = npass;
+      } else if constexpr (F6K == kF6Dw) {
+        const int bs[4] = {b3, b2, b1, b0};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int b = bs[q] / C_::KS;
+          if (b > gs && b < nb) nb = b;
+        }
+      }
+      return nb;
+    };
+    auto row_weights = [&](bool up_pass) {  // dX: f1 (up_pass) or f2 of this lane's rows
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int64_t m = m0 + wm * C_::WM + 32 * i + (lane & 31);
+        float f = 1.f;
+        if (m < M) {
+          const int t = g.out_rows[m];
+          const int wu = g.w_up[t], wd = g.w_dn[t];
+          f = up_pass ? (wu ? (wd ? 14.f / (float)wd : 14.f) : 1.f) : (wd ? (float)wd : 1.f);
+        }
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) accf[i][j][r] *= f;
+      }
+    };
+    auto scale_all = [&](int sh) {
+      const float f = (float)(1 << sh);
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) accf[i][j][r] *= f;
+    };
+    auto rescale6 = [&](int gs) {  // before global stage gs (gs > st0) runs
+      if constexpr (F6K == kF6Dx) {
+        if (two && gs == npass) row_weights(true);
+      } else if constexpr (F6K == kF6Dw) {
+        const int d = cls_of(gs - 1) - cls_of(gs);
+        if (d > 0) scale_all(d);
+      }
+    };
 #pragma unroll
     for (int p = 0; p < C_::NBUF - 1; ++p)
       if (p < nst) issue(p);
@@ -542,20 +651,36 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
         mfma6(0);
       }
     } else {  // two steps per stage: the wait and barrier sit between them
+      static_assert(KST == 2, "FP6 stages of one or two MFMA steps");
       if (nst > 0) {
         stage_ready(0);
         read6(0, 0, 0);
       }
-      for (int st = 0; st < nst; ++st) {
-        read6(1, st, 1);
-        mfma6(0);
-        interleave6();
-        if (st + 1 < nst) {
-          stage_ready(st + 1);
-          read6(0, st + 1, 0);
+      int st = 0;
+      while (st < nst) {
+        const int seg = min(nst, next_bound(st0 + st) - st0);
+        for (; st < seg; ++st) {
+          read6(1, st, 1);
+          mfma6(0);
+          interleave6();
+          if (st + 1 < nst) {
+            stage_ready(st + 1);
+            read6(0, st + 1, 0);
+          }
+          mfma6(1);
+          interleave6();
         }
-        mfma6(1);
-        interleave6();
+        if (st < nst) rescale6(st0 + st);
+      }
+    }
+    if (nst > 0) {  // the weights still due at the end of this split's K range
+      const int gl = st0 + nst - 1;
+      if constexpr (F6K == kF6Dx) {
+        if (two && gl < npass) row_weights(true);
+        row_weights(false);
+      } else if constexpr (F6K == kF6Dw) {
+        const int e = cls_of(gl);
+        if (e > 0) scale_all(e);
       }
     }
   } else {
@@ -737,7 +862,7 @@ template <bool A4, int LOG2B> constexpr int wave_n() { return (A4 || LOG2B >= 6)
 // chunk) item per wave at a time)
 // BN_: workgroup tile width; kNarrowBN for outputs at most that wide (attention head
 // dimensions), which would otherwise leave most of a 256-wide tile idle
-template <int BM, bool A4, int EPI, int DT, int LOG2B, int BN_ = kBN, bool F6 = false>
+template <int BM, bool A4, int EPI, int DT, int LOG2B, int BN_ = kBN, bool F6 = false, int F6K = 0>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   // 128-wide INT4 x INT4 tiles: 64 x 64 wave tiles (one widened fragment per MFMA)
   constexpr int WN = (A4 && BN_ == kMidBN) ? 64 : wave_n<A4, LOG2B>() < BN_ ? wave_n<A4, LOG2B>() : BN_;
@@ -746,7 +871,7 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   dim3 grid((unsigned)(((g.N + BN_ - 1) / BN_) * ((g.M + BM - 1) / BM)), 1u,
             (unsigned)(g.batch > 0 ? g.batch : splits));
   timing_begin(s);
-  gemm_kernel<BM, A4, WN, EPI, DT, LOG2B, BN_, F6><<<grid, C_::THREADS, 0, s>>>(g);
+  gemm_kernel<BM, A4, WN, EPI, DT, LOG2B, BN_, F6, F6K><<<grid, C_::THREADS, 0, s>>>(g);
   timing_end(s, id);
   return hipGetLastError();
 }

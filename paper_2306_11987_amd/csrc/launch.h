@@ -9,7 +9,7 @@ namespace hqlss {
 enum KernelId : int {
   kKAbsmax = 0, kKQuant, kKBitSplit, kKPlan, kKBuild,
   kKGemmFwd, kKGemmDx, kKGemmDw, kKGemmAcc, kKReduce, kKCopy, kKHsizeMax, kKHsizeErr,
-  kKHsizePick, kKLsqQuant, kKLsqStepGrad, kKFp6Convert, kKCount
+  kKHsizePick, kKLsqQuant, kKLsqStepGrad, kKFp6Convert, kKFp6Plan, kKFp6Build, kKCount
 };
 const char* kernel_name(int id);
 
@@ -140,6 +140,16 @@ struct GemmArgs {
   // of ds_part entries per batch.
   int batch;
   int64_t bs_a, bs_b, bs_out, bs_rows, bs_delta;
+  // FP6 route (launch_gemm6) only.  f6_kind 1: the dX product, whose tiles with rows below
+  // *m2_dev run a first K pass over A2 (upper codes, pitch lda) and weight rows by w_up,
+  // w_dn of their token out_rows[m]; f6_kind 2: the dW product, whose K entries come in
+  // weight classes 2^4 .. 2^0 starting at entries 0, kcls[0..3].
+  int f6_kind;
+  const void* A2;
+  const int32_t* m2_dev;
+  const uint8_t* w_up;
+  const uint8_t* w_dn;
+  const int32_t* kcls;
 };
 // Split-K factor the launcher uses for this shape (1 = no split), and the int32 partial
 // buffer it then needs (splits x M x N words).  A non-zero override forces the factor.
@@ -163,6 +173,25 @@ int gemm_split_override();                          // the test hook's forced fa
 // padded FP6 layout [rows][K]: every 32 codes become 24 bytes of e2m3 fields (field i at
 // bits 6i..6i+5, little-endian) followed by 8 zero bytes.  K a multiple of 64.
 hipError_t launch_int4_to_fp6(hipStream_t s, const uint8_t* src, uint8_t* dst, int64_t rows, int64_t K);
+// Row orders of the FP6 backward from the sample's weights (one workgroup, N <= 65536):
+// order6[n_kept] (upper tokens first), *n_up, the dW entries ent[] grouped by weight class
+// (capacity 4 N + 640, -1 = padding) and cls[5] = first entries of classes 3, 2, 1, 0 and
+// the padded entry count.
+hipError_t launch_fp6_plan(hipStream_t s, const uint8_t* w_up, const uint8_t* w_dn, int64_t N,
+                           int32_t* order6, int32_t* n_up, int32_t* ent, int32_t* cls);
+// FP6 operands of the backward GEMMs (padded FP6 layout):
+//   a_dn [N][C]: row i = lower codes of token order6[i] (zero when its w_dn = 0), i < n_kept;
+//   a_up [round_up(N, 256)][C]: row i = upper codes of token order6[i] for i < n_up, zero up
+//        to the next multiple of 256;
+//   a_dw [C][ecap], x_dw [D][ecap]: column e = the codes of entry ent[e] (upper or lower row of
+//        its token; X^ row of its token), zero for padding entries; e < cls[4].
+// Dropped tokens' rows of dX (dtype dt) are zeroed.  Any output may be null.
+hipError_t launch_fp6_build(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
+                            const uint8_t* w_up, const uint8_t* w_dn, const int32_t* order6,
+                            const int32_t* n_kept, const int32_t* n_up, const int32_t* ent,
+                            const int32_t* cls, const uint8_t* xq6, int64_t N, int64_t C,
+                            int64_t D, int64_t ecap, uint8_t* a_dn, uint8_t* a_up, uint8_t* a_dw,
+                            uint8_t* x_dw, void* dX);
 // Number of ds_part entries a kEpiDxL / kEpiDwL launch of this shape writes (one per
 // workgroup: of the GEMM, or of the reduction after split-K; every entry is written, 0 by
 // workgroups without rows).

@@ -394,6 +394,94 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
   }
 }
 
+// Orders of the kept rows for the FP6 MFMA route (gemm6.hip), one workgroup per problem.
+// Categories of a token t: upper (w_up = 1), kept lower-only (w_up = 0, w_dn > 0), and the
+// lower weight class e = log2 w_dn (0..4).
+//   order6: the kept tokens, upper tokens first, each part ascending (the dX row order:
+//           tiles holding upper tokens run a second K pass over the upper codes);
+//   ent:    the dW K entries (2 t + 1: the upper row of t, 2 t: its lower row) grouped by
+//           weight, classes 2^4 .. 2^0, each class padded with -1 to a multiple of 128 (one
+//           GEMM stage).  The upper weight 14 = 8 + 4 + 2 puts each upper row into classes
+//           3, 2 and 1 (after that class's lower rows);
+//   cls:    the first entries of classes 3, 2, 1, 0 and the padded total.
+// Each thread owns a contiguous range of tokens, so a block-wide exclusive scan of the
+// per-thread counts places every token in ascending order within its category.
+constexpr int kCat = 7;  // upper, lower-only, lower classes 0..4
+__global__ __launch_bounds__(1024) void fp6_plan_kernel(
+    const uint8_t* __restrict__ w_up, const uint8_t* __restrict__ w_dn, int N,
+    int32_t* __restrict__ order6, int32_t* __restrict__ n_up_out, int32_t* __restrict__ ent,
+    int32_t* __restrict__ cls) {
+  __shared__ int s_cnt[kCat][1024];
+  __shared__ int s_tot[kCat];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int per = (N + 1023) / 1024;
+  const int t0 = tid * per, t1 = min(N, t0 + per);
+  int c[kCat];
+#pragma unroll
+  for (int k = 0; k < kCat; ++k) c[k] = 0;
+  for (int t = t0; t < t1; ++t) {
+    const int up = w_up[t], dn = w_dn[t];
+    if (up) ++c[0];
+    else if (dn) ++c[1];
+    if (dn) ++c[2 + (31 - __clz(dn))];
+  }
+#pragma unroll
+  for (int k = 0; k < kCat; ++k) s_cnt[k][tid] = c[k];
+  __syncthreads();
+  if (wv < kCat) {  // wave k: exclusive scan of category k over the 1024 threads
+    int v[16], sum = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) { v[i] = s_cnt[wv][16 * lane + i]; sum += v[i]; }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) { s_cnt[wv][16 * lane + i] = run; run += v[i]; }
+    if (lane == 63) s_tot[wv] = incl;
+  }
+  __syncthreads();
+  const int n_up = s_tot[0], n_d0 = s_tot[2], n_d1 = s_tot[3], n_d2 = s_tot[4], n_d3 = s_tot[5],
+            n_d4 = s_tot[6];
+  auto r128 = [](int x) { return (x + 127) & ~127; };
+  const int b3 = r128(n_d4), b2 = b3 + r128(n_d3 + n_up), b1 = b2 + r128(n_d2 + n_up),
+            b0 = b1 + r128(n_d1 + n_up), ke = b0 + r128(n_d0);
+  const int base[5] = {b0, b1, b2, b3, 0};  // first entry of lower class e
+  int p_up = s_cnt[0][tid], p_rest = n_up + s_cnt[1][tid];
+  int p_d[5];
+#pragma unroll
+  for (int e = 0; e < 5; ++e) p_d[e] = base[e] + s_cnt[2 + e][tid];
+  for (int t = t0; t < t1; ++t) {
+    const int up = w_up[t], dn = w_dn[t];
+    if (up) {
+      order6[p_up] = t;
+      ent[b3 + n_d3 + p_up] = 2 * t + 1;
+      ent[b2 + n_d2 + p_up] = 2 * t + 1;
+      ent[b1 + n_d1 + p_up] = 2 * t + 1;
+      ++p_up;
+    } else if (dn) {
+      order6[p_rest++] = t;
+    }
+    if (dn) {
+      const int e = 31 - __clz(dn);
+      ent[p_d[e]++] = 2 * t;
+    }
+  }
+  // padding of every class to its 128-entry boundary
+  const int pad_lo[5] = {n_d4, b3 + n_d3 + n_up, b2 + n_d2 + n_up, b1 + n_d1 + n_up, b0 + n_d0};
+  const int pad_hi[5] = {b3, b2, b1, b0, ke};
+#pragma unroll
+  for (int q = 0; q < 5; ++q)
+    for (int i = pad_lo[q] + tid; i < pad_hi[q]; i += 1024) ent[i] = -1;
+  if (tid == 0) {
+    *n_up_out = n_up;
+    cls[0] = b3; cls[1] = b2; cls[2] = b1; cls[3] = b0; cls[4] = ke;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_t* scores,
@@ -437,6 +525,14 @@ hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, cons
       return hipErrorInvalidValue;
   }
   timing_end(s, kKBuild);
+  return hipGetLastError();
+}
+
+hipError_t launch_fp6_plan(hipStream_t s, const uint8_t* w_up, const uint8_t* w_dn, int64_t N,
+                           int32_t* order6, int32_t* n_up, int32_t* ent, int32_t* cls) {
+  timing_begin(s);
+  fp6_plan_kernel<<<1, 1024, 0, s>>>(w_up, w_dn, (int)N, order6, n_up, ent, cls);
+  timing_end(s, kKFp6Plan);
   return hipGetLastError();
 }
 

@@ -136,3 +136,123 @@ def test_fp6_forward_argument_errors():
     Y = torch.empty(64, 64, device="cuda", dtype=torch.float16)
     with pytest.raises(H.HQLSSError):
         H.hq_linear_fwd_fp6(X, W, Y, H.saved_fp6_empty(64, 128, 64), 0)
+
+
+# ---------------------------------------------------------------- backward (Sec. 4.2)
+BWD_SHAPES = SHAPES + [
+    (4096, 256, 192, 5, "f16", "sparse_rows"),  # ~10 % upper tokens: several two-pass dX tiles
+    (3000, 128, 320, 4, "bf16", "sparse_rows"),
+]
+
+
+def _backward_both(H, G, sv4, sv6, N, D, C, k, dt, budget, seed, offset):
+    tG = dev_tensor(G, dt)
+    dX4 = torch.empty(N, D, device="cuda", dtype=TORCH_DT[dt])
+    dW4 = torch.empty(C, D, device="cuda", dtype=TORCH_DT[dt])
+    H.lss_linear_bwd(tG, sv4, dX4, dW4, D, k, budget, seed, offset)
+    dX6 = torch.full((N, D), float("nan"), device="cuda", dtype=TORCH_DT[dt])
+    dW6 = torch.full((C, D), float("nan"), device="cuda", dtype=TORCH_DT[dt])
+    H.lss_linear_bwd_fp6(tG, sv6, dX6, dW6, D, k, budget, seed, offset)
+    torch.cuda.synchronize()
+    return tG, dX4, dW4, dX6, dW6
+
+
+def _plan(H, tG, sv6, N, D, C, budget, seed, offset):
+    plan = H.Plan.empty(N, C)
+    H.lss_grad_plan(tG, sv6, plan, D, budget, seed, offset)
+    return plan
+
+
+@pytest.mark.parametrize("budget_div", [1, 4])
+@pytest.mark.parametrize("shape", BWD_SHAPES, ids=lambda s: f"N{s[0]}_D{s[1]}_C{s[2]}_k{s[3]}_{s[4]}")
+def test_fp6_backward_parity(shape, budget_div):
+    """dX, dW of the FP6 route equal the int8 route's bit for bit and the oracle's to the
+    float bar; both int32 accumulators equal the oracle's."""
+    H = need_gpu()
+    lin, X, W, G = _case(shape, seed=1)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    budget = max(1, N // budget_div)
+    seed, offset = 1234, 77
+    say(f"FP6 backward parity {shape} budget={budget}")
+    sv4, _, sv6, _ = _forward_both(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)
+    b = O.lss_backward(G, f, budget, seed, offset)
+    tG, dX4, dW4, dX6, dW6 = _backward_both(H, G, sv4, sv6, N, D, C, k, dt, budget, seed, offset)
+    assert torch.equal(_bits(dX6), _bits(dX4)), "FP6 dX differs from the int8 route's"
+    assert torch.equal(_bits(dW6), _bits(dW4)), "FP6 dW differs from the int8 route's"
+    check_float_output("dX", dX6, b.dX, dt)
+    check_float_output("dW", dW6, b.dW, dt)
+    plan = _plan(H, tG, sv6, N, D, C, budget, seed, offset)
+    nk = len(b.plan.kept)
+    ws = H.workspace(H.WS_FROM_PLAN_FP6, N, D, C)
+    acc = torch.zeros(N, D, dtype=torch.int32, device="cuda")
+    H.debug_gemm_acc(11, plan, sv6, acc, N, D, C, ws)
+    accw = torch.empty(C, D, dtype=torch.int32, device="cuda")
+    H.debug_gemm_acc(12, plan, sv6, accw, N, D, C, ws)
+    torch.cuda.synchronize()
+    # FP6 dX rows come upper tokens first: compare by token
+    order = np.concatenate([b.plan.kept[b.plan.w_up[b.plan.kept] > 0], b.plan.kept[b.plan.w_up[b.plan.kept] == 0]])
+    pos = {int(t): i for i, t in enumerate(b.plan.kept)}
+    ref_rows = b.acc_dx[[pos[int(t)] for t in order]] if nk else b.acc_dx
+    assert np.array_equal(to_np(acc)[:nk], ref_rows.astype(np.int32)), "FP6 dX int32 accumulators"
+    assert np.array_equal(to_np(accw), b.acc_dw.astype(np.int32)), "FP6 dW int32 accumulators"
+
+
+def test_fp6_backward_keep_nonzero_and_live_sampling():
+    """The keep-non-zero budget and a small budget (lower rows sampled with weights up to 16:
+    every dW weight class in use) give the int8 route's bits."""
+    H = need_gpu()
+    lin, X, W, G = _case((2048, 512, 384, 7, "bf16", "sparse_rows"), seed=3)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    sv4, _, sv6, _ = _forward_both(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)
+    for budget in (H.BUDGET_KEEP_NONZERO, N // 8, N // 16):
+        say(f"FP6 backward budget {budget}")
+        b = O.lss_backward(G, f, budget, 9, 5)
+        if budget > 0:
+            assert (b.plan.w_dn >= 8).any(), "test must exercise the heavy weight classes"
+        _, dX4, dW4, dX6, dW6 = _backward_both(H, G, sv4, sv6, N, D, C, k, dt, budget, 9, 5)
+        assert torch.equal(_bits(dX6), _bits(dX4)) and torch.equal(_bits(dW6), _bits(dW4))
+        check_float_output("dX", dX6, b.dX, dt)
+        check_float_output("dW", dW6, b.dW, dt)
+
+
+@pytest.mark.parametrize("splits", [2, 3])
+def test_fp6_backward_forced_split_k(splits):
+    """Split along K, each split applying the weights due in its own range: still the bits."""
+    H = need_gpu()
+    lin, X, W, G = _case((1500, 640, 448, 6, "f16", "sparse_rows"), seed=4)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    sv4, _, sv6, _ = _forward_both(H, X, W, k, dt)
+    H.debug_set_gemm_splits(splits)
+    try:
+        say(f"FP6 backward forced split-K {splits}")
+        _, dX4, dW4, dX6, dW6 = _backward_both(H, G, sv4, sv6, N, D, C, k, dt, N // 6, 2, 3)
+    finally:
+        H.debug_set_gemm_splits(0)
+    assert torch.equal(_bits(dX6), _bits(dX4)) and torch.equal(_bits(dW6), _bits(dW4))
+
+
+@pytest.mark.parametrize("li", range(4))
+def test_fp6_backward_full_size_sweep(li):
+    """The GEMM sweep's linears at full size: dX and dW bit for bit equal to the int8 route's."""
+    H = need_gpu()
+    lin = synth.workload(3).linears[li]
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    say(f"FP6 backward full size {lin.name}")
+    X, W, G = synth.linear_inputs(lin, 3, li)
+    sv4, _, sv6, _ = _forward_both(H, X, W, k, dt)
+    del X, W
+    _, dX4, dW4, dX6, dW6 = _backward_both(H, G, sv4, sv6, N, D, C, k, dt, N, 42, 1000)
+    assert torch.equal(_bits(dX6), _bits(dX4)), "FP6 dX differs from the int8 route's"
+    assert torch.equal(_bits(dW6), _bits(dW4)), "FP6 dW differs from the int8 route's"
+
+
+def test_fp6_backward_argument_errors():
+    H = need_gpu()
+    G = torch.zeros(64, 11520, device="cuda", dtype=torch.float16)
+    dX = torch.empty(64, 64, device="cuda", dtype=torch.float16)
+    with pytest.raises(H.HQLSSError) as e:  # C = 11520 > 11412
+        H.lss_linear_bwd_fp6(G, H.saved_fp6_empty(64, 64, 11520), dX, None, 64, 0, 0, 0, 0,
+                             torch.empty(16, dtype=torch.uint8, device="cuda"))
+    assert "overflow" in str(e.value)
