@@ -94,7 +94,7 @@ def parse():
 
 def gemm_source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("gemm.hip", "common.h"):
+    for f in ("gemm.hip", "gemm_kernel.h", "gemm6.hip", "common.h"):
         with open(os.path.join(ROOT, "paper_2306_11987_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
