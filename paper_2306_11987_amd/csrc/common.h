@@ -75,9 +75,11 @@ __device__ __forceinline__ void st_stream2(void* p, uint2 v) {
     *static_cast<uint2*>(p) = v;
   }
 }
-// Cache policy per access site (1 = streaming, 0 = cached)
+// Cache policy per access site (1 = streaming, 0 = cached).  The maximum pass reads
+// cached: the quantizer or bit split that reads the same tensor next then finds part of
+// it in the 256 MB MALL.
 #ifndef HQ_NT_ABS_LD
-#define HQ_NT_ABS_LD 1
+#define HQ_NT_ABS_LD 0
 #endif
 #ifndef HQ_NT_Q_LD
 #define HQ_NT_Q_LD 1
