@@ -40,11 +40,35 @@ constexpr int kPlanThreadsSmall = 256;
 
 constexpr int kPlanRegs = 32;  // scores per thread kept in registers (2N <= 32 x threads)
 
-// two block-wide sums with one pair of barriers (red holds 2 WAVES words)
+// Sum of a 32-bit value over the wave (every lane gets it): DPP adds inside each row of
+// 16 lanes (swap neighbours, swap pairs, mirror halves, mirror the row), then the four row
+// sums read as scalars.  Needs every lane of the wave active.
+__device__ __forceinline__ uint32_t wave_sum_u32_dpp(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, true);   // quad_perm 1,0,3,2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, true);   // quad_perm 2,3,0,1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, true);  // row_half_mirror
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, true);  // row_mirror
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 0) + (uint32_t)__builtin_amdgcn_readlane((int)v, 16) +
+         (uint32_t)__builtin_amdgcn_readlane((int)v, 32) + (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+}
+
+// 64-bit wave sum as three 21-bit limbs (64 limbs of at most 22 bits stay below 2^28, so
+// each limb sum is exact in 32 bits), recombined modulo 2^64.
+__device__ __forceinline__ uint64_t wave_sum_u64_dpp(uint64_t v) {
+  constexpr uint64_t kM21 = (1ull << 21) - 1;
+  const uint32_t s0 = wave_sum_u32_dpp((uint32_t)(v & kM21));
+  const uint32_t s1 = wave_sum_u32_dpp((uint32_t)((v >> 21) & kM21));
+  const uint32_t s2 = wave_sum_u32_dpp((uint32_t)(v >> 42));
+  return (uint64_t)s0 + ((uint64_t)s1 << 21) + ((uint64_t)s2 << 42);
+}
+
+// Two block-wide sums with one barrier.  red holds 2 WAVES words; callers alternate
+// between two such buffers, so that a buffer is written again only after the barrier
+// that follows every read of it.
 template <int WAVES>
 __device__ __forceinline__ void block_sum2_u64(uint64_t& a, uint64_t& b, uint64_t* red) {
-  a = wave_sum_u64(a);
-  b = wave_sum_u64(b);
+  a = wave_sum_u64_dpp(a);
+  b = wave_sum_u64_dpp(b);
   if ((threadIdx.x & 63) == 0) {
     red[threadIdx.x >> 6] = a;
     red[WAVES + (threadIdx.x >> 6)] = b;
@@ -57,7 +81,6 @@ __device__ __forceinline__ void block_sum2_u64(uint64_t& a, uint64_t& b, uint64_
     a += red[i];
     b += red[WAVES + i];
   }
-  __syncthreads();
 }
 
 // 8 consecutive words from p + t0 (n8 of them valid, the rest 0).
@@ -79,7 +102,7 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     uint64_t offset, uint8_t* __restrict__ w_up, uint8_t* __restrict__ w_dn,
     int32_t* __restrict__ kept, int32_t* __restrict__ n_kept, uint64_t offset_stride) {
   constexpr int kPlanWaves = kPlanThreads / kWave;
-  __shared__ uint64_t red[2 * kPlanWaves];
+  __shared__ uint64_t red[4 * kPlanWaves];  // two buffers of block_sum2_u64
   __shared__ int wtot[kPlanWaves];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   {  // workgroup b samples batch b of a batched call (its own inputs, outputs and counters)
@@ -101,7 +124,7 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
     nz += p.x;
     st += ((uint64_t)p.z << 32) | p.y;
   }
-  block_sum2_u64<kPlanWaves>(nz, st, red);
+  block_sum2_u64<kPlanWaves>(nz, st, red);  // buffer 0; the rounds start on buffer 1
   const uint64_t S_all = st;
   const bool all_nonzero_kept = (int64_t)nz <= B;
 
@@ -119,6 +142,7 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
       cs[j] = (in_regs && i < n2) ? scores[i < N ? i : pitch + (i - N)] : 0u;
     }
     int64_t k = 0;
+    int par = 1;
     for (;;) {
       R = B - k;
       // R c >= S  <=>  c >= ceil(S / R) for integers and R > 0: one division per round
@@ -155,7 +179,8 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
         }
       }
       uint64_t cnt = n;
-      block_sum2_u64<kPlanWaves>(cnt, sum, red);
+      block_sum2_u64<kPlanWaves>(cnt, sum, red + 2 * kPlanWaves * par);
+      par ^= 1;
       if ((int64_t)cnt == k) break;  // nothing newly clamped
       k = (int64_t)cnt;
       S = S_all - sum;
