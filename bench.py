@@ -499,6 +499,22 @@ def main():
         cpu = cpu_baseline(lins, cfg_id, args.cpu_seconds, lsq_mode)
         progress("CPU baseline done")
 
+    # linears whose forward product runs on the FP6 MFMA (hq_linear_fwd's size rule): their
+    # forward workspace holds the FP6 copies of the codes
+    fwd_fp6 = []
+    if not (fp6_mode or lsq_mode):
+        for e in L:
+            lin = e["lin"]
+            auto = H.workspace_bytes(H.WS_FWD, lin.N, lin.D, lin.C)
+            H.debug_set_fwd_fp6(-1)
+            int8 = H.workspace_bytes(H.WS_FWD, lin.N, lin.D, lin.C)
+            H.debug_set_fwd_fp6(0)
+            if auto > int8:
+                fwd_fp6.append([lin.D, lin.C])
+    route = "FP6 MFMA (e2m3 codes)" if fp6_mode else "int8 MFMA"
+    if fwd_fp6:
+        route += "; forward products of the linears " + ", ".join(f"{d}x{c}" for d, c in fwd_fp6) + \
+                 " on the FP6 MFMA (e2m3 copies of the codes)"
     out = {
         "metric": METRIC,
         "value": round(tops, 2),
@@ -510,12 +526,12 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp6-e2m3" if fp6_mode else "i8",
+        "dtype": "fp6-e2m3" if fp6_mode else ("i8+fp6-e2m3" if fwd_fp6 else "i8"),
         "data": "synthetic",
         "config": {"workload": wl.name, "N": N, "linears": [[e["lin"].D, e["lin"].C] for e in L],
                    "log2_block": lins[0].log2_block, "io_dtype": lins[0].dtype, "budget": lins[0].budget,
                    "quantizer": "lsq (s = max|V H| / 14)" if lsq_mode else "per-tensor max",
-                   "route": "FP6 MFMA (e2m3 codes)" if fp6_mode else "int8 MFMA",
+                   "route": route,
                    "kept_tokens": [round(k, 1) for k in kept]},
         "frac_int8_peak": round(tops / INT8_PEAK_TOPS, 4),
         "timing": "median of per-step HIP-event times over the timed steps",

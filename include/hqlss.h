@@ -149,7 +149,11 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C);
  *   3. acc = X^ W^^T (int32, exact);
  *   4. Y = fl(alpha * acc), alpha = fl(fl(s_x s_w) / 2^k), cast to dt.
  * X [N][D], W [C][D] inputs; Y [N][C] output; saved: outputs (all fields required);
- * ws: scratch of at least hqlss_workspace_bytes(HQLSS_WS_FWD, ...) bytes. */
+ * ws: scratch of at least hqlss_workspace_bytes(HQLSS_WS_FWD, ...) bytes.
+ * Products of more than 2^38 multiply-adds (N D C) run step 3 on the FP6 MFMA, as
+ * hq_linear_fwd_fp6 does (every code is exact in e2m3 and the fp32 sums are exact), with
+ * the codes written a second time as FP6 into the workspace; acc, Y and the saved codes are
+ * the same bits either way, only the workspace size differs. */
 hqlss_status hq_linear_fwd(const void *X, const void *W, void *Y, int64_t N, int64_t D,
                            int64_t C, hqlss_dtype dt, int log2_block,
                            const hqlss_saved_t *saved, void *ws, size_t ws_bytes,
@@ -366,6 +370,12 @@ void hqlss_debug_set_gemm_splits(int splits);
  * on the width.  Workspace sizes follow the width in force when they are queried.  Per
  * calling thread, as the split hook. */
 void hqlss_debug_set_gemm_tile_n(int bn);
+
+/* Test hook: the product of hq_linear_fwd on the FP6 MFMA (mode > 0), on the int8 MFMA
+ * (mode < 0), or chosen by size (0, the default).  Results do not depend on it; workspace
+ * sizes follow the choice in force when they are queried.  Per calling thread, as the split
+ * hook. */
+void hqlss_debug_set_fwd_fp6(int mode);
 
 /* Benchmark hook: a plain device-to-device copy kernel ("copy") of `bytes` bytes (a
  * multiple of 16, both pointers 16-byte aligned, non-overlapping), asynchronous on

@@ -83,6 +83,7 @@ def _load() -> ctypes.CDLL:
         "hqlss_kernel_name": (ctypes.c_char_p, [_int]),
         "hqlss_debug_set_gemm_splits": (None, [_int]),
         "hqlss_debug_set_gemm_tile_n": (None, [_int]),
+        "hqlss_debug_set_fwd_fp6": (None, [_int]),
         "hqlss_debug_copy": (st, [_vp, _vp, _sz, _vp]),
     }
     for name, (res, args) in sig.items():
@@ -464,6 +465,11 @@ def debug_set_gemm_splits(splits: int) -> None:
 
 def debug_set_gemm_tile_n(bn: int) -> None:
     lib.hqlss_debug_set_gemm_tile_n(int(bn))
+
+
+def debug_set_fwd_fp6(mode: int) -> None:
+    """Test hook: hq_linear_fwd's product on FP6 (mode > 0), int8 (< 0) or by size (0)."""
+    lib.hqlss_debug_set_fwd_fp6(int(mode))
 
 
 def debug_copy(src: torch.Tensor, dst: torch.Tensor) -> None:

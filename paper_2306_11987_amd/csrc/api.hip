@@ -100,7 +100,24 @@ size_t dx_gemm_partial(int64_t N, int64_t D, int64_t C) {
 size_t dw_gemm_partial(int64_t N, int64_t D, int64_t C) {
   return al(gemm_partial_bytes(C, D, gemm_splits(C, D, (N + 127) / 128 * 128, false, true)));
 }
-size_t fwd_bytes(int64_t N, int64_t D, int64_t C) { return kFwdHead + fwd_gemm_partial(N, D, C); }
+// The forward product of hq_linear_fwd runs on the FP6 MFMA (the quantizer then also writes
+// the codes as FP6 into the workspace) when the product is large enough for the faster
+// matrix cores to repay the N D + C D bytes of those extra codes: above 2^38 multiply-adds
+// (measured at N = 16384: 4096 x 4096 breaks even, 4096 x 11008 and 8192 x 8192 gain
+// 54-65 us per launch).  A per-thread test hook forces either product.
+thread_local int g_fwd_fp6_override = 0;  // 1: FP6, -1: int8, 0: by size
+bool fwd_uses_fp6(int64_t N, int64_t D, int64_t C) {
+  if (g_fwd_fp6_override) return g_fwd_fp6_override > 0;
+  return (double)N * (double)D * (double)C > 274877906944.0;  // 2^38
+}
+size_t fwd6_partial(int64_t N, int64_t D, int64_t C);
+// int8 product: the absmax partials and the split-K partials; FP6 product (fp6 = true): also
+// the FP6 codes of X and W
+size_t fwd_bytes(int64_t N, int64_t D, int64_t C, bool fp6) {
+  return fp6 ? kFwdHead + al(N * D) + al(C * D) + fwd6_partial(N, D, C)
+             : kFwdHead + fwd_gemm_partial(N, D, C);
+}
+size_t fwd_bytes(int64_t N, int64_t D, int64_t C) { return fwd_bytes(N, D, C, fwd_uses_fp6(N, D, C)); }
 // FP6 route: the forward's INT4 codes (X^, W^, W^^T) staged before their conversion
 size_t fwd6_partial(int64_t N, int64_t D, int64_t C) {
   return al(gemm_partial_bytes(N, C, gemm6_splits(N, C, D)));
@@ -227,12 +244,31 @@ constexpr size_t kLogPairs = 4096;
 
 // ---------------------------------------------------------------- the two passes
 hqlss_status do_fwd(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
-                    int dt, int k, const hqlss_saved_t* sv, void* ws, hipStream_t s) {
+                    int dt, int k, const hqlss_saved_t* sv, void* ws, bool fp6, hipStream_t s) {
   uint32_t* amax = reinterpret_cast<uint32_t*>(sv->amax);
   float* px = static_cast<float*>(ws);  // [2][kQMaxWg] absmax partials
   float* pw = px + kQMaxWg;
   QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
   HQ_TRY(launch_fwht_absmax(s, dt, k, jx, px, jw, pw));
+  if (fp6 && Y) {  // the codes also as FP6 (workspace), the product on the FP6 MFMA
+    Carve w{static_cast<char*>(ws), kFwdHead, fwd_bytes(N, D, C, true)};
+    uint8_t* x6 = w.take<uint8_t>(N * D);
+    uint8_t* w6 = w.take<uint8_t>(C * D);
+    int32_t* part = w.take<int32_t>(fwd6_partial(N, D, C));
+    const QOut ox{px, jx.wg, sv->amax, sv->xq, sv->x_sumsq, nullptr, x6};
+    const QOut ow{pw, jw.wg, sv->amax + 1, sv->wq, nullptr, sv->wqT, w6};
+    HQ_TRY(launch_fwht_quant(s, dt, k, jx, ox, jw, ow));
+    GemmArgs g{};
+    g.A = x6; g.lda = D;
+    g.B = w6; g.ldb = D;
+    g.M = N; g.N = C; g.K = D;
+    g.out = Y; g.ldo = C;
+    g.amax1 = amax; g.amax2 = amax + 1;
+    g.denom = (float)(int64_t(1) << k);
+    g.log2b = k;
+    HQ_TRY(launch_gemm6(s, kEpiFwd, dt, g, gemm6_splits(N, C, D), part));
+    return HQLSS_OK;
+  }
   const QOut ox{px, jx.wg, sv->amax, sv->xq, sv->x_sumsq};
   const QOut ow{pw, jw.wg, sv->amax + 1, sv->wq, nullptr, sv->wqT};  // W^ and W^^T
   HQ_TRY(launch_fwht_quant(s, dt, k, jx, ox, jw, ow));
@@ -267,11 +303,9 @@ hqlss_status do_fwd_fp6(const void* X, const void* W, void* Y, int64_t N, int64_
   int32_t* part = w.take<int32_t>(fwd6_partial(N, D, C));
   QJob jx = make_job(X, N, D), jw = make_job(W, C, D);
   HQ_TRY(launch_fwht_absmax(s, dt, k, jx, px, jw, pw));
-  const QOut ox{px, jx.wg, sv->amax, xq4, sv->x_sumsq};
-  const QOut ow{pw, jw.wg, sv->amax + 1, wq4, nullptr, wqT4};
+  const QOut ox{px, jx.wg, sv->amax, xq4, sv->x_sumsq, nullptr, sv->xq};
+  const QOut ow{pw, jw.wg, sv->amax + 1, wq4, nullptr, wqT4, sv->wq};
   HQ_TRY(launch_fwht_quant(s, dt, k, jx, ox, jw, ow));
-  HQ_TRY(launch_int4_to_fp6(s, xq4, sv->xq, N, D));
-  HQ_TRY(launch_int4_to_fp6(s, wq4, sv->wq, C, D));
   HQ_TRY(launch_int4_to_fp6(s, wqT4, sv->wqT, D, C));
   if (Y) {
     GemmArgs g{};
@@ -778,9 +812,10 @@ hqlss_status hq_linear_fwd(const void* X, const void* W, void* Y, int64_t N, int
   if ((st = check_saved(saved))) return st;
   if (!a16(X) || !a16(W) || !a16(Y)) return HQLSS_ERR_ALIGN;
   if ((st = check_fwd_overflow(D))) return st;
-  if (!ws || ws_bytes < fwd_bytes(N, D, C)) return HQLSS_ERR_WORKSPACE;
+  const bool fp6 = fwd_uses_fp6(N, D, C);
+  if (!ws || ws_bytes < fwd_bytes(N, D, C, fp6)) return HQLSS_ERR_WORKSPACE;
   if (!a16(ws)) return HQLSS_ERR_ALIGN;
-  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
+  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, fp6, static_cast<hipStream_t>(stream));
 }
 
 hqlss_status hq_linear_fwd_noalloc(const void* X, const void* W, void* Y, int64_t N, int64_t D,
@@ -794,10 +829,10 @@ hqlss_status hq_linear_fwd_noalloc(const void* X, const void* W, void* Y, int64_
   if ((st = check_saved(saved))) return st;
   if (!a16(X) || !a16(W) || !a16(Y)) return HQLSS_ERR_ALIGN;
   if ((st = check_fwd_overflow(D))) return st;
-  if (fwd_bytes(N, D, C) > HQLSS_STATIC_SCRATCH_BYTES) return HQLSS_ERR_SCRATCH;
+  if (fwd_bytes(N, D, C, false) > HQLSS_STATIC_SCRATCH_BYTES) return HQLSS_ERR_SCRATCH;
   void* ws = nullptr;
   if ((st = scratch_address(&ws))) return st;
-  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, static_cast<hipStream_t>(stream));
+  return do_fwd(X, W, Y, N, D, C, dt, log2_block, saved, ws, false, static_cast<hipStream_t>(stream));
 }
 
 hqlss_status hq_linear_fwd_fp6(const void* X, const void* W, void* Y, int64_t N, int64_t D, int64_t C,
@@ -1002,7 +1037,7 @@ hqlss_status hqlss_debug_gemm_acc(int which, const lss_plan_t* plan, const hqlss
     g.M = N; g.N = C; g.K = D;
     g.out = acc; g.ldo = C;
     const int sp = gemm_splits(N, C, D, true, true);
-    if (sp > 1 && (!ws || ws_bytes < fwd_bytes(N, D, C))) return HQLSS_ERR_WORKSPACE;
+    if (sp > 1 && (!ws || ws_bytes < fwd_bytes(N, D, C, false))) return HQLSS_ERR_WORKSPACE;
     int32_t* part = sp > 1 ? reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kFwdHead)
                            : nullptr;
     return hip_status(launch_gemm(s, kEpiAcc, HQLSS_F32, true, true, g, sp, part));
@@ -1077,6 +1112,7 @@ const char* hqlss_kernel_name(int id) { return hqlss::kernel_name(id); }
 
 void hqlss_debug_set_gemm_splits(int splits) { hqlss::gemm_set_split_override(splits); }
 void hqlss_debug_set_gemm_tile_n(int bn) { hqlss::gemm_set_tile_override(bn); }
+void hqlss_debug_set_fwd_fp6(int mode) { g_fwd_fp6_override = mode > 0 ? 1 : mode < 0 ? -1 : 0; }
 
 hqlss_status hqlss_debug_copy(const void* src, void* dst, size_t bytes, void* stream) {
   if (!src || !dst) return HQLSS_ERR_NULL;

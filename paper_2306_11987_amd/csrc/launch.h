@@ -54,6 +54,8 @@ struct QOut {
   uint8_t* packed;
   int32_t* row_sumsq;  // may be null
   uint8_t* packed_t;   // may be null; honoured for the second job only
+  uint8_t* fp6;        // may be null: the codes again, as FP6 (e2m3) in the padded layout
+                       // of fp6.hip (row pitch: cols bytes), row-major
 };
 hipError_t launch_fwht_quant(hipStream_t s, int dt, int log2b, const QJob& j0, const QOut& o0,
                              const QJob& j1, const QOut& o1);

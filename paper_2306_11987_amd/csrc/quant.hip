@@ -101,6 +101,39 @@ __device__ __forceinline__ void fwht16(float v[16], int lane) {
 // Bits of fl(x + 1.5 * 2^23): rint(x) (half-to-even) sits in the low mantissa bits.
 __device__ __forceinline__ uint32_t rne_bits(float x) { return __float_as_uint(x + kRne); }
 
+// 16 consecutive codes (as rne_bits) -> their 12 bytes of FP6 (e2m3) fields, field i at bits
+// 6i..6i+5: half of a 32-code group of the padded FP6 layout.  The hardware conversion of
+// two 16-float operands interleaves them (field 2k from the first, 2k + 1 from the second),
+// so even and odd codes go in separately; the upper 16 fields come out zero.  Exact: the
+// codes are integers |q| <= 7, all e2m3 values, and the scale is 1.  The instruction is
+// issued through inline assembly with an early-clobber result: the compiler builtin let
+// the result registers overlap the source registers, and the instruction then read some
+// sources after writing over them (wrong fields at one fixed position of the chunk).
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x6 __attribute__((ext_vector_type(6)));
+__device__ __forceinline__ uint3 fp6_half16(const uint32_t y[16]) {
+  f32x16 ev, od;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    ev[k] = __uint_as_float(y[2 * k]) - kRne;
+    od[k] = __uint_as_float(y[2 * k + 1]) - kRne;
+    ev[8 + k] = 0.f;
+    od[8 + k] = 0.f;
+  }
+  i32x6 w;
+  asm volatile("v_cvt_scalef32_2xpk16_fp6_f32 %0, %1, %2, 1.0" : "=&v"(w) : "v"(ev), "v"(od));
+  return make_uint3((uint32_t)w[0], (uint32_t)w[1], (uint32_t)w[2]);
+}
+
+// Store the FP6 fields of 16-code chunk c of a row (row base `row6`, padded layout): the
+// even chunk of a group fills bytes 0..11, the odd one bytes 12..23 and the 8 zero bytes.
+__device__ __forceinline__ void store_fp6_chunk(uint8_t* row6, int64_t c, const uint32_t y[16]) {
+  const uint3 f = fp6_half16(y);
+  uint8_t* p = row6 + (c >> 1) * 32 + (c & 1) * 12;
+  *reinterpret_cast<uint3*>(p) = f;
+  if (c & 1) *reinterpret_cast<uint2*>(p + 12) = make_uint2(0u, 0u);
+}
+
 // Pack 8 codes given as rne_bits (low nibbles) into one word, element j at bits 4j.
 __device__ __forceinline__ uint32_t pack8_bits(const uint32_t y[8]) {
   uint32_t b[4];
@@ -253,7 +286,7 @@ template <int LOG2B> struct TileT {
 template <int DT, int LOG2B, bool LSQ>
 __device__ void quant_tile(const void* src, int64_t rows, int64_t cols, float inv, int t,
                            uint8_t* __restrict__ packed, uint16_t* __restrict__ delta,
-                           uint8_t* __restrict__ packed_t) {
+                           uint8_t* __restrict__ packed_t, uint8_t* __restrict__ fp6 = nullptr) {
   using T = TileT<LOG2B>;
   constexpr int TW = T::TW, LPR = T::LPR, R = T::R, PITCH = TW + 4;
   __shared__ uint8_t tile[R * PITCH];
@@ -292,6 +325,7 @@ __device__ void quant_tile(const void* src, int64_t rows, int64_t cols, float in
     if (ok) {
       st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(packed + r * (cols / 2)) + c,
                              make_uint2(pack8_bits(y), pack8_bits(y + 8)));
+      if (fp6) store_fp6_chunk(fp6 + r * cols, c, y);
       if constexpr (LSQ) {
         uint4* dp = reinterpret_cast<uint4*>(delta + r * cols) + 2 * c;
         st_stream<HQ_NT_Q_ST>(dp, make_uint4(dh[0], dh[1], dh[2], dh[3]));
@@ -328,7 +362,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
     const int t = (int)blockIdx.x - j0.wg - j1.wg;
     if (t == 0 && threadIdx.x == 0) *o1.amax_out = a;
     quant_tile<DT, LOG2B, false>(j1.src, j1.rows, j1.cols, a > 0.f ? 7.0f / a : 0.f, t, o1.packed,
-                                 nullptr, o1.packed_t);
+                                 nullptr, o1.packed_t, o1.fp6);
     return;
   }
   const bool second = (int)blockIdx.x >= j0.wg;
@@ -365,6 +399,7 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
         const bool ok = g.valid(kp);
         const int64_t r = g.row_of(kp);
         if (ok) st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(o.packed + r * (j.cols / 2)) + (int64_t)ip * g.G + g.sub, make_uint2(w0, w1));
+        if (ok && o.fp6) store_fp6_chunk(o.fp6 + r * j.cols, (int64_t)ip * g.G + g.sub, y);
         if (++ip == g.iters) {  // end of the group's row
           if (o.row_sumsq) {
             ss = group_sum(ss, g.G);

@@ -290,3 +290,27 @@ def test_forced_gemm_tile_width(bn):
         check_float_output("dW", dW, b.dW, dt)
     finally:
         H.debug_set_gemm_tile_n(0)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"N{s[0]}_D{s[1]}_C{s[2]}_k{s[3]}_{s[4]}")
+def test_forward_fp6_product(shape):
+    """hq_linear_fwd with its product forced onto the FP6 MFMA (the quantizer then also
+    writes the codes as FP6): codes, scales and row sums bit-exact against the oracle, Y
+    within the forward tolerance, and Y bit for bit the int8 product's."""
+    H = need_gpu()
+    lin, X, W, _ = _case(shape, seed=3)
+    k, dt = lin.log2_block, lin.dtype
+    say(f"forward, FP6 product {shape}")
+    try:
+        H.debug_set_fwd_fp6(1)
+        saved6, Y6 = run_forward(H, X, W, k, dt)
+        rel = check_forward(H, X, W, k, dt, saved6, Y6)
+        assert rel <= (1e-5 if dt == "f32" else 2e-3)
+        H.debug_set_fwd_fp6(-1)
+        saved8, Y8 = run_forward(H, X, W, k, dt)
+    finally:
+        H.debug_set_fwd_fp6(0)
+    assert torch.equal(Y6.view(torch.int16 if Y6.dtype != torch.float32 else torch.int32),
+                       Y8.view(torch.int16 if Y8.dtype != torch.float32 else torch.int32))
+    for name in ("xq", "wq", "wqT", "x_sumsq", "amax"):
+        assert torch.equal(getattr(saved6, name), getattr(saved8, name)), name
