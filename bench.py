@@ -372,6 +372,22 @@ def main():
     # scale is implementation cost): F2+F3 (maximum + quantiser of X and W) and B1+B2
     # (maximum + bit split of dY), each over the summed time of its kernels
     stages = {}
+    # linears whose forward product runs on the FP6 MFMA (hq_linear_fwd's size rule): their
+    # forward workspace holds the FP6 copies of the codes
+    fwd_fp6 = []
+    if not (fp6_mode or lsq_mode):
+        for e in L:
+            lin = e["lin"]
+            auto = H.workspace_bytes(H.WS_FWD, lin.N, lin.D, lin.C)
+            H.debug_set_fwd_fp6(-1)
+            int8 = H.workspace_bytes(H.WS_FWD, lin.N, lin.D, lin.C)
+            H.debug_set_fwd_fp6(0)
+            if auto > int8:
+                fwd_fp6.append([lin.D, lin.C])
+    # bytes of the FP6 copies of the codes that the quantizer writes: X and W of every
+    # linear on the FP6 route, of the FP6-product linears otherwise
+    copies6 = sum(e["lin"].N * e["lin"].D + e["lin"].C * e["lin"].D for e in L
+                  if fp6_mode or [e["lin"].D, e["lin"].C] in fwd_fp6)
     if lsq_mode:
         b_q = sum((eb + 2.5) * (e["lin"].N + e["lin"].C) * e["lin"].D + 0.5 * e["lin"].C * e["lin"].D
                   + 4 * (e["lin"].N + e["lin"].C) for e in L)
@@ -403,6 +419,11 @@ def main():
             gbs = b / (us * 1e-6) / 1e9
             hbm[stage] = {"algorithmic_MB_per_step": round(b / 1e6, 2), "us_per_step": round(us, 1),
                           "achieved_GBps": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+            if stage.startswith("F2+F3") and copies6 > 0:
+                # the quantizer also writes FP6 copies of the codes for the FP6 products
+                gbs6 = (b + copies6) / (us * 1e-6) / 1e9
+                hbm[stage].update({"fp6_copies_MB_per_step": round(copies6 / 1e6, 2),
+                                   "frac_with_fp6_copies": round(gbs6 / HBM_PEAK_GBS, 4)})
     overhead = {k: round(kernels[k]["us_per_step"], 1)
                 for k in ("build_operands", "lss_plan", "gemm_reduce", "lsq_step_grad", "fp6_convert",
                           "fp6_plan", "fp6_build") if k in kernels}
@@ -499,18 +520,6 @@ def main():
         cpu = cpu_baseline(lins, cfg_id, args.cpu_seconds, lsq_mode)
         progress("CPU baseline done")
 
-    # linears whose forward product runs on the FP6 MFMA (hq_linear_fwd's size rule): their
-    # forward workspace holds the FP6 copies of the codes
-    fwd_fp6 = []
-    if not (fp6_mode or lsq_mode):
-        for e in L:
-            lin = e["lin"]
-            auto = H.workspace_bytes(H.WS_FWD, lin.N, lin.D, lin.C)
-            H.debug_set_fwd_fp6(-1)
-            int8 = H.workspace_bytes(H.WS_FWD, lin.N, lin.D, lin.C)
-            H.debug_set_fwd_fp6(0)
-            if auto > int8:
-                fwd_fp6.append([lin.D, lin.C])
     route = "FP6 MFMA (e2m3 codes)" if fp6_mode else "int8 MFMA"
     if fwd_fp6:
         route += "; forward products of the linears " + ", ".join(f"{d}x{c}" for d, c in fwd_fp6) + \
