@@ -386,11 +386,14 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
       const uint2 lo = interleave8(v), hi = interleave8(v + 8);
       st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
     }
-    uint32_t* tp = reinterpret_cast<uint32_t*>(&tile[r][q]);  // 4-byte aligned: pitch 132
+    // word w of row r sits at word w ^ ((r / 16) % 8) of the row: the transpose below reads
+    // one column of 8 row blocks at once, which would otherwise fall on 4 banks
+    uint32_t* tp = reinterpret_cast<uint32_t*>(&tile[r][0]);  // 4-byte aligned: pitch 132
+    const int sw = (r >> 4) & 7;
 #pragma unroll
     for (int w = 0; w < 4; ++w)
-      tp[w] = ((uint32_t)v[4 * w] & 0xFFu) | (((uint32_t)v[4 * w + 1] & 0xFFu) << 8) |
-              (((uint32_t)v[4 * w + 2] & 0xFFu) << 16) | (((uint32_t)v[4 * w + 3] & 0xFFu) << 24);
+      tp[(q / 4 + w) ^ sw] = ((uint32_t)v[4 * w] & 0xFFu) | (((uint32_t)v[4 * w + 1] & 0xFFu) << 8) |
+                             (((uint32_t)v[4 * w + 2] & 0xFFu) << 16) | (((uint32_t)v[4 * w + 3] & 0xFFu) << 24);
   }
   if (isA && !At) return;  // uniform: no transpose wanted
   __syncthreads();
@@ -399,18 +402,19 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
   for (int k = 0; k < 4; ++k) {
     const int item = tid + 256 * k, c = item >> 3, q = (item & 7) * 16;
     if (col0 + c >= ncol) continue;
+    const int cs = (((c >> 2) ^ ((q >> 4) & 7)) << 2) | (c & 3);  // column c's byte in rows q..q+15
     if (isA) {
       int a[16];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) a[j] = tile[q + j][c];
+      for (int j = 0; j < 16; ++j) a[j] = tile[q + j][cs];
       const uint2 lo = interleave8(a), hi = interleave8(a + 8);
       st_stream<HQ_NT_B_ST>(At + (col0 + c) * pitch + i0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
     } else {
       uint32_t w0 = 0, w1 = 0;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const uint32_t byte = ((uint32_t)tile[q + 2 * j][c] & 15u) |
-                              (((uint32_t)tile[q + 2 * j + 1][c] & 15u) << 4);
+        const uint32_t byte = ((uint32_t)tile[q + 2 * j][cs] & 15u) |
+                              (((uint32_t)tile[q + 2 * j + 1][cs] & 15u) << 4);
         if (j < 4) w0 |= byte << (8 * j);
         else w1 |= byte << (8 * (j - 4));
       }
