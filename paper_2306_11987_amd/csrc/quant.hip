@@ -7,6 +7,8 @@
 //    (the ||X_i|| factor of the leverage score, Sec. 4.2).  One launch serves X and W:
 //    X by rows, W by tiles, each tile workgroup writing its codes row-major and also
 //    transposed through LDS (the K-contiguous operand of the dX GEMM), so W is read once.
+//    On request the codes of X and W are also written as FP6 (e2m3, the padded layout of
+//    fp6.hip) for a product on the FP6 MFMA, through the hardware conversion.
 //  * fwht_lsq: the same transform quantised at a caller-given (learned) step in one pass,
 //    with the fp16 deltas q - I r that the learned-step backward needs (Eq. 2, App. A.3);
 //    the second tensor by tiles as above.
