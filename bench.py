@@ -153,8 +153,8 @@ def _auto_rotation(L, eb):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); "
-              "multi-GPU runs are not part of it", file=sys.stderr)
+        print(f"bench.py: the operator runs on exactly one GPU (asked for {args.gpus}); "
+              "multi-GPU runs are not supported", file=sys.stderr)
         sys.exit(3)
 
     import numpy as np
