@@ -163,6 +163,11 @@ size_t dx_bytes(int64_t N, int64_t D, int64_t C) {
 size_t dw_bytes(int64_t N, int64_t D, int64_t C) {
   return al(C * rup(N, kPad)) + al(D * rup(N, kPad) / 2) + dw_gemm_partial(N, D, C);
 }
+// dynamic-scale gradients (do_grads without lsq): dX and dW share the int8 operand A_T
+size_t grads_bytes(int64_t N, int64_t D, int64_t C, bool dx, bool dw) {
+  if (dx && dw) return dx_bytes(N, D, C) + al(D * rup(N, kPad) / 2) + dw_gemm_partial(N, D, C);
+  return (dx ? dx_bytes(N, D, C) : 0) + (dw ? dw_bytes(N, D, C) : 0);
+}
 // learned-step-size mode: per-workgroup sums of acc * delta of the dX and dW epilogues
 int64_t lsq_parts_dx(int64_t N, int64_t D, int64_t C) {
   return gemm_epi_parts(N, D, gemm_splits(N, D, C, false, true));
@@ -512,19 +517,20 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   const bool want_dx = dX || (acc && which_acc == 1);
   const bool want_dw = dW || (acc && which_acc == 2);
   const int64_t Kp = rup(N, kPad);
+  // The dynamic-scale dW product reads the dX operand A_T itself, k-major (its kept rows
+  // are the K of dW), through transposing LDS reads; the learned-step one reads A_T^T.
+  const bool dw_kmajor = lsq == nullptr;
   int8_t* Ag = nullptr;
   int32_t* part_dx = nullptr;
   const int sp_dx = gemm_splits(N, D, C, false, true);
-  if (want_dx) {
-    Ag = w.take<int8_t>(Kp * C);
-    part_dx = w.take<int32_t>(gemm_partial_bytes(N, D, sp_dx));
-  }
+  if (want_dx || (want_dw && dw_kmajor)) Ag = w.take<int8_t>(Kp * C);
+  if (want_dx) part_dx = w.take<int32_t>(gemm_partial_bytes(N, D, sp_dx));
   int8_t* At = nullptr;
   uint8_t* XtT = nullptr;
   int32_t* part_dw = nullptr;
   const int sp_dw = gemm_splits(C, D, Kp, false, true);
   if (want_dw) {
-    At = w.take<int8_t>(C * Kp);
+    if (!dw_kmajor) At = w.take<int8_t>(C * Kp);
     XtT = w.take<uint8_t>(D * Kp / 2);
     part_dw = w.take<int32_t>(gemm_partial_bytes(C, D, sp_dw));
   }
@@ -553,7 +559,11 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   }
   if (want_dw) {
     GemmArgs g{};
-    g.A = At; g.lda = Kp;
+    if (dw_kmajor) {
+      g.A = Ag; g.lda = C; g.a_kmajor = 1;
+    } else {
+      g.A = At; g.lda = Kp;
+    }
     g.B = XtT; g.ldb = Kp / 2;
     g.M = C; g.N = D; g.K = Kp; g.k_dev = p->n_kept;
     g.amax1 = ag; g.amax2 = amax; g.denom = denom; g.log2b = k;
@@ -710,9 +720,8 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
     case HQLSS_WS_FWD: return fwd_bytes(N, D, C);
     case HQLSS_WS_BWD_DX: return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C);
     case HQLSS_WS_BWD_DW: return plan_bytes(N, C) + plan_scratch_bytes(N) + dw_bytes(N, D, C);
-    case HQLSS_WS_BWD:
-      return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C) + dw_bytes(N, D, C);
-    case HQLSS_WS_FROM_PLAN: return dx_bytes(N, D, C) + dw_bytes(N, D, C);
+    case HQLSS_WS_BWD: return plan_bytes(N, C) + plan_scratch_bytes(N) + grads_bytes(N, D, C, true, true);
+    case HQLSS_WS_FROM_PLAN: return grads_bytes(N, D, C, true, true);
     case HQLSS_WS_PLAN: return plan_scratch_bytes(N);
     case HQLSS_WS_HSIZE: return hsize_bytes();
     case HQLSS_WS_FWD_LSQ: return fwd_gemm_partial(N, D, C);
@@ -923,7 +932,7 @@ hqlss_status lss_linear_bwd_from_plan(const lss_plan_t* plan, const hqlss_saved_
   if ((st = check_plan(plan))) return st;
   if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
   if ((st = check_bwd_overflow(N, D, C, log2_block))) return st;
-  const size_t need = (dX ? dx_bytes(N, D, C) : 0) + (dW ? dw_bytes(N, D, C) : 0);
+  const size_t need = grads_bytes(N, D, C, dX != nullptr, dW != nullptr);
   if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
   Carve w{static_cast<char*>(ws), 0, ws_bytes};
   return do_grads(plan, saved, dX, dW, nullptr, 0, N, D, C, dt, log2_block, w,
@@ -938,8 +947,7 @@ static hqlss_status bwd_impl(const void* dY, const hqlss_saved_t* saved, void* d
   hqlss_status st;
   if ((st = check_bwd_common(dY, saved, N, D, C, dt, log2_block, budget_rows))) return st;
   if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws))) return HQLSS_ERR_ALIGN;
-  const size_t need = plan_bytes(N, C) + plan_scratch_bytes(N) + (dX ? dx_bytes(N, D, C) : 0) +
-                      (dW ? dw_bytes(N, D, C) : 0);
+  const size_t need = plan_bytes(N, C) + plan_scratch_bytes(N) + grads_bytes(N, D, C, dX != nullptr, dW != nullptr);
   if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Carve w{static_cast<char*>(ws), 0, ws_bytes};

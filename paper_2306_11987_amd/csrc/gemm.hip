@@ -210,49 +210,49 @@ int fwd_bn(int64_t M, int64_t N, int splits, int64_t batch) {
 }
 
 // the Hadamard block is a template parameter of the gradient epilogues
-template <int BM, bool A4, int EPI, int DT>
+template <int BM, bool A4, int EPI, int DT, bool TRA = false>
 hipError_t gemm_b(hipStream_t s, const GemmArgs& g, int splits, int id) {
   if constexpr (EPI == kEpiDx || EPI == kEpiDw || EPI == kEpiDxL || EPI == kEpiDwL) {
     const int bn = grad_bn(g.M, g.N, splits);
     if (bn == kMidBN) {
       switch (g.log2b) {
-        case 0: return gemm_t<BM, A4, EPI, DT, 0, kMidBN>(s, g, splits, id);
-        case 1: return gemm_t<BM, A4, EPI, DT, 1, kMidBN>(s, g, splits, id);
-        case 2: return gemm_t<BM, A4, EPI, DT, 2, kMidBN>(s, g, splits, id);
-        case 3: return gemm_t<BM, A4, EPI, DT, 3, kMidBN>(s, g, splits, id);
-        case 4: return gemm_t<BM, A4, EPI, DT, 4, kMidBN>(s, g, splits, id);
-        case 5: return gemm_t<BM, A4, EPI, DT, 5, kMidBN>(s, g, splits, id);
-        case 6: return gemm_t<BM, A4, EPI, DT, 6, kMidBN>(s, g, splits, id);
-        case 7: return gemm_t<BM, A4, EPI, DT, 7, kMidBN>(s, g, splits, id);
+        case 0: return gemm_t<BM, A4, EPI, DT, 0, kMidBN, false, 0, TRA>(s, g, splits, id);
+        case 1: return gemm_t<BM, A4, EPI, DT, 1, kMidBN, false, 0, TRA>(s, g, splits, id);
+        case 2: return gemm_t<BM, A4, EPI, DT, 2, kMidBN, false, 0, TRA>(s, g, splits, id);
+        case 3: return gemm_t<BM, A4, EPI, DT, 3, kMidBN, false, 0, TRA>(s, g, splits, id);
+        case 4: return gemm_t<BM, A4, EPI, DT, 4, kMidBN, false, 0, TRA>(s, g, splits, id);
+        case 5: return gemm_t<BM, A4, EPI, DT, 5, kMidBN, false, 0, TRA>(s, g, splits, id);
+        case 6: return gemm_t<BM, A4, EPI, DT, 6, kMidBN, false, 0, TRA>(s, g, splits, id);
+        case 7: return gemm_t<BM, A4, EPI, DT, 7, kMidBN, false, 0, TRA>(s, g, splits, id);
       }
       return hipErrorInvalidValue;
     }
     if (bn == kNarrowBN) {  // narrow output: blocks of at most 64 columns
       switch (g.log2b) {
-        case 0: return gemm_t<BM, A4, EPI, DT, 0, kNarrowBN>(s, g, splits, id);
-        case 1: return gemm_t<BM, A4, EPI, DT, 1, kNarrowBN>(s, g, splits, id);
-        case 2: return gemm_t<BM, A4, EPI, DT, 2, kNarrowBN>(s, g, splits, id);
-        case 3: return gemm_t<BM, A4, EPI, DT, 3, kNarrowBN>(s, g, splits, id);
-        case 4: return gemm_t<BM, A4, EPI, DT, 4, kNarrowBN>(s, g, splits, id);
-        case 5: return gemm_t<BM, A4, EPI, DT, 5, kNarrowBN>(s, g, splits, id);
-        case 6: return gemm_t<BM, A4, EPI, DT, 6, kNarrowBN>(s, g, splits, id);
+        case 0: return gemm_t<BM, A4, EPI, DT, 0, kNarrowBN, false, 0, TRA>(s, g, splits, id);
+        case 1: return gemm_t<BM, A4, EPI, DT, 1, kNarrowBN, false, 0, TRA>(s, g, splits, id);
+        case 2: return gemm_t<BM, A4, EPI, DT, 2, kNarrowBN, false, 0, TRA>(s, g, splits, id);
+        case 3: return gemm_t<BM, A4, EPI, DT, 3, kNarrowBN, false, 0, TRA>(s, g, splits, id);
+        case 4: return gemm_t<BM, A4, EPI, DT, 4, kNarrowBN, false, 0, TRA>(s, g, splits, id);
+        case 5: return gemm_t<BM, A4, EPI, DT, 5, kNarrowBN, false, 0, TRA>(s, g, splits, id);
+        case 6: return gemm_t<BM, A4, EPI, DT, 6, kNarrowBN, false, 0, TRA>(s, g, splits, id);
       }
       return hipErrorInvalidValue;
     }
     switch (g.log2b) {
-      case 0: return gemm_t<BM, A4, EPI, DT, 0>(s, g, splits, id);
-      case 1: return gemm_t<BM, A4, EPI, DT, 1>(s, g, splits, id);
-      case 2: return gemm_t<BM, A4, EPI, DT, 2>(s, g, splits, id);
-      case 3: return gemm_t<BM, A4, EPI, DT, 3>(s, g, splits, id);
-      case 4: return gemm_t<BM, A4, EPI, DT, 4>(s, g, splits, id);
-      case 5: return gemm_t<BM, A4, EPI, DT, 5>(s, g, splits, id);
-      case 6: return gemm_t<BM, A4, EPI, DT, 6>(s, g, splits, id);
-      case 7: return gemm_t<BM, A4, EPI, DT, 7>(s, g, splits, id);
+      case 0: return gemm_t<BM, A4, EPI, DT, 0, kBN, false, 0, TRA>(s, g, splits, id);
+      case 1: return gemm_t<BM, A4, EPI, DT, 1, kBN, false, 0, TRA>(s, g, splits, id);
+      case 2: return gemm_t<BM, A4, EPI, DT, 2, kBN, false, 0, TRA>(s, g, splits, id);
+      case 3: return gemm_t<BM, A4, EPI, DT, 3, kBN, false, 0, TRA>(s, g, splits, id);
+      case 4: return gemm_t<BM, A4, EPI, DT, 4, kBN, false, 0, TRA>(s, g, splits, id);
+      case 5: return gemm_t<BM, A4, EPI, DT, 5, kBN, false, 0, TRA>(s, g, splits, id);
+      case 6: return gemm_t<BM, A4, EPI, DT, 6, kBN, false, 0, TRA>(s, g, splits, id);
+      case 7: return gemm_t<BM, A4, EPI, DT, 7, kBN, false, 0, TRA>(s, g, splits, id);
     }
     return hipErrorInvalidValue;
   } else {
-    if (fwd_bn(g.M, g.N, splits, g.batch) == kMidBN) return gemm_t<BM, A4, EPI, DT, 0, kMidBN>(s, g, splits, id);
-    return gemm_t<BM, A4, EPI, DT, 0>(s, g, splits, id);
+    if (fwd_bn(g.M, g.N, splits, g.batch) == kMidBN) return gemm_t<BM, A4, EPI, DT, 0, kMidBN, false, 0, TRA>(s, g, splits, id);
+    return gemm_t<BM, A4, EPI, DT, 0, kBN, false, 0, TRA>(s, g, splits, id);
   }
 }
 
@@ -265,25 +265,26 @@ hipError_t reduce_t(hipStream_t s, const int32_t* P, int S, const GemmArgs& g) {
   return hipGetLastError();
 }
 
-template <bool A4, int EPI, int DT>
+// TRA: A stored k-major (GemmArgs::a_kmajor)
+template <bool A4, int EPI, int DT, bool TRA = false>
 hipError_t run(hipStream_t s, const GemmArgs& g, int splits, int32_t* partial, int id) {
   constexpr int BM = tile_m<A4>();
-  if (splits <= 1) return gemm_b<BM, A4, EPI, DT>(s, g, 1, id);
+  if (splits <= 1) return gemm_b<BM, A4, EPI, DT, TRA>(s, g, 1, id);
   GemmArgs p = g;
   p.out = partial;
   p.ldo = g.N;
-  hipError_t e = split_mid(A4, g.N) ? gemm_t<BM, A4, kEpiPartial, DT, 0, kMidBN>(s, p, splits, id)
-                                     : gemm_t<BM, A4, kEpiPartial, DT, 0>(s, p, splits, id);
+  hipError_t e = split_mid(A4, g.N) ? gemm_t<BM, A4, kEpiPartial, DT, 0, kMidBN, false, 0, TRA>(s, p, splits, id)
+                                     : gemm_t<BM, A4, kEpiPartial, DT, 0, kBN, false, 0, TRA>(s, p, splits, id);
   if (e != hipSuccess) return e;
   return reduce_t<DT, EPI>(s, partial, splits, g);
 }
 
-template <bool A4, int EPI>
+template <bool A4, int EPI, bool TRA = false>
 hipError_t run_dt(hipStream_t s, int dt, const GemmArgs& g, int splits, int32_t* partial, int id) {
   switch (dt) {
-    case kF32: return run<A4, EPI, kF32>(s, g, splits, partial, id);
-    case kF16: return run<A4, EPI, kF16>(s, g, splits, partial, id);
-    case kBF16: return run<A4, EPI, kBF16>(s, g, splits, partial, id);
+    case kF32: return run<A4, EPI, kF32, TRA>(s, g, splits, partial, id);
+    case kF16: return run<A4, EPI, kF16, TRA>(s, g, splits, partial, id);
+    case kBF16: return run<A4, EPI, kBF16, TRA>(s, g, splits, partial, id);
   }
   return hipErrorInvalidValue;
 }
@@ -351,6 +352,9 @@ hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4,
   if (a_int4) {
     if (epi == kEpiFwd) return run_dt<true, kEpiFwd>(s, dt, g, splits, partial, kKGemmFwd);
     if (epi == kEpiAcc) return run<true, kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
+  } else if (g.a_kmajor) {
+    if (epi == kEpiDw) return run_dt<false, kEpiDw, true>(s, dt, g, splits, partial, kKGemmDw);
+    if (epi == kEpiAcc) return run<false, kEpiAcc, kF32, true>(s, g, splits, partial, kKGemmAcc);
   } else {
     if (epi == kEpiDx) return run_dt<false, kEpiDx>(s, dt, g, splits, partial, kKGemmDx);
     if (epi == kEpiDw) return run_dt<false, kEpiDw>(s, dt, g, splits, partial, kKGemmDw);

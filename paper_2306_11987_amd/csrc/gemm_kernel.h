@@ -14,6 +14,7 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -66,6 +67,10 @@ struct Cfg {
   static constexpr int SHIFT = F6 ? 0 : (A4 ? 4 : 0) + 4;
   static_assert(A_BYTES % (1024 * WAVES) == 0 && B_BYTES % (1024 * WAVES) == 0, "DMA split");
 };
+
+// Position p of a group of 8 int8 k in the K-interleaved order holds k = nu8(p):
+// 0,2,4,6,1,3,5,7 (the order in which a packed INT4 word widens, see widen()).
+__device__ __forceinline__ constexpr int nu8(int p) { return ((p & 3) << 1) | (p >> 2); }
 
 // 16-byte chunk of row r that holds data chunk c (XOR swizzle; see the file comment).
 template <int RB>
@@ -227,7 +232,15 @@ __device__ __forceinline__ double block_sum_f64(double v, double* red) {
 // F6K (FP6 route): 0 the plain product (forward), kF6Dx the dX product (two K passes for tiles
 // holding upper tokens, row weights), kF6Dw the dW product (weight classes along K)
 constexpr int kF6Dx = 1, kF6Dw = 2;
-template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B, int BN_, bool F6 = false, int F6K = 0>
+// TRA (int8 x INT4 only): A is stored k-major, A[k][m] with pitch lda and its m positions
+// K-interleaved in groups of 8 (the dX operand A_T read as the dW operand A_T^T).  A stage
+// of it lands in LDS as 128 k rows of BM m bytes, and the gfx950 transposing read
+// ds_read_b64_tr_b8 forms the k-contiguous MFMA fragments out of it: in each group of 16
+// lanes, byte b of lane j comes from byte j % 8 of the 8 bytes addressed by lane
+// 2 b + j / 8.  Output row m' of the tile is then the interleaved position, i.e. row
+// (m' & ~7) | nu8(m' & 7) of the result.  K must be whole stages.
+template <int BM, bool A4, int WN, int EPI, int DT, int LOG2B, int BN_, bool F6 = false, int F6K = 0,
+          bool TRA = false>
 __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, WN, BN_, F6>::OCC)) void gemm_kernel(GemmArgs g) {
   using C_ = Cfg<BM, A4, WN, BN_, F6>;
   constexpr int TI = C_::TI, TJ = C_::TJ, BN = C_::BN;
@@ -242,6 +255,8 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
                          : (BM / 4 * E_PITCH <= C_::LDS_MAIN) ? BM / 4 : BM / 8;
   static_assert(E_ROWS >= 32 && E_ROWS * E_PITCH <= C_::LDS_MAIN, "epilogue staging");
   static_assert(!(F6 && LSQ), "the learned-step epilogues run on the int8 route");
+  static_assert(!TRA || (!A4 && !F6 && !LSQ && !ROWMAP && C_::RA == 128 && C_::KS == 128),
+                "k-major A: int8 A, 128-byte rows of 128 k per stage, plain output rows");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[C_::LDS_MAIN];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -316,6 +331,14 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
 #pragma unroll
   for (int x = 0; x < C_::A_BPW; ++x) {
     const int r = (wid * C_::A_BPW + x) * (1024 / C_::RA) + lane / C_::CPA;
+    if constexpr (TRA) {  // r: k row of the stage; chunks past M re-read the last 16 m
+      const int c = (lane % C_::CPA) ^ (r & 7);
+      int64_t col = m0 + c * 16;
+      col = col + 16 <= M ? col : M - 16;
+      ca[x] = c * 16;
+      pa[x] = static_cast<const uint8_t*>(g.A) + ((int64_t)st0 * C_::KS + r) * g.lda + col;
+      continue;
+    }
     const int c = (lane % C_::CPA) ^ swz<C_::RA>(r);
     int64_t gm = m0 + r;
     gm = gm < M ? gm : M - 1;
@@ -368,6 +391,15 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
       }
       return;
     }
+    if constexpr (TRA) {  // whole stages (K a multiple of 128): A advances by 128 rows
+#pragma unroll
+      for (int x = 0; x < C_::A_BPW; ++x)
+        dma16(pa[x] + (int64_t)st * C_::KS * g.lda, sa + (wid * C_::A_BPW + x) * 1024);
+#pragma unroll
+      for (int x = 0; x < C_::B_BPW; ++x)
+        dma16(pb[x] + (int64_t)st * C_::RB, sb + (wid * C_::B_BPW + x) * 1024);
+      return;
+    }
     const int64_t ka = (int64_t)(st0 + st) * C_::RA, kb = (int64_t)(st0 + st) * C_::RB;
     if (ka + C_::RA <= Ka && kb + C_::RB <= Kb) {  // whole stage inside K: straight line
 #pragma unroll
@@ -417,6 +449,14 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     const int r = wm * C_::WM + 32 * i + frow;
     offa[i] = r * C_::RA;
     sza[i] = swz<C_::RA>(r);
+    if constexpr (TRA) {
+      // lane j of 16-lane group q (m half q % 2, k half fg = q / 2) supplies the 8 bytes
+      // of k row 32 fg + nu8(j / 2) (+ the step's offset) at m bytes 16 (q % 2) + 8 (j % 2)
+      // of the fragment's 32; that row's chunks are swizzled by its k % 8 = nu8(j / 2)
+      const int j = lane & 15, q = lane >> 4, kr = nu8(j >> 1);
+      const int chunk = (wm * C_::WM + 32 * i) / 16 + (q & 1);
+      offa[i] = (32 * (q >> 1) + kr) * C_::RA + ((chunk ^ kr) << 4) + 8 * (j & 1);
+    }
   }
 #pragma unroll
   for (int j = 0; j < TJ; ++j) {
@@ -446,6 +486,16 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     for (int h = 0; h < RA_PAIR; ++h)
 #pragma unroll
       for (int i = 0; i < TI; ++i) {
+        if constexpr (TRA) {
+          // k step 2 pp + h: bytes 0-7 of the fragment from k rows 64 pp + 16 h + 0..7 (+ 32 fg),
+          // bytes 8-15 from the next 8 rows
+          typedef __attribute__((address_space(3))) v2i lds_v2i;
+          const uint8_t* p = sa + offa[i] + (64 * pp + 16 * h) * C_::RA;
+          const v2i lo = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(lds_void*)p);
+          const v2i hi = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(lds_void*)(p + 8 * C_::RA));
+          ra[slot][h][i] = make_uint4((uint32_t)lo[0], (uint32_t)lo[1], (uint32_t)hi[0], (uint32_t)hi[1]);
+          continue;
+        }
         const int c = A4 ? 2 * pp + fg : 4 * pp + 2 * fg + h;
         ra[slot][h][i] = *reinterpret_cast<const uint4*>(sa + offa[i] + ((c ^ sza[i]) << 4));
       }
@@ -468,7 +518,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     for (int q = 0; q < TI * TJ; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
       __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // up to 5 VALU
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // up to 1 LDS read
+      __builtin_amdgcn_sched_group_barrier(0x100, TRA ? 2 : 1, 0);  // LDS reads
     }
   };
 #ifndef HQLSS_LSQ_PREFETCH
@@ -833,7 +883,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
       const int r = idx / PIECES, pc = idx % PIECES;
       const int64_t gm = m0 + r_lo + r;
       val[it] = *reinterpret_cast<const uint4*>(smem + r * E_PITCH + pc * 16);
-      orow[it] = gm < M ? (ROWMAP ? g.out_rows[gm] : (int)gm) : -1;
+      orow[it] = gm < M ? (ROWMAP ? g.out_rows[gm] : TRA ? (int)((gm & ~7) | nu8((int)(gm & 7))) : (int)gm) : -1;
     }
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {
@@ -862,7 +912,8 @@ template <bool A4, int LOG2B> constexpr int wave_n() { return (A4 || LOG2B >= 6)
 // chunk) item per wave at a time)
 // BN_: workgroup tile width; kNarrowBN for outputs at most that wide (attention head
 // dimensions), which would otherwise leave most of a 256-wide tile idle
-template <int BM, bool A4, int EPI, int DT, int LOG2B, int BN_ = kBN, bool F6 = false, int F6K = 0>
+template <int BM, bool A4, int EPI, int DT, int LOG2B, int BN_ = kBN, bool F6 = false, int F6K = 0,
+          bool TRA = false>
 hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   // 128-wide INT4 x INT4 tiles: 64 x 64 wave tiles (one widened fragment per MFMA)
   constexpr int WN = (A4 && BN_ == kMidBN) ? 64 : wave_n<A4, LOG2B>() < BN_ ? wave_n<A4, LOG2B>() : BN_;
@@ -871,7 +922,8 @@ hipError_t gemm_t(hipStream_t s, const GemmArgs& g, int splits, int id) {
   dim3 grid((unsigned)(((g.N + BN_ - 1) / BN_) * ((g.M + BM - 1) / BM)), 1u,
             (unsigned)(g.batch > 0 ? g.batch : splits));
   timing_begin(s);
-  gemm_kernel<BM, A4, WN, EPI, DT, LOG2B, BN_, F6, F6K><<<grid, C_::THREADS, 0, s>>>(g);
+  if (TRA && (g.K % kKS != 0 || g.M % 16 != 0)) return hipErrorInvalidValue;  // whole stages, 16 m
+  gemm_kernel<BM, A4, WN, EPI, DT, LOG2B, BN_, F6, F6K, TRA><<<grid, C_::THREADS, 0, s>>>(g);
   timing_end(s, id);
   return hipGetLastError();
 }

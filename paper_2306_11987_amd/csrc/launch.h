@@ -152,6 +152,10 @@ struct GemmArgs {
   const uint8_t* w_up;
   const uint8_t* w_dn;
   const int32_t* kcls;
+  // int8 x INT4 kEpiDw / kEpiAcc only: A is stored k-major (A[k][m], pitch lda, m positions
+  // K-interleaved in groups of 8: the dX operand A_T serves as the dW operand), K whole
+  // stages of 128 and M a multiple of 16
+  int a_kmajor;
 };
 // Split-K factor the launcher uses for this shape (1 = no split), and the int32 partial
 // buffer it then needs (splits x M x N words).  A non-zero override forces the factor.
