@@ -163,7 +163,7 @@ size_t dx_bytes(int64_t N, int64_t D, int64_t C) {
 size_t dw_bytes(int64_t N, int64_t D, int64_t C) {
   return al(C * rup(N, kPad)) + al(D * rup(N, kPad) / 2) + dw_gemm_partial(N, D, C);
 }
-// dynamic-scale gradients (do_grads without lsq): dX and dW share the int8 operand A_T
+// dX and dW together: the two products share the int8 operand A_T
 size_t grads_bytes(int64_t N, int64_t D, int64_t C, bool dx, bool dw) {
   if (dx && dw) return dx_bytes(N, D, C) + al(D * rup(N, kPad) / 2) + dw_gemm_partial(N, D, C);
   return (dx ? dx_bytes(N, D, C) : 0) + (dw ? dw_bytes(N, D, C) : 0);
@@ -404,8 +404,9 @@ size_t bmm_bwd_bytes(int64_t B, int64_t N, int64_t M, int64_t P, bool dq, bool d
   size_t t = 2 * al(B * N * P / 2) + 2 * al(4 * B * N) + 2 * al(B * N) + al(4 * B * N) +
              al(4 * B) * 2;
   t += al(4 * d.parts) + al(4 * B * 2 * score_pitch(N)) + al(16 * d.parts);
-  if (dq) t += al(B * d.kp * P) + al(8 * B * d.tiles_dx);
-  if (dk) t += al(B * P * d.kp) + al(B * M * d.kp / 2) + al(8 * B * d.tiles_dw);
+  if (dq || dk) t += al(B * d.kp * P);  // A_T, read by both gradient products
+  if (dq) t += al(8 * B * d.tiles_dx);
+  if (dk) t += al(B * M * d.kp / 2) + al(8 * B * d.tiles_dw);
   return t;
 }
 
@@ -428,9 +429,8 @@ hqlss_status do_bmm_bwd(const void* dT, const hqlss_saved_t* sv, const hqlss_bmm
   float* pg = w.take<float>(4 * d.parts);
   uint32_t* scores = w.take<uint32_t>(4 * B * 2 * pitch);
   uint4* bparts = w.take<uint4>(16 * d.parts);
-  int8_t* Ag = dQ ? w.take<int8_t>(B * d.kp * P) : nullptr;
+  int8_t* Ag = w.take<int8_t>(B * d.kp * P);
   double* px = dQ ? w.take<double>(8 * B * d.tiles_dx) : nullptr;
-  int8_t* At = dK ? w.take<int8_t>(B * P * d.kp) : nullptr;
   uint8_t* XtT = dK ? w.take<uint8_t>(B * M * d.kp / 2) : nullptr;
   double* pw = dK ? w.take<double>(8 * B * d.tiles_dw) : nullptr;
   if (!w.ok()) return HQLSS_ERR_WORKSPACE;
@@ -443,8 +443,8 @@ hqlss_status do_bmm_bwd(const void* dT, const hqlss_saved_t* sv, const hqlss_bmm
   HQ_TRY(launch_bit_split(s, dt, jg, pg, nparts, o, seed, offset));
   HQ_TRY(launch_lss_plan(s, su, scores, pitch, bparts, jg.wg, N, budget, seed, offset, wu, wd,
                          kept, nk, B, ostride));
-  HQ_TRY(launch_build_operands(s, dt, qup, qdn, wu, wd, kept, nk, sv->xq, N, P, M, Ag, At, XtT,
-                               dQ, B));
+  HQ_TRY(launch_build_operands(s, dt, qup, qdn, wu, wd, kept, nk, sv->xq, N, P, M, Ag, XtT, dQ,
+                               B));
   const uint32_t* agb = reinterpret_cast<const uint32_t*>(ag);
   const float denom = (float)(kBsRatio * (int64_t(1) << k));
   if (dQ) {  // grad Q_b = s_K[b] (I_Q o grad T_b K^_b) H^T on the kept rows
@@ -463,7 +463,7 @@ hqlss_status do_bmm_bwd(const void* dT, const hqlss_saved_t* sv, const hqlss_bmm
   }
   if (dK) {  // grad K_b = s_Q[b] (I_K o grad T_b^T Q^_b) H^T over the kept tokens
     GemmArgs g{};
-    g.A = At; g.lda = d.kp;
+    g.A = Ag; g.lda = P; g.a_kmajor = 1;
     g.B = XtT; g.ldb = d.kp / 2;
     g.M = P; g.N = M; g.K = d.kp; g.k_dev = nk;
     g.amax1 = agb; g.amax2 = reinterpret_cast<const uint32_t*>(l->step_q);
@@ -471,7 +471,7 @@ hqlss_status do_bmm_bwd(const void* dT, const hqlss_saved_t* sv, const hqlss_bmm
     g.out = dK; g.ldo = M;
     g.delta = l->delta_k; g.ds_part = pw;
     g.batch = (int)B;
-    g.bs_a = P * d.kp; g.bs_b = M * d.kp / 2; g.bs_out = P * M; g.bs_delta = P * M;
+    g.bs_a = d.kp * P; g.bs_b = M * d.kp / 2; g.bs_out = P * M; g.bs_delta = P * M;
     HQ_TRY(launch_gemm(s, kEpiDwL, dt, false, true, g, 1, nullptr));
   }
   const bool sq = dQ && dstep_q, sk = dK && dstep_k;
@@ -517,20 +517,17 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   const bool want_dx = dX || (acc && which_acc == 1);
   const bool want_dw = dW || (acc && which_acc == 2);
   const int64_t Kp = rup(N, kPad);
-  // The dynamic-scale dW product reads the dX operand A_T itself, k-major (its kept rows
-  // are the K of dW), through transposing LDS reads; the learned-step one reads A_T^T.
-  const bool dw_kmajor = lsq == nullptr;
+  // The dW product reads the dX operand A_T itself, k-major (its kept rows are the K of
+  // dW), through transposing LDS reads.
   int8_t* Ag = nullptr;
   int32_t* part_dx = nullptr;
   const int sp_dx = gemm_splits(N, D, C, false, true);
-  if (want_dx || (want_dw && dw_kmajor)) Ag = w.take<int8_t>(Kp * C);
+  if (want_dx || want_dw) Ag = w.take<int8_t>(Kp * C);
   if (want_dx) part_dx = w.take<int32_t>(gemm_partial_bytes(N, D, sp_dx));
-  int8_t* At = nullptr;
   uint8_t* XtT = nullptr;
   int32_t* part_dw = nullptr;
   const int sp_dw = gemm_splits(C, D, Kp, false, true);
   if (want_dw) {
-    if (!dw_kmajor) At = w.take<int8_t>(C * Kp);
     XtT = w.take<uint8_t>(D * Kp / 2);
     part_dw = w.take<int32_t>(gemm_partial_bytes(C, D, sp_dw));
   }
@@ -538,7 +535,7 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   double* pw = (lsq && dW) ? w.take<double>(8 * lsq_parts_dw(N, D, C)) : nullptr;
   if (!w.ok()) return HQLSS_ERR_WORKSPACE;
   HQ_TRY(launch_build_operands(s, dt, p->qup, p->qdn, p->w_up, p->w_dn, p->kept, p->n_kept, sv->xq,
-                               N, C, D, Ag, At, XtT, dX));
+                               N, C, D, Ag, XtT, dX));
   if (want_dx) {
     GemmArgs g{};
     g.A = Ag; g.lda = C;
@@ -559,11 +556,7 @@ hqlss_status do_grads(const lss_plan_t* p, const hqlss_saved_t* sv, void* dX, vo
   }
   if (want_dw) {
     GemmArgs g{};
-    if (dw_kmajor) {
-      g.A = Ag; g.lda = C; g.a_kmajor = 1;
-    } else {
-      g.A = At; g.lda = Kp;
-    }
+    g.A = Ag; g.lda = C; g.a_kmajor = 1;
     g.B = XtT; g.ldb = Kp / 2;
     g.M = C; g.N = D; g.K = Kp; g.k_dev = p->n_kept;
     g.amax1 = ag; g.amax2 = amax; g.denom = denom; g.log2b = k;
@@ -731,7 +724,7 @@ size_t hqlss_workspace_bytes(int which, int64_t N, int64_t D, int64_t C) {
              dw6_bytes(N, D, C);
     case HQLSS_WS_FROM_PLAN_FP6: return plan6_bytes(N) + dx6_bytes(N, D, C) + dw6_bytes(N, D, C);
     case HQLSS_WS_BWD_LSQ:
-      return plan_bytes(N, C) + plan_scratch_bytes(N) + dx_bytes(N, D, C) + dw_bytes(N, D, C) +
+      return plan_bytes(N, C) + plan_scratch_bytes(N) + grads_bytes(N, D, C, true, true) +
              lsq_parts_bytes(N, D, C, true, true);
   }
   return 0;
@@ -1016,8 +1009,8 @@ hqlss_status lss_linear_bwd_lsq(const void* dY, const hqlss_saved_t* saved,
   if ((st = check_lsq(lsq, dX != nullptr, dW != nullptr))) return st;
   if ((dX && !a16(dX)) || (dW && !a16(dW)) || (ws && !a16(ws)) || (dstep && !a4(dstep)))
     return HQLSS_ERR_ALIGN;
-  const size_t need = plan_bytes(N, C) + plan_scratch_bytes(N) + (dX ? dx_bytes(N, D, C) : 0) +
-                      (dW ? dw_bytes(N, D, C) : 0) + lsq_parts_bytes(N, D, C, dX, dW);
+  const size_t need = plan_bytes(N, C) + plan_scratch_bytes(N) + grads_bytes(N, D, C, dX != nullptr, dW != nullptr) +
+                      lsq_parts_bytes(N, D, C, dX, dW);
   if (!ws || ws_bytes < need) return HQLSS_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Carve w{static_cast<char*>(ws), 0, ws_bytes};

@@ -7,7 +7,9 @@
 //   dW       acc = A_T^T X^_T             (Sec. 4.2, Eq. 5 on the kept rows), then
 //            dW = alpha FWHT_b(acc)
 //
-// All three are "NT" products acc[m][n] = sum_k A[m][k] B[n][k] with K-contiguous rows.
+// All three are "NT" products acc[m][n] = sum_k A[m][k] B[n][k] with K-contiguous rows,
+// except the A operand of dW: that is A_T itself, stored k-major as the dX product reads
+// it, and transposed on its way out of LDS by ds_read_b64_tr_b8 (see gemm_kernel.h).
 // CDNA4 has no INT4 matrix instruction, so INT4 codes run on the int8 MFMA
 // (v_mfma_i32_32x32x32_i8, int32 accumulation).  INT4 operands stay packed in HBM and in
 // LDS and are widened right after the LDS read with two masks per 32-bit word:
@@ -354,6 +356,7 @@ hipError_t launch_gemm(hipStream_t s, int epi, int dt, bool a_int4, bool b_int4,
     if (epi == kEpiAcc) return run<true, kEpiAcc, kF32>(s, g, splits, partial, kKGemmAcc);
   } else if (g.a_kmajor) {
     if (epi == kEpiDw) return run_dt<false, kEpiDw, true>(s, dt, g, splits, partial, kKGemmDw);
+    if (epi == kEpiDwL) return run_dt<false, kEpiDwL, true>(s, dt, g, splits, partial, kKGemmDw);
     if (epi == kEpiAcc) return run<false, kEpiAcc, kF32, true>(s, g, splits, partial, kKGemmAcc);
   } else {
     if (epi == kEpiDx) return run_dt<false, kEpiDx>(s, dt, g, splits, partial, kKGemmDx);

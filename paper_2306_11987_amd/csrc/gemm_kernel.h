@@ -255,8 +255,10 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
                          : (BM / 4 * E_PITCH <= C_::LDS_MAIN) ? BM / 4 : BM / 8;
   static_assert(E_ROWS >= 32 && E_ROWS * E_PITCH <= C_::LDS_MAIN, "epilogue staging");
   static_assert(!(F6 && LSQ), "the learned-step epilogues run on the int8 route");
-  static_assert(!TRA || (!A4 && !F6 && !LSQ && !ROWMAP && C_::RA == 128 && C_::KS == 128),
+  static_assert(!TRA || (!A4 && !F6 && !ROWMAP && C_::RA == 128 && C_::KS == 128),
                 "k-major A: int8 A, 128-byte rows of 128 k per stage, plain output rows");
+  // result row of tile row gm (k-major A: the K-interleaved position gm)
+  auto res_row = [](int64_t gm) -> int64_t { return TRA ? ((gm & ~int64_t(7)) | nu8((int)(gm & 7))) : gm; };
   __shared__ __attribute__((aligned(1024))) uint8_t smem[C_::LDS_MAIN];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -537,7 +539,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     for (int x = 0; x < 2; ++x) {
       int64_t gm = m0 + (wid * 2 + x) * 16 + (lane >> 2);
       gm = gm < M ? gm : M - 1;
-      pf_row[x] = ROWMAP ? g.out_rows[gm] : (int)gm;
+      pf_row[x] = ROWMAP ? g.out_rows[gm] : (int)res_row(gm);
     }
   }
   auto prefetch_delta = [&]() {
@@ -795,7 +797,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     for (int i = 0; i < TI; ++i) {
       const int64_t gm = m0 + wm * C_::WM + 32 * i + ml;
       if (gm >= M) continue;
-      const int64_t drow = ROWMAP ? (int64_t)g.out_rows[gm] : gm;
+      const int64_t drow = ROWMAP ? (int64_t)g.out_rows[gm] : res_row(gm);
       const uint16_t* dp = g.delta + drow * g.ldo + n0 + wn * C_::WN + nh;
 #pragma unroll
       for (int j = 0; j < TJ; ++j) {
@@ -883,7 +885,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
       const int r = idx / PIECES, pc = idx % PIECES;
       const int64_t gm = m0 + r_lo + r;
       val[it] = *reinterpret_cast<const uint4*>(smem + r * E_PITCH + pc * 16);
-      orow[it] = gm < M ? (ROWMAP ? g.out_rows[gm] : TRA ? (int)((gm & ~7) | nu8((int)(gm & 7))) : (int)gm) : -1;
+      orow[it] = gm < M ? (ROWMAP ? g.out_rows[gm] : (int)res_row(gm)) : -1;
     }
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {

@@ -103,15 +103,14 @@ hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_
                            int64_t budget, uint64_t seed, uint64_t offset, uint8_t* w_up,
                            uint8_t* w_dn, int32_t* kept, int32_t* n_kept, int64_t batch = 1,
                            uint64_t offset_stride = 0);
-// GEMM operands of the kept tokens in one pass (any of Ag, At, XtT, dX may be null):
+// GEMM operands of the kept tokens in one pass (any of Ag, XtT, dX may be null):
 // Ag [round_up(N,128)][C] weighted rows (int8, K-interleaved; rows < round_up(n_kept,128)
-// written), At [C][Kp] the same transposed and XtT [D][Kp/2] the gathered X^ rows
-// transposed (packed), Kp = round_up(N, 128); rows of dX (dtype dt) of dropped tokens are
-// zeroed.
+// written) and XtT [D][Kp/2] the gathered X^ rows transposed (packed),
+// Kp = round_up(N, 128); rows of dX (dtype dt) of dropped tokens are zeroed.
 hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
                                  const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
                                  const int32_t* n_kept, const uint8_t* xq, int64_t N, int64_t C,
-                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX,
+                                 int64_t D, int8_t* Ag, uint8_t* XtT, void* dX,
                                  int64_t batch = 1);
 
 // Integer GEMM  acc[m][n] = sum_k A[m][k] B[n][k]  (both operands K-contiguous rows).
@@ -152,7 +151,7 @@ struct GemmArgs {
   const uint8_t* w_up;
   const uint8_t* w_dn;
   const int32_t* kcls;
-  // int8 x INT4 kEpiDw / kEpiAcc only: A is stored k-major (A[k][m], pitch lda, m positions
+  // int8 x INT4 kEpiDw / kEpiDwL / kEpiAcc only: A is stored k-major (A[k][m], pitch lda, m positions
   // K-interleaved in groups of 8: the dX operand A_T serves as the dW operand), K whole
   // stages of 128 and M a multiple of 16
   int a_kmajor;

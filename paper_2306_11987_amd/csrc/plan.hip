@@ -21,10 +21,11 @@
 //
 // build_operands materialises, for the kept tokens only, the weighted integer
 // rows A_t = 14 w_up q_up[t] + w_dn q_dn[t] (|A| <= 126, one int8 operand that carries the
-// bit split and the 1/p factors together) and the gathered X^ rows, in the K-contiguous
-// layouts the MFMA GEMM reads.  int8 operands use the "K-interleaved" byte order of the
-// GEMM: inside every group of 8 consecutive k the bytes hold k = 0,2,4,6,1,3,5,7, the
-// order in which a packed INT4 word unpacks for free.
+// bit split and the 1/p factors together; the dX GEMM reads it K-contiguous, the dW GEMM
+// k-major through transposing LDS reads) and the gathered X^ rows, transposed to the
+// K-contiguous layout the dW GEMM reads.  The int8 operand uses the "K-interleaved" byte
+// order of the GEMM: inside every group of 8 consecutive k the bytes hold
+// k = 0,2,4,6,1,3,5,7, the order in which a packed INT4 word unpacks for free.
 #include "common.h"
 #include "launch.h"
 
@@ -303,12 +304,12 @@ __device__ __forceinline__ void weighted8(uint32_t up, uint32_t dn, int wu, int 
 // One pass over the kept tokens builds every GEMM operand the sample selects: workgroup
 // (x, y) takes kept indices [128 x, 128 x + 128) and one block of up to 128 columns (the
 // last block of C or D may hold 64).  Blocks of the C columns read q_up, q_dn and the
-// weights, form A_t and write it row-major into Ag (the dX operand) and, through an LDS
-// transpose, column-major into At (the dW operand); blocks of the D columns gather X^ rows
-// into XtT.  Every row piece written is 128 bytes (64 for XtT), two full cache lines.
-// The last block row zeroes the rows of dX that belong to dropped tokens.  Rows of Ag and
-// columns of At / XtT between n_kept and the next multiple of 128 are written as zeros
-// (the GEMMs read whole K steps).
+// weights, form A_t and write it row-major into Ag (the operand of both gradient GEMMs);
+// blocks of the D columns gather X^ rows and write them, through an LDS transpose,
+// column-major into XtT.  Every row piece written is 128 bytes (64 for XtT), two full
+// cache lines.  The last block row zeroes the rows of dX that belong to dropped tokens.
+// Rows of Ag and columns of XtT between n_kept and the next multiple of 128 are written as
+// zeros (the GEMMs read whole K steps).
 constexpr int kBK = 128;  // kept indices per workgroup
 constexpr int kBC = 128;  // columns per workgroup
 template <int DT>
@@ -317,7 +318,7 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
     const uint8_t* __restrict__ w_up, const uint8_t* __restrict__ w_dn,
     const int32_t* __restrict__ kept, const int32_t* __restrict__ n_kept,
     const uint8_t* __restrict__ xq, int64_t N, int64_t C, int64_t D, int8_t* __restrict__ Ag,
-    int8_t* __restrict__ At, uint8_t* __restrict__ XtT, void* __restrict__ dX) {
+    uint8_t* __restrict__ XtT, void* __restrict__ dX) {
   __shared__ __attribute__((aligned(16))) int8_t tile[kBK][kBC + 4];  // [kept index][column]
   const int tid = threadIdx.x;
   const int64_t cb = (C + kBC - 1) / kBC, db = (D + kBC - 1) / kBC;
@@ -331,7 +332,6 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
     n_kept += bt;
     xq += bt * N * (D / 2);
     if (Ag) Ag += bt * kpad * C;
-    if (At) At += bt * C * kpad;
     if (XtT) XtT += bt * D * (kpad / 2);
     if (dX) dX = static_cast<char*>(dX) + bt * N * D * Elem<DT>::bytes;
   }
@@ -351,9 +351,9 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
   const int64_t kp = (nk + 127) / 128 * 128;
   const int64_t i0 = (int64_t)blockIdx.x * kBK;
   if (i0 >= kp) return;
-  const int64_t pitch = (N + 127) / 128 * 128;  // K pitch of At (bytes) and 2x of XtT
+  const int64_t pitch = (N + 127) / 128 * 128;  // K pitch of XtT (in codes)
   const bool isA = (int64_t)blockIdx.y < cb;
-  if (isA ? (!Ag && !At) : !XtT) return;
+  if (isA ? !Ag : !XtT) return;
   const int64_t col0 = isA ? (int64_t)blockIdx.y * kBC : ((int64_t)blockIdx.y - cb) * kBC;
   const int64_t ncol = isA ? C : D;
   // 128 kept rows x 8 chunks of 16 columns, four per thread
@@ -382,9 +382,12 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
         }
       }
     }
-    if (isA && Ag && inside) {
-      const uint2 lo = interleave8(v), hi = interleave8(v + 8);
-      st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
+    if (isA) {
+      if (inside) {
+        const uint2 lo = interleave8(v), hi = interleave8(v + 8);
+        st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      }
+      continue;
     }
     // word w of row r sits at word w ^ ((r / 16) % 8) of the row: the transpose below reads
     // one column of 8 row blocks at once, which would otherwise fall on 4 banks
@@ -395,7 +398,7 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
       tp[(q / 4 + w) ^ sw] = ((uint32_t)v[4 * w] & 0xFFu) | (((uint32_t)v[4 * w + 1] & 0xFFu) << 8) |
                              (((uint32_t)v[4 * w + 2] & 0xFFu) << 16) | (((uint32_t)v[4 * w + 3] & 0xFFu) << 24);
   }
-  if (isA && !At) return;  // uniform: no transpose wanted
+  if (isA) return;  // uniform: A_t needs no transpose
   __syncthreads();
   // 128 columns x 8 chunks of 16 kept indices, four per thread
 #pragma unroll
@@ -403,23 +406,15 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
     const int item = tid + 256 * k, c = item >> 3, q = (item & 7) * 16;
     if (col0 + c >= ncol) continue;
     const int cs = (((c >> 2) ^ ((q >> 4) & 7)) << 2) | (c & 3);  // column c's byte in rows q..q+15
-    if (isA) {
-      int a[16];
+    uint32_t w0 = 0, w1 = 0;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) a[j] = tile[q + j][cs];
-      const uint2 lo = interleave8(a), hi = interleave8(a + 8);
-      st_stream<HQ_NT_B_ST>(At + (col0 + c) * pitch + i0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
-    } else {
-      uint32_t w0 = 0, w1 = 0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t byte = ((uint32_t)tile[q + 2 * j][cs] & 15u) |
-                              (((uint32_t)tile[q + 2 * j + 1][cs] & 15u) << 4);
-        if (j < 4) w0 |= byte << (8 * j);
-        else w1 |= byte << (8 * (j - 4));
-      }
-      st_stream2<HQ_NT_B_ST>(XtT + (col0 + c) * (pitch / 2) + (i0 + q) / 2, make_uint2(w0, w1));
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t byte = ((uint32_t)tile[q + 2 * j][cs] & 15u) |
+                            (((uint32_t)tile[q + 2 * j + 1][cs] & 15u) << 4);
+      if (j < 4) w0 |= byte << (8 * j);
+      else w1 |= byte << (8 * (j - 4));
     }
+    st_stream2<HQ_NT_B_ST>(XtT + (col0 + c) * (pitch / 2) + (i0 + q) / 2, make_uint2(w0, w1));
   }
 }
 
@@ -534,21 +529,20 @@ hipError_t launch_lss_plan(hipStream_t s, const int32_t* sumsq_up, const uint32_
 hipError_t launch_build_operands(hipStream_t s, int dt, const uint8_t* qup, const uint8_t* qdn,
                                  const uint8_t* w_up, const uint8_t* w_dn, const int32_t* kept,
                                  const int32_t* n_kept, const uint8_t* xq, int64_t N, int64_t C,
-                                 int64_t D, int8_t* Ag, int8_t* At, uint8_t* XtT, void* dX,
-                                 int64_t batch) {
+                                 int64_t D, int8_t* Ag, uint8_t* XtT, void* dX, int64_t batch) {
   const int64_t pitch = (N + 127) / 128 * 128;
   dim3 grid((unsigned)(pitch / kBK), (unsigned)((C + kBC - 1) / kBC + (D + kBC - 1) / kBC + 1),
             (unsigned)batch);
   timing_begin(s);
   switch (dt) {
     case kF32:
-      build_operands_kernel<kF32><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, At, XtT, dX);
+      build_operands_kernel<kF32><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, XtT, dX);
       break;
     case kF16:
-      build_operands_kernel<kF16><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, At, XtT, dX);
+      build_operands_kernel<kF16><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, XtT, dX);
       break;
     case kBF16:
-      build_operands_kernel<kBF16><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, At, XtT, dX);
+      build_operands_kernel<kBF16><<<grid, 256, 0, s>>>(qup, qdn, w_up, w_dn, kept, n_kept, xq, N, C, D, Ag, XtT, dX);
       break;
     default:
       return hipErrorInvalidValue;
