@@ -26,6 +26,17 @@ __device__ __forceinline__ float bf2f(uint32_t h) { return __uint_as_float(h << 
 __device__ __forceinline__ uint32_t f2h(float f) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
 }
+// Two values rounded to nearest-even and packed (the first in the low half), by the
+// packed conversions of gfx950 (v_cvt_pk_f16_f32 / v_cvt_pk_bf16_f32).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+template <int DT>
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  const f32x2 x = {a, b};
+  if constexpr (DT == kF16) return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, f16x2));
+  else return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
+}
 __device__ __forceinline__ uint32_t f2bf(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);  // inputs are finite
@@ -144,8 +155,7 @@ __device__ __forceinline__ void store_vec(void* p, const float* v) {
     uint32_t w[NV / 2];
 #pragma unroll
     for (int j = 0; j < NV / 2; ++j) {
-      if constexpr (DT == kF16) w[j] = f2h(v[2 * j]) | (f2h(v[2 * j + 1]) << 16);
-      else w[j] = f2bf(v[2 * j]) | (f2bf(v[2 * j + 1]) << 16);
+      w[j] = pack2<DT>(v[2 * j], v[2 * j + 1]);
     }
     if constexpr (NV == 8) {
       *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
@@ -168,8 +178,7 @@ __device__ __forceinline__ void store8_stream(void* p, const float* v) {
     uint32_t w[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      if constexpr (DT == kF16) w[j] = f2h(v[2 * j]) | (f2h(v[2 * j + 1]) << 16);
-      else w[j] = f2bf(v[2 * j]) | (f2bf(v[2 * j + 1]) << 16);
+      w[j] = pack2<DT>(v[2 * j], v[2 * j + 1]);
     }
     st_stream<NT>(p, make_uint4(w[0], w[1], w[2], w[3]));
   }

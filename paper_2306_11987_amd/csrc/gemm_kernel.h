@@ -121,12 +121,20 @@ __device__ __forceinline__ void fwht_lane(int* v, int lane) {
       }
   }
   if constexpr (b > NV) {
-    const bool upper = (lane & 32) != 0;
+    // v_permlane32_swap exchanges the upper half-wave of its first register with the lower
+    // half-wave of its second: after one swap of (v[e], v[e + 1]) every lane holds both
+    // partners of one butterfly (lanes 0-31 those of element e, lanes 32-63 those of
+    // e + 1), and a second swap returns the sum to the lower and the difference to the
+    // upper lanes
+    static_assert(NV % 2 == 0, "pairs of elements");
 #pragma unroll
-    for (int e = 0; e < NV; ++e) {
-      const int p = __shfl_xor(v[e], 32);
-      v[e] = upper ? (p - v[e]) : (v[e] + p);
+    for (int e = 0; e < NV; e += 2) {
+      const v2i s = __builtin_amdgcn_permlane32_swap(v[e], v[e + 1], false, false);
+      const v2i t = __builtin_amdgcn_permlane32_swap(s[0] + s[1], s[0] - s[1], false, false);
+      v[e] = t[0];
+      v[e + 1] = t[1];
     }
+    (void)lane;
   }
 }
 
