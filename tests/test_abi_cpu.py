@@ -47,6 +47,19 @@ def test_status_strings():
     assert H.status_string(99) == "unknown status"
 
 
+def test_backward_workspace_shares_the_int8_operand():
+    """dX and dW read one int8 operand A_T (dW reads it k-major): the combined backward needs
+    at least round_up(N, 128) x C bytes less than the two single-gradient calls together
+    (each of which also carries the sample's own buffers)."""
+    for N, D, C in ((128, 256, 256), (16384, 768, 3072), (16384, 4096, 11008), (300, 1024, 384)):
+        kp = (N + 127) // 128 * 128
+        dx = H.workspace_bytes(H.WS_BWD_DX, N, D, C)
+        dw = H.workspace_bytes(H.WS_BWD_DW, N, D, C)
+        both = H.workspace_bytes(H.WS_BWD, N, D, C)
+        assert max(dx, dw) <= both < dx + dw
+        assert dx + dw - both >= kp * C
+
+
 def test_workspace_sizes_monotone():
     for which in range(5):
         a = H.workspace_bytes(which, 128, 256, 256)

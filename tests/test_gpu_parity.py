@@ -72,10 +72,15 @@ def test_backward_parity(shape, budget_div):
     dW3 = torch.empty_like(dW)
     H.lss_linear_bwd_dx(tG, saved, dX3, k, budget, seed, offset, ws)
     H.lss_linear_bwd_dw(tG, saved, dW3, k, budget, seed, offset, ws)
+    # the single-gradient calls with workspaces of exactly their queried sizes
+    dX4 = torch.empty_like(dX)
+    dW4 = torch.empty_like(dW)
+    H.lss_linear_bwd_dx(tG, saved, dX4, k, budget, seed, offset, H.workspace(H.WS_BWD_DX, N, D, C))
+    H.lss_linear_bwd_dw(tG, saved, dW4, k, budget, seed, offset, H.workspace(H.WS_BWD_DW, N, D, C))
     torch.cuda.synchronize()
-    for t in (dX2, dX3):
+    for t in (dX2, dX3, dX4):
         assert torch.equal(t, dX)
-    for t in (dW2, dW3):
+    for t in (dW2, dW3, dW4):
         assert torch.equal(t, dW)
 
 
