@@ -377,6 +377,13 @@ void hqlss_debug_set_gemm_tile_n(int bn);
  * hook. */
 void hqlss_debug_set_fwd_fp6(int mode);
 
+/* Test hook: where lss_grad_plan leaves the integer leverage scores of its sample inside
+ * the workspace it was given (Sec. 4.2; see lss_grad_plan for their definition): the
+ * scores of the N upper rows start at the returned byte offset, those of the N lower rows
+ * `*pitch` uint32 entries later; they stay there until the workspace is reused.  Returns
+ * 0 and sets *pitch to 0 for N < 1. */
+size_t hqlss_debug_plan_scores_offset(int64_t N, int64_t *pitch);
+
 /* Benchmark hook: a plain device-to-device copy kernel ("copy") of `bytes` bytes (a
  * multiple of 16, both pointers 16-byte aligned, non-overlapping), asynchronous on
  * `stream`.  Its bytes read and written are known exactly, which calibrates hardware

@@ -85,6 +85,7 @@ def _load() -> ctypes.CDLL:
         "hqlss_debug_set_gemm_tile_n": (None, [_int]),
         "hqlss_debug_set_fwd_fp6": (None, [_int]),
         "hqlss_debug_copy": (st, [_vp, _vp, _sz, _vp]),
+        "hqlss_debug_plan_scores_offset": (_sz, [_i64, ctypes.POINTER(_i64)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -470,6 +471,13 @@ def debug_set_gemm_tile_n(bn: int) -> None:
 def debug_set_fwd_fp6(mode: int) -> None:
     """Test hook: hq_linear_fwd's product on FP6 (mode > 0), int8 (< 0) or by size (0)."""
     lib.hqlss_debug_set_fwd_fp6(int(mode))
+
+
+def debug_plan_scores_offset(N: int):
+    """Test hook: (byte offset, pitch) of the leverage scores in lss_grad_plan's workspace."""
+    pitch = ctypes.c_int64(0)
+    off = lib.hqlss_debug_plan_scores_offset(int(N), ctypes.byref(pitch))
+    return int(off), int(pitch.value)
 
 
 def debug_copy(src: torch.Tensor, dst: torch.Tensor) -> None:

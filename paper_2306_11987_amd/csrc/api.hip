@@ -485,6 +485,10 @@ hqlss_status do_bmm_bwd(const void* dT, const hqlss_saved_t* sv, const hqlss_bmm
   return HQLSS_OK;
 }
 
+// do_plan's scratch: the absmax partials, then the scores (lss_grad_plan starts it at the
+// workspace's first byte, so the scores sit at plan_scores_offset() there)
+size_t plan_scores_offset() { return al(sizeof(float) * kQMaxWg); }
+
 hqlss_status do_plan(const void* dY, const hqlss_saved_t* sv, const lss_plan_t* p, int64_t N,
                      int64_t C, int dt, int64_t budget, uint64_t seed, uint64_t offset,
                      Carve& w, hipStream_t s) {
@@ -1114,6 +1118,15 @@ const char* hqlss_kernel_name(int id) { return hqlss::kernel_name(id); }
 void hqlss_debug_set_gemm_splits(int splits) { hqlss::gemm_set_split_override(splits); }
 void hqlss_debug_set_gemm_tile_n(int bn) { hqlss::gemm_set_tile_override(bn); }
 void hqlss_debug_set_fwd_fp6(int mode) { g_fwd_fp6_override = mode > 0 ? 1 : mode < 0 ? -1 : 0; }
+
+size_t hqlss_debug_plan_scores_offset(int64_t N, int64_t* pitch) {
+  if (N < 1) {
+    if (pitch) *pitch = 0;
+    return 0;
+  }
+  if (pitch) *pitch = score_pitch(N);
+  return plan_scores_offset();
+}
 
 hqlss_status hqlss_debug_copy(const void* src, void* dst, size_t bytes, void* stream) {
   if (!src || !dst) return HQLSS_ERR_NULL;

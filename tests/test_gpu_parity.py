@@ -84,6 +84,30 @@ def test_backward_parity(shape, budget_div):
         assert torch.equal(t, dW)
 
 
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"N{s[0]}_D{s[1]}_C{s[2]}_{s[5]}")
+def test_leverage_scores(shape):
+    """The integer leverage scores the bit split writes (both stacked rows of every token)
+    equal the oracle's, bit for bit (Sec. 4.2)."""
+    H = need_gpu()
+    lin, X, W, G = _case(shape, seed=3)
+    N, D, C, k, dt = lin.N, lin.D, lin.C, lin.log2_block, lin.dtype
+    say(f"leverage scores {shape}")
+    saved, _ = run_forward(H, X, W, k, dt)
+    f = O.hq_forward(X, W, k, compute_output=False)
+    b = O.lss_backward(G, f, N, 5, 9, need_dx=False, need_dw=False)
+    plan = H.Plan.empty(N, C)
+    ws = H.workspace(H.WS_PLAN, N, D, C)
+    H.lss_grad_plan(dev_tensor(G, dt), saved, plan, D, N, 5, 9, ws)
+    torch.cuda.synchronize()
+    off, pitch = H.debug_plan_scores_offset(N)
+    raw = to_np(ws)[off:off + 8 * pitch].view(np.uint32)
+    got = np.concatenate([raw[:N], raw[pitch:pitch + N]]).astype(np.int64)
+    su = (b.bs.q_up.astype(np.int64) ** 2).sum(1)
+    sd = (b.bs.q_dn.astype(np.int64) ** 2).sum(1)
+    ref = O.leverage_scores(su, sd, f.x_sumsq)
+    assert np.array_equal(got, ref), "leverage scores"
+
+
 def test_sampling_exercised_and_deterministic():
     """A small budget makes the Bernoulli path live; equal (seed, offset) give identical
     samples, a different offset a different one."""
@@ -158,7 +182,8 @@ def _acc_rows(H, which, plan, saved, N, D, C, rows, shape):
 @pytest.mark.parametrize("case", FULL_SIZE, ids=lambda c: f"w{c[0]}_{synth.workload(c[0]).linears[c[1]].name}")
 def test_full_size_sampled(case):
     """A linear of a named workload at full size, in the configuration the benchmark uses
-    (budget N): the codes of every row and the whole sample bit for bit; whole int32
+    (budget N): the codes of every row, the leverage scores and the whole sample bit for
+    bit; whole int32
     accumulator rows of all three GEMMs (sampled tokens and channels) bit for bit; sampled
     output rows of Y, dX and dW against the oracle computing them one by one."""
     H = need_gpu()
@@ -186,9 +211,20 @@ def test_full_size_sampled(case):
 
     seed, offset = 42, 1000
     b = O.lss_backward(G, f, N, seed, offset, need_dx=False, need_dw=False)
-    _, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N, seed, offset)
+    tG, plan, dX, dW = run_backward(H, G, saved, N, D, C, k, dt, N, seed, offset)
     nk = check_plan(plan, b)
     say(f"  kept {nk}/{N}")
+    # the leverage scores of every stacked row, bit for bit
+    ws = H.workspace(H.WS_PLAN, N, D, C)
+    H.lss_grad_plan(tG, saved, H.Plan.empty(N, C), D, N, seed, offset, ws)
+    torch.cuda.synchronize()
+    off, pitch = H.debug_plan_scores_offset(N)
+    raw = to_np(ws)[off:off + 8 * pitch].view(np.uint32)
+    su = (b.bs.q_up.astype(np.int64) ** 2).sum(1)
+    sd = (b.bs.q_dn.astype(np.int64) ** 2).sum(1)
+    assert np.array_equal(np.concatenate([raw[:N], raw[pitch:pitch + N]]).astype(np.int64),
+                          O.leverage_scores(su, sd, f.x_sumsq)), "leverage scores"
+    del ws, tG
     A = b.A.astype(np.float64)
     kept = b.plan.kept
     a_dx, a_dw = b.alpha_dx, b.alpha_dw
