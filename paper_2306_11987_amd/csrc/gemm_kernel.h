@@ -568,6 +568,10 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     if (st + C_::NBUF - 1 < nst) issue(st + C_::NBUF - 1);
     if (st == 0) prefetch_delta();
   };
+  // The main loop runs at wave priority 1 and the epilogue at 0: when the two workgroups
+  // of a CU share a SIMD, the one feeding the matrix core wins the issue slots over the
+  // other's conversion and Hadamard arithmetic.
+  __builtin_amdgcn_s_setprio(1);
   if constexpr (F6) {
     // FP6 main loop: one stage is one 64-k MFMA step.  A lane's fragment of a row is the
     // 32-byte group of its 32 k (24 bytes of fields, then the 8 zero bytes the instruction
@@ -789,6 +793,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
   }
   wait_vm_lgkm0<0>();
   __builtin_amdgcn_s_barrier();  // every wave is done with the stage buffers
+  __builtin_amdgcn_s_setprio(0);
 
   // ---------------------------------------------------------------- epilogue
   // values of (i, j): row m = wm*WM + 32 i + (lane % 32), columns n = wn*WN + 16 j +
