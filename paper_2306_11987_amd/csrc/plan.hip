@@ -9,7 +9,9 @@
 //   1. inclusion probabilities by the clamp-and-rescale loop of App. A.2 with sum p = B,
 //      in exact integers.  Thresholds S/R only fall from one round to the next, so the
 //      rows clamped after a round are exactly {c > 0 : R c >= S} for that round's (R, S):
-//      each round is one pass over the scores and needs no per-row state.  If no more
+//      a round needs that set's count and sum, and no per-row state (the 1024-thread
+//      build takes them from scores binned once, the 256-thread one from a pass over
+//      the scores).  If no more
 //      than B rows have c > 0, every such row has p = 1 (the "keep rows with norm > 0"
 //      rule of the paper's implementation, App. A.6);
 //   2. upper rows are kept iff non-zero; a lower row with p* < 1 gets p~ = 2^-e >= p*, the
@@ -84,6 +86,17 @@ __device__ __forceinline__ void block_sum2_u64(uint64_t& a, uint64_t& b, uint64_
   }
 }
 
+// Score bins of the 1024-thread sampler's clamp-and-rescale rounds: 32 per octave (the
+// position of the leading one, then the next five bits), so the bin never decreases with
+// the score: a score in a bin above the threshold's bin is at least the threshold, one in
+// a bin below it is smaller, and only the threshold's own bin needs comparisons.
+constexpr int kHistBins = 1024;
+__device__ __forceinline__ int score_bin(uint32_t c) {  // c > 0
+  const int e = 31 - __builtin_clz(c);
+  const uint32_t m = e >= 5 ? (c >> (e - 5)) : (c << (5 - e));
+  return e * 32 + (int)(m & 31u);
+}
+
 // 8 consecutive words from p + t0 (n8 of them valid, the rest 0).
 __device__ __forceinline__ void load8u(const uint32_t* p, int t0, int n8, uint32_t v[8]) {
   if (n8 == 8) {
@@ -105,6 +118,17 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
   constexpr int kPlanWaves = kPlanThreads / kWave;
   __shared__ uint64_t red[4 * kPlanWaves];  // two buffers of block_sum2_u64
   __shared__ int wtot[kPlanWaves];
+  // the 1024-thread sampler runs its rounds on binned scores (below): per-bin counts (then
+  // the end of each bin's bucket), first slots and sums (then the sums of the bins above),
+  // and the non-zero scores bucketed by bin, highest bin first (128 KB of LDS)
+  constexpr bool kHist = kPlanThreads == 1024;
+  constexpr int kHistCap = kHist ? kPlanRegs * kPlanThreads : 1;
+  static_assert(!kHist || kHistBins == kPlanThreads, "one bin per thread in the scan");
+  __shared__ uint32_t h_end[kHist ? kHistBins : 1];
+  __shared__ uint32_t h_off[kHist ? kHistBins : 1];
+  __shared__ uint64_t h_sum[kHist ? kHistBins : 1];
+  __shared__ uint32_t h_score[kHistCap];
+  __shared__ uint64_t h_rs[2];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   {  // workgroup b samples batch b of a batched call (its own inputs, outputs and counters)
     const int64_t bt = blockIdx.x;
@@ -142,49 +166,145 @@ __global__ __launch_bounds__(kPlanThreads) void lss_plan_kernel(
       const int64_t i = tid + (int64_t)j * kPlanThreads;
       cs[j] = (in_regs && i < n2) ? scores[i < N ? i : pitch + (i - N)] : 0u;
     }
-    int64_t k = 0;
-    int par = 1;
-    for (;;) {
-      R = B - k;
-      // R c >= S  <=>  c >= ceil(S / R) for integers and R > 0: one division per round
-      // instead of a 64-bit product per score.  S = 0 admits every non-zero score (as
-      // R c >= 0 does); R = 0 with S > 0 admits none.
-      const uint64_t T = S == 0 ? 1 : R <= 0 ? ~uint64_t(0) : (S + (uint64_t)R - 1) / (uint64_t)R;
-      // T >= 1, so c >= T implies c > 0; a threshold past the 32-bit scores admits none
-      const uint32_t T32 = (uint32_t)T;
-      uint32_t n = 0;
-      uint64_t sum = 0;
-      if (T > 0xFFFFFFFFull) {  // uniform
-      } else if (in_regs) {
+    if (kHist && in_regs) {
+      // The same rounds on binned scores.  One pass builds each bin's count and sum, a
+      // scan from the top bin down gives the count and sum of all bins above each bin,
+      // and a second pass places the scores in per-bin buckets.  A round then takes the
+      // bins above its threshold's bin from the scan and compares only the threshold's
+      // own bin, in one wave: the rounds' counts and sums, and so their sequence, are
+      // those of the full passes.
+      for (int b = tid; b < kHistBins; b += kPlanThreads) {
+        h_end[b] = 0;
+        h_sum[b] = 0;
+      }
+      __syncthreads();
 #pragma unroll
-        for (int j = 0; j < kPlanRegs; ++j) {
-          const uint32_t c = cs[j];
-          const bool in = c >= T32;
-          n += in;
-          sum += in ? c : 0u;
+      for (int j = 0; j < kPlanRegs; ++j)
+        if (cs[j]) {
+          const int b = score_bin(cs[j]);
+          atomicAdd(&h_end[b], 1u);
+          atomicAdd(reinterpret_cast<unsigned long long*>(&h_sum[b]), (unsigned long long)cs[j]);
         }
-      } else {  // eight loads in flight per thread
-        for (int64_t i0 = tid; i0 < n2; i0 += 8 * (int64_t)kPlanThreads) {
-          uint32_t c8[8];
+      __syncthreads();
+      const int hb = kHistBins - 1 - tid;  // thread t scans bin 1023 - t
+      const uint32_t c0 = h_end[hb];
+      const uint64_t s0 = h_sum[hb];
+      uint32_t ci = c0;
+      uint64_t si = s0;
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int64_t i = i0 + (int64_t)u * kPlanThreads;
-            c8[u] = i < n2 ? scores[i < N ? i : pitch + (i - N)] : 0u;
-          }
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const bool in = c8[u] >= T32;
-            n += in;
-            sum += in ? c8[u] : 0u;
-          }
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t cy = __shfl_up(ci, o);
+        const uint32_t lo = __shfl_up((uint32_t)si, o), hi = __shfl_up((uint32_t)(si >> 32), o);
+        if (lane >= o) {
+          ci += cy;
+          si += ((uint64_t)hi << 32) | lo;
         }
       }
-      uint64_t cnt = n;
-      block_sum2_u64<kPlanWaves>(cnt, sum, red + 2 * kPlanWaves * par);
-      par ^= 1;
-      if ((int64_t)cnt == k) break;  // nothing newly clamped
-      k = (int64_t)cnt;
-      S = S_all - sum;
+      // red: its last reads (the totals above) came before the barriers since
+      if (lane == 63) {
+        red[wid] = ci;
+        red[kPlanWaves + wid] = si;
+      }
+      __syncthreads();
+      uint32_t cpre = 0;
+      uint64_t spre = 0;
+#pragma unroll
+      for (int i = 0; i < kPlanWaves; ++i)
+        if (i < wid) {
+          cpre += (uint32_t)red[i];
+          spre += red[kPlanWaves + i];
+        }
+      const uint32_t above = cpre + ci - c0;  // scores in the bins above hb
+      h_off[hb] = above;
+      h_end[hb] = above;  // the bucket's fill cursor, then its end
+      h_sum[hb] = spre + si - s0;
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < kPlanRegs; ++j)
+        if (cs[j]) h_score[atomicAdd(&h_end[score_bin(cs[j])], 1u)] = cs[j];
+      __syncthreads();
+      if (wid == 0) {  // the rounds, in one wave (uniform)
+        int64_t k = 0, Rr = B;
+        uint64_t Sr = S_all;
+        // the count grows every round that does not stop, so at most 2N + 1 rounds run;
+        // the bound only makes that certain
+        for (int64_t round = 0; round <= n2; ++round) {
+          Rr = B - k;
+          const uint64_t T = Sr == 0 ? 1 : Rr <= 0 ? ~uint64_t(0) : (Sr + (uint64_t)Rr - 1) / (uint64_t)Rr;
+          uint64_t cnt = 0, sum = 0;
+          if (T <= 0xFFFFFFFFull) {  // else no score reaches it
+            const uint32_t T32 = (uint32_t)T;
+            const int b = score_bin(T32);
+            const uint32_t end = h_end[b];
+            uint32_t n = 0;
+            uint64_t sm = 0;
+            for (uint32_t i = h_off[b] + lane; i < end; i += 64) {
+              const uint32_t c = h_score[i];
+              if (c >= T32) {
+                ++n;
+                sm += c;
+              }
+            }
+            cnt = (uint64_t)h_off[b] + wave_sum_u32_dpp(n);
+            sum = h_sum[b] + wave_sum_u64_dpp(sm);
+          }
+          if ((int64_t)cnt == k) break;  // nothing newly clamped
+          k = (int64_t)cnt;
+          Sr = S_all - sum;
+        }
+        if (lane == 0) {
+          h_rs[0] = (uint64_t)Rr;
+          h_rs[1] = Sr;
+        }
+      }
+      __syncthreads();
+      R = (int64_t)h_rs[0];
+      S = h_rs[1];
+    } else {  // full passes (256-thread sampler, or 2N beyond the register-held scores)
+      int64_t k = 0;
+      int par = 1;
+      for (;;) {
+        R = B - k;
+        // R c >= S  <=>  c >= ceil(S / R) for integers and R > 0: one division per round
+        // instead of a 64-bit product per score.  S = 0 admits every non-zero score (as
+        // R c >= 0 does); R = 0 with S > 0 admits none.
+        const uint64_t T = S == 0 ? 1 : R <= 0 ? ~uint64_t(0) : (S + (uint64_t)R - 1) / (uint64_t)R;
+        // T >= 1, so c >= T implies c > 0; a threshold past the 32-bit scores admits none
+        const uint32_t T32 = (uint32_t)T;
+        uint32_t n = 0;
+        uint64_t sum = 0;
+        if (T > 0xFFFFFFFFull) {  // uniform
+        } else if (in_regs) {
+#pragma unroll
+          for (int j = 0; j < kPlanRegs; ++j) {
+            const uint32_t c = cs[j];
+            const bool in = c >= T32;
+            n += in;
+            sum += in ? c : 0u;
+          }
+        } else {  // eight loads in flight per thread
+          for (int64_t i0 = tid; i0 < n2; i0 += 8 * (int64_t)kPlanThreads) {
+            uint32_t c8[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int64_t i = i0 + (int64_t)u * kPlanThreads;
+              c8[u] = i < n2 ? scores[i < N ? i : pitch + (i - N)] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const bool in = c8[u] >= T32;
+              n += in;
+              sum += in ? c8[u] : 0u;
+            }
+          }
+        }
+        uint64_t cnt = n;
+        block_sum2_u64<kPlanWaves>(cnt, sum, red + 2 * kPlanWaves * par);
+        par ^= 1;
+        if ((int64_t)cnt == k) break;  // nothing newly clamped
+        k = (int64_t)cnt;
+        S = S_all - sum;
+      }
     }
   }
 

@@ -267,15 +267,17 @@ def test_sampler_max_tokens():
     check_float_output("dW", dW, b.dW, dt)
 
 
-@pytest.mark.parametrize("N", [3000, 6000, 12000, 16384])
-def test_sampler_clamp_sizes(N):
+@pytest.mark.parametrize("N,kind", [(3000, "lognormal"), (6000, "lognormal"), (12000, "lognormal"),
+                                    (16384, "lognormal"), (16384, "pareto"), (12000, "sparse_rows")])
+def test_sampler_clamp_sizes(N, kind):
     """The clamp-and-rescale loop live (budget N/4) on both sides of the sampler's size
-    limits: the 256-thread build (N <= 4096) and the 1024-thread one; one or two
-    compaction rounds (N > 8192); up to the largest N whose scores the clamp rounds hold
-    in registers (2N = 32768; test_sampler_max_tokens covers the memory path).  Plan and
-    both gradients against the oracle."""
+    limits: the 256-thread build (N <= 4096, full passes over the scores) and the
+    1024-thread one (binned scores); one or two compaction rounds (N > 8192); up to the
+    largest N whose scores the clamp rounds hold in registers (2N = 32768;
+    test_sampler_max_tokens covers the memory path).  Heavy-tailed and sparse rows put many
+    scores in few bins.  Plan and both gradients against the oracle."""
     H = need_gpu()
-    lin, X, W, G = _case((N, 64, 128, 5, "f16", "lognormal"), seed=N)
+    lin, X, W, G = _case((N, 64, 128, 5, "f16", kind), seed=N)
     D, C, k, dt = lin.D, lin.C, lin.log2_block, lin.dtype
     say(f"sampler clamp at N={N}")
     saved, _ = run_forward(H, X, W, k, dt)
