@@ -476,49 +476,53 @@ __global__ __launch_bounds__(256) void build_operands_kernel(
   if (isA ? !Ag : !XtT) return;
   const int64_t col0 = isA ? (int64_t)blockIdx.y * kBC : ((int64_t)blockIdx.y - cb) * kBC;
   const int64_t ncol = isA ? C : D;
-  // 128 kept rows x 8 chunks of 16 columns, four per thread
+  // 128 kept rows x 4 chunks of 32 columns, two per thread: 16-byte loads of the code rows
+  if (isA) {  // uniform: A_t is written row-major straight from registers
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int item = tid + 256 * k, r = item >> 3, q = (item & 7) * 16;
-    const int64_t i = i0 + r;
-    const bool inside = col0 + q < ncol;  // the last block of a 64-multiple width
-    int v[16];
+    for (int k = 0; k < 2; ++k) {
+      const int item = tid + 256 * k, r = item >> 2, q = (item & 3) * 32;
+      const int64_t i = i0 + r;
+      if (col0 + q >= ncol) continue;  // the last block of a 64-multiple width
+      int v[32];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) v[j] = 0;
-    if (i < nk && inside) {
-      const int64_t t = kept[i];
-      if (isA) {
+      for (int j = 0; j < 32; ++j) v[j] = 0;
+      if (i < nk) {  // rows past the kept count are the zero padding up to 128
+        const int64_t t = kept[i];
         const int wu = w_up[t], wd = w_dn[t];
-        const uint2 up = ld_stream2<HQ_NT_B_LD>(qup + t * (C / 2) + (col0 + q) / 2);
-        const uint2 dn = ld_stream2<HQ_NT_B_LD>(qdn + t * (C / 2) + (col0 + q) / 2);
+        const uint4 up = ld_stream<HQ_NT_B_LD>(qup + t * (C / 2) + (col0 + q) / 2);
+        const uint4 dn = ld_stream<HQ_NT_B_LD>(qdn + t * (C / 2) + (col0 + q) / 2);
         weighted8(up.x, dn.x, wu, wd, v);
         weighted8(up.y, dn.y, wu, wd, v + 8);
-      } else {
-        const uint2 x = ld_stream2<HQ_NT_B_LD>(xq + t * (D / 2) + (col0 + q) / 2);
+        weighted8(up.z, dn.z, wu, wd, v + 16);
+        weighted8(up.w, dn.w, wu, wd, v + 24);
+      }
+      const uint2 a0 = interleave8(v), a1 = interleave8(v + 8), a2 = interleave8(v + 16),
+                  a3 = interleave8(v + 24);
+      st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q, make_uint4(a0.x, a0.y, a1.x, a1.y));
+      st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q + 16, make_uint4(a2.x, a2.y, a3.x, a3.y));
+    }
+    return;
+  }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          v[j] = sext4((x.x >> (4 * j)) & 15u);
-          v[8 + j] = sext4((x.y >> (4 * j)) & 15u);
-        }
-      }
-    }
-    if (isA) {
-      if (inside) {
-        const uint2 lo = interleave8(v), hi = interleave8(v + 8);
-        st_stream<HQ_NT_B_ST>(Ag + i * C + col0 + q, make_uint4(lo.x, lo.y, hi.x, hi.y));
-      }
-      continue;
-    }
+  for (int k = 0; k < 2; ++k) {
+    const int item = tid + 256 * k, r = item >> 2, q = (item & 3) * 32;
+    const int64_t i = i0 + r;
+    uint4 x = make_uint4(0u, 0u, 0u, 0u);
+    if (i < nk && col0 + q < ncol) x = ld_stream<HQ_NT_B_LD>(xq + kept[i] * (D / 2) + (col0 + q) / 2);
     // word w of row r sits at word w ^ ((r / 16) % 8) of the row: the transpose below reads
     // one column of 8 row blocks at once, which would otherwise fall on 4 banks
     uint32_t* tp = reinterpret_cast<uint32_t*>(&tile[r][0]);  // 4-byte aligned: pitch 132
     const int sw = (r >> 4) & 7;
+    const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
-      tp[(q / 4 + w) ^ sw] = ((uint32_t)v[4 * w] & 0xFFu) | (((uint32_t)v[4 * w + 1] & 0xFFu) << 8) |
-                             (((uint32_t)v[4 * w + 2] & 0xFFu) << 16) | (((uint32_t)v[4 * w + 3] & 0xFFu) << 24);
+    for (int w = 0; w < 8; ++w) {  // bytes 4 w .. 4 w + 3 of the chunk: one code each
+      const uint32_t c4 = xw[w >> 1] >> (16 * (w & 1));
+      uint32_t b = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b |= ((uint32_t)sext4((c4 >> (4 * j)) & 15u) & 0xFFu) << (8 * j);
+      tp[(q / 4 + w) ^ sw] = b;
+    }
   }
-  if (isA) return;  // uniform: A_t needs no transpose
   __syncthreads();
   // 128 columns x 8 chunks of 16 kept indices, four per thread
 #pragma unroll
