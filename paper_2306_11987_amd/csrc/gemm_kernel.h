@@ -805,7 +805,9 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
     // sum of acc * delta over this workgroup's valid entries, then the clip mask (App. A.3):
     // both use the integer accumulator before the transform H^T.  Rows past M hold
     // re-read data and are skipped; N is a multiple of the block, so the mask never mixes
-    // valid and invalid columns inside one transform.
+    // valid and invalid columns inside one transform.  Four partial sums (by r % 4) keep
+    // the fp64 additions out of one dependent chain; each product is exact in fp64.
+    double part[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
       const int64_t gm = m0 + wm * C_::WM + 32 * i + ml;
@@ -821,11 +823,12 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
         for (int r = 0; r < 16; ++r) {
           const uint32_t h = (dw[r >> 1] >> (16 * (r & 1))) & 0xFFFFu;
           const int a = acc[i][j][r];
-          lsq_sum += (double)(a >> C_::SHIFT) * f16_bits_to_double(h);
+          part[r & 3] = __builtin_fma((double)(a >> C_::SHIFT), f16_bits_to_double(h), part[r & 3]);
           acc[i][j][r] = inside_of(h) ? a : 0;
         }
       }
     }
+    lsq_sum = (part[0] + part[1]) + (part[2] + part[3]);
   }
   if constexpr (GRAD) {
 #pragma unroll
