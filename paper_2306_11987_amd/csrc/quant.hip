@@ -127,13 +127,18 @@ __device__ __forceinline__ uint3 fp6_half16(const uint32_t y[16]) {
   return make_uint3((uint32_t)w[0], (uint32_t)w[1], (uint32_t)w[2]);
 }
 
-// Store the FP6 fields of 16-code chunk c of a row (row base `row6`, padded layout): the
-// even chunk of a group fills bytes 0..11, the odd one bytes 12..23 and the 8 zero bytes.
-__device__ __forceinline__ void store_fp6_chunk(uint8_t* row6, int64_t c, const uint32_t y[16]) {
+// The 16 bytes lane pair (2g, 2g + 1) stores of 32-code group g of a row in the padded FP6
+// layout: the even chunk's fields fill bytes 0..11, the odd one's bytes 12..23, then 8 zero
+// bytes.  The even lane takes bytes 0..15 (the first word of its partner's fields comes
+// over), the odd lane bytes 16..31, so both store one aligned 16-byte piece.  Lanes 2g and
+// 2g + 1 must hold chunks 2g and 2g + 1 and both be active.
+__device__ __forceinline__ uint4 fp6_chunk16(const uint32_t y[16], bool odd) {
   const uint3 f = fp6_half16(y);
-  uint8_t* p = row6 + (c >> 1) * 32 + (c & 1) * 12;
-  *reinterpret_cast<uint3*>(p) = f;
-  if (c & 1) *reinterpret_cast<uint2*>(p + 12) = make_uint2(0u, 0u);
+  const uint32_t partner = (uint32_t)__shfl_xor((int)f.x, 1);
+  return odd ? make_uint4(f.y, f.z, 0u, 0u) : make_uint4(f.x, f.y, f.z, partner);
+}
+__device__ __forceinline__ void store_fp6_chunk(uint8_t* row6, int64_t c, const uint4& v) {
+  *reinterpret_cast<uint4*>(row6 + (c >> 1) * 32 + (c & 1) * 16) = v;
 }
 
 // Pack 8 codes given as rne_bits (low nibbles) into one word, element j at bits 4j.
@@ -324,10 +329,11 @@ __device__ void quant_tile(const void* src, int64_t rows, int64_t cols, float in
       dh[e / 2] = h[0] | (h[1] << 16);
     }
     const int64_t c = (c0 + sub * kVE) / kVE;  // 16-column chunk of the row
+    const uint4 f6 = fp6 ? fp6_chunk16(y, (c & 1) != 0) : make_uint4(0u, 0u, 0u, 0u);  // all lanes
     if (ok) {
       st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(packed + r * (cols / 2)) + c,
                              make_uint2(pack8_bits(y), pack8_bits(y + 8)));
-      if (fp6) store_fp6_chunk(fp6 + r * cols, c, y);
+      if (fp6) store_fp6_chunk(fp6 + r * cols, c, f6);
       if constexpr (LSQ) {
         uint4* dp = reinterpret_cast<uint4*>(delta + r * cols) + 2 * c;
         st_stream<HQ_NT_Q_ST>(dp, make_uint4(dh[0], dh[1], dh[2], dh[3]));
@@ -401,7 +407,11 @@ __global__ __launch_bounds__(kQThreads) void fwht_quant_kernel(QJob j0, QJob j1,
         const bool ok = g.valid(kp);
         const int64_t r = g.row_of(kp);
         if (ok) st_stream2<HQ_NT_Q_ST>(reinterpret_cast<uint2*>(o.packed + r * (j.cols / 2)) + (int64_t)ip * g.G + g.sub, make_uint2(w0, w1));
-        if (ok && o.fp6) store_fp6_chunk(o.fp6 + r * j.cols, (int64_t)ip * g.G + g.sub, y);
+        if (o.fp6) {  // the pair exchange runs in every lane, the store only in valid rows
+          const int64_t c = (int64_t)ip * g.G + g.sub;
+          const uint4 f6 = fp6_chunk16(y, (c & 1) != 0);
+          if (ok) store_fp6_chunk(o.fp6 + r * j.cols, c, f6);
+        }
         if (++ip == g.iters) {  // end of the group's row
           if (o.row_sumsq) {
             ss = group_sum(ss, g.G);
