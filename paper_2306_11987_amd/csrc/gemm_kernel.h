@@ -258,16 +258,21 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
   constexpr bool ROWMAP = (EPI == kEpiDx || EPI == kEpiDxL);  // rows scatter through out_rows
   constexpr int ES = (RAW || DT == kF32) ? 4 : 2;
   constexpr int E_PITCH = BN * ES + 16;
-  constexpr int E_ROWS = (BM * E_PITCH <= C_::LDS_MAIN) ? BM
-                         : (BM / 2 * E_PITCH <= C_::LDS_MAIN) ? BM / 2
-                         : (BM / 4 * E_PITCH <= C_::LDS_MAIN) ? BM / 4 : BM / 8;
-  static_assert(E_ROWS >= 32 && E_ROWS * E_PITCH <= C_::LDS_MAIN, "epilogue staging");
+  // Two workgroups per CU leave up to 80 KB of LDS each: the epilogue stages all BM rows in
+  // one round when they fit there, even past the stage buffers (the 128 x 256 gradient
+  // tiles with 2-byte outputs: 66 KB against 64 KB of stages).
+  constexpr int SMEM = (C_::OCC == 2 && BM * E_PITCH > C_::LDS_MAIN && BM * E_PITCH <= 78 * 1024)
+                           ? BM * E_PITCH : C_::LDS_MAIN;
+  constexpr int E_ROWS = (BM * E_PITCH <= SMEM) ? BM
+                         : (BM / 2 * E_PITCH <= SMEM) ? BM / 2
+                         : (BM / 4 * E_PITCH <= SMEM) ? BM / 4 : BM / 8;
+  static_assert(E_ROWS >= 32 && E_ROWS * E_PITCH <= SMEM, "epilogue staging");
   static_assert(!(F6 && LSQ), "the learned-step epilogues run on the int8 route");
   static_assert(!TRA || (!A4 && !F6 && !ROWMAP && C_::RA == 128 && C_::KS == 128),
                 "k-major A: int8 A, 128-byte rows of 128 k per stage, plain output rows");
   // result row of tile row gm (k-major A: the K-interleaved position gm)
   auto res_row = [](int64_t gm) -> int64_t { return TRA ? ((gm & ~int64_t(7)) | nu8((int)(gm & 7))) : gm; };
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[C_::LDS_MAIN];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63;
   // wave index as a scalar: the LDS-DMA destinations (M0) then need no lane-to-scalar moves
