@@ -532,7 +532,7 @@ __global__ __launch_bounds__((Cfg<BM, A4, WN, BN_, F6>::THREADS), (Cfg<BM, A4, W
 #pragma unroll
     for (int q = 0; q < TI * TJ; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // up to 5 VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // up to 3 VALU
       __builtin_amdgcn_sched_group_barrier(0x100, TRA ? 2 : 1, 0);  // LDS reads
     }
   };
